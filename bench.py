@@ -1,0 +1,203 @@
+"""Benchmark of the retrieval-drafted verify step on one MI355X.
+
+A step is one decoding iteration: draft lookup -> verify forward (all layers,
+lm_head, greedy accept) -> KV commit, on seeded synthetic inputs already
+resident in HBM. The cache length and context are reset after every commit
+so the cached prefix P stays fixed. Default workload: the 3B-class bf16
+decoder, K = 16 linear draft over a 4096-token prefix.
+
+Prints one JSON line. `value` is achieved HBM bandwidth of the whole step:
+algorithmic bytes (every weight once + the KV prefix read + the draft rows'
+KV read and written) divided by the measured step time.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "verify-step latency (ms) + achieved HBM GB/s vs peak; accepted tokens/sec"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def gate_up_bytes(wl) -> int:
+    m = wl.model
+    esz = 2 if m.dtype == "bf16" else 4
+    M = wl.rows
+    return esz * (2 * m.ffn * m.hidden + M * m.hidden + M * m.ffn)
+
+
+def cpu_baseline(wl, w, kv_host, draft, layers: int):
+    """The oracle's batched verify, timed on this host's cores, on a sample:
+    the first `layers` layers at full widths plus the full lm_head, same
+    prefix and rows. Scaled to GB/s with the sample's own algorithmic bytes."""
+    import oracle
+
+    shape = wl.model.with_layers(layers)
+    ws = dict(w)
+    for k in ("wqkv", "wo", "wgu", "wd", "attn_norm", "ffn_norm"):
+        ws[k] = w[k][:layers]
+    kvs = kv_host[:layers]
+    om = oracle.Model(shape, ws)
+    t0 = time.perf_counter()
+    oracle.verify_batched(om, kvs, draft, wl.rows, wl.tree, want_logits=False)
+    dt = time.perf_counter() - t0
+    sample_wl = synth.Workload(wl.name, wl.index, shape, wl.prefix, wl.k_max, wl.ngram, wl.tree,
+                               wl.n_cand, wl.max_nodes, wl.store_seqs, wl.store_len,
+                               wl.store_tokens, wl.planted)
+    nbytes = sample_wl.verify_bytes()
+    return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"one batched verify of {wl.rows} rows over P={wl.prefix} with the first "
+                      f"{layers} of {wl.model.n_layers} layers at full width plus the full "
+                      f"lm_head ({nbytes / 1e9:.2f} GB algorithmic), {dt:.1f} s",
+            "seconds": round(dt, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="3b", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--profile-steps", type=int, default=5)
+    ap.add_argument("--cpu-layers", type=int, default=0, help="0: every layer")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
+              f"sharding of this path is a design note, not a measured configuration",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_32166_amd as pf
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    shape = wl.model
+    seed = synth.case_seed(wl, 0)
+    t0 = time.perf_counter()
+    w = synth.make_weights(shape, seed)
+    kv_host = synth.make_kv_prefix(shape, seed, wl.prefix)
+    store = synth.make_store(wl, seed)
+    ctx, info = synth.make_context(wl, seed, store, hit=True)
+    log(f"inputs generated in {time.perf_counter() - t0:.1f} s (hit={info['hit']})")
+
+    t0 = time.perf_counter()
+    wdev = pf.weights_to_device(w, shape.dtype)
+    model = pf.pf_model_create(pf.model_config(shape), wdev)
+    del wdev
+    torch.cuda.empty_cache()
+    cap = ((wl.prefix + 2 * wl.rows + 63) // 64) * 64
+    kv = pf.KVCache(model, cap)
+    kvd = pf.array_to_device(kv_host)
+    pf.pf_kv_import(kv, kvd, wl.prefix)
+    st = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
+    c = pf.Context(ctx, len(ctx) + 2 * wl.rows)
+    draft, res = pf.new_draft(), pf.new_result()
+    torch.cuda.synchronize()
+    del kvd
+    log(f"model {model.bytes / 1e9:.2f} GB on device, set up in {time.perf_counter() - t0:.1f} s")
+
+    max_nodes = wl.max_nodes if wl.tree else 64
+    n_cand = wl.n_cand if wl.tree else 1
+
+    def step():
+        pf.pf_kv_set_len(kv, wl.prefix)
+        pf.pf_context_init(c, len(ctx))
+        pf.pf_draft_lookup(st, c, wl.k_max, wl.tree, n_cand, max_nodes, draft)
+        pf.pf_verify_step(model, kv, draft, wl.rows, wl.tree, None, res)
+        pf.pf_kv_commit(kv, res, c)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    r = pf.read_result(res)
+    d = pf.read_draft(draft)
+    log(f"step {ms:.3f} ms, draft {int(d['n_nodes']) - 1} tokens, accepted {int(r['accept_len'])}")
+
+    # per-kernel durations (event pairs around every launch)
+    tot = np.zeros(pf.PF_PROF_KINDS)
+    cnt = np.zeros(pf.PF_PROF_KINDS, np.int64)
+    for _ in range(args.profile_steps):
+        pf.pf_kv_set_len(kv, wl.prefix)
+        pf.pf_context_init(c, len(ctx))
+        pf.pf_draft_lookup(st, c, wl.k_max, wl.tree, n_cand, max_nodes, draft)
+        m_, c_ = pf.pf_verify_step_profiled(model, kv, draft, wl.rows, wl.tree, None, res)
+        tot += m_
+        cnt += c_
+    kernels = {}
+    for i, name in enumerate(pf.PROF_NAMES):
+        if cnt[i]:
+            kernels[name] = {"ms_per_step": round(tot[i] / args.profile_steps, 4),
+                             "avg_launch_us": round(1000 * tot[i] / cnt[i], 2),
+                             "launches_per_step": int(cnt[i] // args.profile_steps)}
+    gu_us = 1000 * tot[6] / max(1, cnt[6])
+    gu_gbs = gate_up_bytes(wl) / (gu_us * 1e-6) / 1e9
+    nbytes = wl.verify_bytes()
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    K = wl.k_max
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape.dtype,
+        "data": "synthetic (seeded random-init weights N(0,0.02), N(0,1) KV prefix, Zipf(1.1) store)",
+        "config": {"workload": f"{wl.name}: {shape.n_layers}L H{shape.hidden} "
+                               f"{shape.n_heads}q/{shape.n_kv_heads}kv hd{shape.head_dim} "
+                               f"F{shape.ffn} V{shape.vocab}, P={wl.prefix}, K={K} "
+                               f"{'tree' if wl.tree else 'linear'}, {wl.ngram}-gram lookup",
+                   "rows": wl.rows, "prefix": wl.prefix, "k_max": K,
+                   "algorithmic_bytes_per_step": nbytes},
+        "hbm_frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "accepted_tokens_per_s": {f"l_acc={l}": round((l + 1) / (ms * 1e-3), 1)
+                                  for l in (0, K // 2, K)},
+        "roofline": {"bound": "hbm", "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "k_gemm<bf16,*,EPI_SWIGLU> (gate/up projection + SwiGLU)",
+                     "bytes_per_launch": gate_up_bytes(wl),
+                     "avg_launch_us": round(gu_us, 2)},
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        od = {"n_nodes": int(d["n_nodes"]), "token": np.array(d["token"][:int(d["n_nodes"])]),
+              "parent": np.array(d["parent"][:int(d["n_nodes"])]),
+              "depth": np.array(d["depth"][:int(d["n_nodes"])])}
+        log("timing the oracle on the host ...")
+        nl = args.cpu_layers if args.cpu_layers > 0 else shape.n_layers
+        out["cpu_baseline"] = cpu_baseline(wl, w, kv_host, od, min(nl, shape.n_layers))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,306 @@
+/*
+ * pf.h -- C ABI of the retrieval-drafted verify step for MI355X (gfx950).
+ *
+ * One decoding iteration of Experience-Guided Adaptive Decoding (arXiv
+ * 2609.32166, Section 3.2) is
+ *     pf_draft_lookup -> pf_verify_step -> pf_kv_commit
+ * on one HIP stream, with every input and output resident in device memory
+ * and no host synchronisation between the calls. pf_prefill covers the
+ * prompt-prefix carryover of Section 3.4 (resume after a reused prefix).
+ *
+ * Conventions
+ *  - Every call returns a pf_status and never throws. On error the message
+ *    of pf_last_error() (thread-local, valid until the next pf_* call on the
+ *    thread) says what was wrong.
+ *  - Argument errors are detected on the host before anything is launched.
+ *  - "device" pointers are HIP device memory of the current device; "host"
+ *    pointers are ordinary process memory read during the call only.
+ *  - Work is enqueued on the caller's stream (a hipStream_t passed as
+ *    pf_stream; NULL is the legacy default stream). Outputs are valid after
+ *    the stream has been synchronised.
+ *  - The caller owns every pointer it passes; the library owns the handles
+ *    it creates (pf_store, pf_model) and frees them in the destroy calls.
+ *  - pf_draft_lookup, pf_verify_step and pf_kv_commit allocate nothing and
+ *    do not synchronise: the step can be captured into a HIP graph. A model
+ *    holds one set of step work buffers, so steps on one model must not
+ *    overlap (serialise them on one stream).
+ */
+#ifndef PF_H
+#define PF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t pf_status;
+#define PF_OK 0
+#define PF_EINVAL (-1)       /* bad argument (null pointer, size out of range) */
+#define PF_ENOMEM (-2)       /* device allocation failed (create calls only) */
+#define PF_EHIP (-3)         /* a HIP runtime call failed */
+#define PF_ECAPACITY (-4)    /* KV cache or context capacity would be exceeded */
+#define PF_ESTATE (-5)       /* object in the wrong state for the call */
+#define PF_EUNSUPPORTED (-6) /* shape or dtype this build does not handle */
+
+#define PF_DTYPE_F32 0
+#define PF_DTYPE_BF16 1
+
+/* The proposal length is capped at 64 (Section 4, "Memory and retrieval");
+ * a draft holds the current token plus at most 64 proposal tokens. */
+#define PF_MAX_DRAFT 64
+#define PF_MAX_NODES 65
+#define PF_MAX_CAND 4
+#define PF_MAX_TREE_NODES 63 /* non-root nodes of a tree draft */
+
+typedef void *pf_stream; /* hipStream_t */
+
+typedef struct pf_store pf_store;
+typedef struct pf_model pf_model;
+
+const char *pf_last_error(void);
+const char *pf_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Draft record (device memory, written by pf_draft_lookup)                  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Node 0 is the current token (the last context token). Linear drafts are a
+ * chain: node i (1 <= i < n_nodes) is proposal token i, parent i-1, depth i.
+ * Tree drafts merge up to PF_MAX_CAND proposals into a prefix-shared token
+ * trie; anc[i] has bit u set for every ancestor-or-self u of node i.
+ */
+typedef struct pf_draft {
+  int32_t n_nodes;   /* 1 + number of proposal tokens (1: no proposal) */
+  int32_t tree;      /* 1 if built as a tree */
+  int32_t n_found;   /* candidates returned (0..n_cand) */
+  int32_t n_eligible;/* eligible store entries seen for the query */
+  int32_t token[PF_MAX_NODES];
+  int32_t parent[PF_MAX_NODES]; /* -1 for the root */
+  int32_t depth[PF_MAX_NODES];
+  int32_t reserved0;
+  uint64_t anc[PF_MAX_NODES];
+  int32_t cand_len[PF_MAX_CAND];  /* proposal length of candidate c */
+  int64_t cand_pos[PF_MAX_CAND];  /* store position p of candidate c */
+} pf_draft;
+
+/* Verify result (device memory, written by pf_verify_step). */
+typedef struct pf_verify_result {
+  int32_t accept_len;  /* l_acc: accepted proposal tokens */
+  int32_t bonus;       /* the model's own token after the accepted prefix */
+  int32_t rows;        /* verify rows used */
+  int32_t status;      /* 0, or PF_VSTATUS_* bits */
+  int64_t kv_base;     /* cache length the step appended after (P) */
+  int32_t path[PF_MAX_NODES];       /* node at depth d of the accepted path, d <= accept_len */
+  int32_t pred[PF_MAX_NODES];       /* greedy token predicted at each row */
+  int32_t out_tokens[PF_MAX_NODES]; /* accept_len accepted tokens, then the bonus */
+  int32_t reserved0;
+} pf_verify_result;
+
+#define PF_VSTATUS_NAN 1        /* a row's logits held NaN (NaN never wins argmax) */
+#define PF_VSTATUS_CTX_FULL 2   /* context buffer too small for the commit */
+#define PF_VSTATUS_BAD_TOKEN 4  /* a row's token id was outside [0, vocab); id 0 was used */
+
+/* ------------------------------------------------------------------------ */
+/* Decoding context (tokens of prompt and output so far, on the device)     */
+/* ------------------------------------------------------------------------ */
+
+typedef struct pf_context {
+  int32_t *tokens;    /* device [capacity] */
+  int32_t *len;       /* device int32: tokens in use; tokens[len-1] is the current token */
+  int64_t capacity;
+  int64_t host_bound; /* host upper bound of *len, maintained by the library */
+} pf_context;
+
+/* Describe a context buffer whose first `len` tokens are already on the
+ * device; sets *len_dev = len (async on s) and host_bound = len. */
+pf_status pf_context_init(pf_context *ctx, int32_t *tokens_dev, int32_t *len_dev, int64_t capacity,
+                          int64_t len, pf_stream s);
+/* Synchronise s and tighten host_bound to the device length. */
+pf_status pf_context_sync_bound(pf_context *ctx, pf_stream s);
+
+/* ------------------------------------------------------------------------ */
+/* Experience store (Section 3.2, "Decoding experience memory")             */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Build the store from prior output sequences appended once to a shared
+ * token array. tokens_host[T] holds all sequences back to back;
+ * seq_offsets_host[n_seqs+1] are their start offsets (offsets[0] = 0,
+ * offsets[n_seqs] = T). An entry at position p is eligible for an n-gram
+ * query when the n tokens ending at p lie inside p's sequence and p < b(p),
+ * b(p) being the last position of that sequence. The host arrays are copied;
+ * the store owns its device copy. ngram in [1, 8]; T < 2^31.
+ */
+pf_status pf_store_build(const int32_t *tokens_host, const int64_t *seq_offsets_host,
+                         int64_t n_seqs, int32_t ngram, pf_stream s, pf_store **out);
+void pf_store_destroy(pf_store *store);
+int64_t pf_store_size(const pf_store *store); /* tokens T */
+
+/*
+ * Draft lookup. The query is the last `ngram` context tokens (ending with the
+ * current token). Every eligible entry p proposes tokens p+1..p+len with
+ * len = min(k_max, b(p) - p) (truncated at the boundary, Section 3.2).
+ * Entries rank by (len, p), larger first. Linear (tree = 0): the best entry's
+ * proposal. Tree (tree = 1): the best n_cand proposals merged in rank order
+ * into a trie of at most max_nodes non-root nodes. A context shorter than
+ * ngram, or no eligible entry, gives an empty proposal (n_nodes = 1), which
+ * verifies as an ordinary greedy step. Requires *ctx->len >= 1.
+ * k_max in [0, 64]; n_cand in [1, 4] (1 if linear); max_nodes in [1, 63].
+ * draft_dev: device pf_draft, written asynchronously on s.
+ */
+pf_status pf_draft_lookup(const pf_store *store, const pf_context *ctx, int32_t k_max,
+                          int32_t tree, int32_t n_cand, int32_t max_nodes, pf_draft *draft_dev,
+                          pf_stream s);
+
+/* ------------------------------------------------------------------------ */
+/* Model                                                                    */
+/* ------------------------------------------------------------------------ */
+
+typedef struct pf_model_config {
+  int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
+  int32_t dtype;     /* PF_DTYPE_F32 or PF_DTYPE_BF16 (weights, cache, activations) */
+  double rope_theta; /* rotate-half RoPE, angle pos * theta^(-2i/head_dim) */
+  double rms_eps;
+} pf_model_config;
+
+/*
+ * Device pointers to the caller's weights, row-major, in the model dtype
+ * except the norm gains (fp32). L = n_layers, H = hidden, q = n_heads *
+ * head_dim, kv = n_kv_heads * head_dim, F = ffn, V = vocab.
+ *   embed [V][H], lm_head [V][H]
+ *   wqkv [L][q+2kv][H]  rows: query heads, then key heads, then value heads
+ *   wo   [L][H][q]
+ *   wgu  [L][2F][H]     rows: gate, then up
+ *   wd   [L][H][F]
+ *   attn_norm, ffn_norm [L][H]; final_norm [H]
+ * pf_model_create copies everything into library-owned buffers (weights in a
+ * tiled layout for the matrix cores); the caller may free its copies after
+ * the stream has been synchronised.
+ */
+typedef struct pf_model_weights {
+  const void *embed, *lm_head, *wqkv, *wo, *wgu, *wd;
+  const float *attn_norm, *ffn_norm, *final_norm;
+} pf_model_weights;
+
+/* Requirements: head_dim in {64, 128}; n_heads % n_kv_heads == 0; hidden,
+ * q, F multiples of 16; vocab multiple of 16. */
+pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w, pf_stream s,
+                          pf_model **out);
+void pf_model_destroy(pf_model *model);
+/* Device bytes held by the model (weights + work buffers). */
+int64_t pf_model_bytes(const pf_model *model);
+
+/* ------------------------------------------------------------------------ */
+/* KV cache (caller-owned device buffer with this layout)                   */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Per layer l and KV head g, a key plane and a value plane of
+ * capacity*head_dim elements each, in the model dtype:
+ *   keys   at ((l*2 + 0)*n_kv + g) * capacity*head_dim, element [slot][i]
+ *   values at ((l*2 + 1)*n_kv + g) * capacity*head_dim, element [i][slot]
+ * (values are stored transposed so that the attention's value operand is a
+ * contiguous run of slots). Slot t holds position t. *len is the committed
+ * length; slots >= *len are dead. capacity must be a multiple of 64.
+ */
+typedef struct pf_kv_cache {
+  void *data;         /* device, pf_kv_bytes() bytes */
+  int32_t *len;       /* device int32 */
+  int64_t capacity;
+  int64_t host_bound; /* host upper bound of *len, maintained by the library */
+  int32_t n_layers, n_kv_heads, head_dim, dtype;
+  int32_t pending;      /* rows appended by the last verify, not yet committed */
+  int32_t pending_tree; /* 1 if that verify was a tree draft */
+} pf_kv_cache;
+
+int64_t pf_kv_bytes(const pf_model *model, int64_t capacity);
+pf_status pf_kv_init(pf_kv_cache *kv, const pf_model *model, void *data_dev, int32_t *len_dev,
+                     int64_t capacity);
+/* Copy a prefix given in the logical layout [L][2][n_kv][n][head_dim]
+ * (device) into slots 0..n-1 and set the length to n. */
+pf_status pf_kv_import(pf_kv_cache *kv, const void *src_dev, int64_t n, pf_stream s);
+/* Copy slots start..start+n-1 out in the logical layout [L][2][n_kv][n][head_dim]. */
+pf_status pf_kv_export(const pf_kv_cache *kv, void *dst_dev, int64_t start, int64_t n,
+                       pf_stream s);
+/* Set the committed length (rolls back whole steps; len <= capacity). */
+pf_status pf_kv_set_len(pf_kv_cache *kv, int64_t len, pf_stream s);
+/* Synchronise s and tighten host_bound to the device length (the bound
+ * otherwise grows by the verify rows at every commit). */
+pf_status pf_kv_sync_bound(pf_kv_cache *kv, pf_stream s);
+
+/* ------------------------------------------------------------------------ */
+/* Verify step (Section 3.2, "Single-pass token verification")              */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * One decoder forward over `rows` rows: node j of the draft (row 0 the
+ * current token; rows >= n_nodes are padding: token 0, never accepted, never
+ * attended by real rows) at position P + depth(j), P = *kv->len. Each row
+ * attends to the cached prefix 0..P-1 and to the draft rows it may see:
+ * rows <= j for a linear draft, ancestors-or-self for a tree. K/V of row j
+ * are appended at slot P + j. Greedy prediction per row (largest fp32 logit,
+ * lowest index on ties, NaN never wins), then acceptance of the longest
+ * proposal prefix that matches the predictions plus the model's next token.
+ * rows = k_max + 1 for linear drafts (<= 65), max_nodes + 1 for trees (<= 64),
+ * at least the draft's n_nodes. logits_dev: NULL or device fp32
+ * [rows][vocab] receiving the logits. res_dev: device pf_verify_result.
+ * Fails with PF_ECAPACITY if host_bound + rows > capacity.
+ */
+pf_status pf_verify_step(pf_model *model, pf_kv_cache *kv, const pf_draft *draft_dev,
+                         int32_t rows, int32_t tree, float *logits_dev,
+                         pf_verify_result *res_dev, pf_stream s);
+
+/*
+ * Profiling variant of pf_verify_step: the same work, with a HIP event pair
+ * recorded around every kernel launch. It synchronises s, then adds each
+ * launch's duration in ms to ms_out[kind] and 1 to count_out[kind] (host
+ * arrays of PF_PROF_KINDS entries, caller-initialised). Allocates events:
+ * not for graph capture.
+ */
+#define PF_PROF_KINDS 10
+#define PF_PROF_SETUP 0     /* row setup, embedding + first RMSNorm */
+#define PF_PROF_QKV 1       /* QKV projection */
+#define PF_PROF_QKV_POST 2  /* split-K reduction, RoPE, KV append */
+#define PF_PROF_ATTN 3      /* verify attention + split merge */
+#define PF_PROF_O 4         /* output projection */
+#define PF_PROF_NORM 5      /* residual add + RMSNorm */
+#define PF_PROF_GATE_UP 6   /* gate/up projection + SwiGLU */
+#define PF_PROF_DOWN 7      /* down projection */
+#define PF_PROF_LM_HEAD 8   /* lm_head + argmax partials */
+#define PF_PROF_ACCEPT 9    /* argmax reduction + acceptance */
+pf_status pf_verify_step_profiled(pf_model *model, pf_kv_cache *kv, const pf_draft *draft_dev,
+                                  int32_t rows, int32_t tree, float *logits_dev,
+                                  pf_verify_result *res_dev, pf_stream s, double *ms_out,
+                                  int32_t *count_out);
+
+/*
+ * Commit the accepted rows (Section 3.2: the iteration advances the output
+ * by l_acc + 1 tokens). Linear: the accepted rows already sit at slots
+ * P..P+l_acc; the length becomes P + l_acc + 1 and later slots are dead
+ * (rollback of the rejected rows). Tree: the rows of the accepted path are
+ * moved to slots P..P+l_acc first. ctx (nullable): the accepted tokens and
+ * the bonus token are appended, so the bonus becomes the current token.
+ */
+pf_status pf_kv_commit(pf_kv_cache *kv, const pf_verify_result *res_dev, pf_context *ctx,
+                       pf_stream s);
+
+/* ------------------------------------------------------------------------ */
+/* Prompt-prefix carryover prefill (Section 3.4)                            */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Run n new tokens (device int32) through the decoder after the cached
+ * prefix P = *kv->len, in causal chunks of `chunk` rows, appending their K/V
+ * at slots P..P+n-1 and setting the length to P+n. logits_last_dev: NULL or
+ * device fp32 [vocab] for the last new token. Needs host_bound + n <= capacity.
+ */
+pf_status pf_prefill(pf_model *model, pf_kv_cache *kv, const int32_t *tokens_dev, int32_t n,
+                     int32_t chunk, float *logits_last_dev, pf_stream s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PF_H */

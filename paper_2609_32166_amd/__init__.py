@@ -1,0 +1,341 @@
+"""Python binding of libpf, the MI355X (gfx950) retrieval-drafted verify step.
+
+Thin ctypes marshalling over the C ABI in ``include/pf.h``: every function
+here packs arguments and calls the library; all computation runs in the HIP
+kernels. torch supplies device memory (tensors) and streams. There is no CPU
+fallback: importing works anywhere, but any call raises if ``libpf.so`` is
+missing or no GPU is present.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpf.so")
+
+PF_OK, PF_EINVAL, PF_ENOMEM, PF_EHIP, PF_ECAPACITY, PF_ESTATE, PF_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
+PF_DTYPE_F32, PF_DTYPE_BF16 = 0, 1
+PF_MAX_DRAFT, PF_MAX_NODES, PF_MAX_CAND, PF_MAX_TREE_NODES = 64, 65, 4, 63
+PF_VSTATUS_NAN, PF_VSTATUS_CTX_FULL = 1, 2
+
+# Device records, same layout as pf_draft / pf_verify_result in pf.h.
+DRAFT_DTYPE = np.dtype([("n_nodes", "<i4"), ("tree", "<i4"), ("n_found", "<i4"),
+                        ("n_eligible", "<i4"), ("token", "<i4", 65), ("parent", "<i4", 65),
+                        ("depth", "<i4", 65), ("reserved0", "<i4"), ("anc", "<u8", 65),
+                        ("cand_len", "<i4", 4), ("cand_pos", "<i8", 4)])
+RESULT_DTYPE = np.dtype([("accept_len", "<i4"), ("bonus", "<i4"), ("rows", "<i4"),
+                         ("status", "<i4"), ("kv_base", "<i8"), ("path", "<i4", 65),
+                         ("pred", "<i4", 65), ("out_tokens", "<i4", 65), ("reserved0", "<i4")])
+assert DRAFT_DTYPE.itemsize == 1368 and RESULT_DTYPE.itemsize == 808
+
+EXPORTED = ["pf_last_error", "pf_version", "pf_context_init", "pf_context_sync_bound",
+            "pf_store_build", "pf_store_destroy", "pf_store_size", "pf_draft_lookup",
+            "pf_model_create", "pf_model_destroy", "pf_model_bytes", "pf_kv_bytes", "pf_kv_init",
+            "pf_kv_import", "pf_kv_export", "pf_kv_set_len", "pf_kv_sync_bound", "pf_verify_step",
+            "pf_kv_commit", "pf_prefill", "pf_verify_step_profiled"]
+
+PF_PROF_KINDS = 10
+PROF_NAMES = ["setup", "qkv", "qkv_post", "attn", "o_proj", "norm", "gate_up", "down",
+              "lm_head", "accept"]
+
+
+class PfError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"pf status {status}: {msg}")
+        self.status = status
+
+
+class pf_context(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_void_p), ("len", ctypes.c_void_p),
+                ("capacity", ctypes.c_int64), ("host_bound", ctypes.c_int64)]
+
+
+class pf_kv_cache(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("len", ctypes.c_void_p), ("capacity", ctypes.c_int64),
+                ("host_bound", ctypes.c_int64), ("n_layers", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("pending", ctypes.c_int32),
+                ("pending_tree", ctypes.c_int32)]
+
+
+class pf_model_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("rope_theta", ctypes.c_double),
+                ("rms_eps", ctypes.c_double)]
+
+
+class pf_model_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("embed", "lm_head", "wqkv", "wo", "wgu", "wd", "attn_norm", "ffn_norm",
+                 "final_norm")]
+
+
+_lib = None
+
+
+def lib():
+    """Load libpf.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        sig = {
+            "pf_last_error": (ctypes.c_char_p, []),
+            "pf_version": (ctypes.c_char_p, []),
+            "pf_context_init": (i32, [vp, vp, vp, i64, i64, vp]),
+            "pf_context_sync_bound": (i32, [vp, vp]),
+            "pf_store_build": (i32, [vp, vp, i64, i32, vp, vp]),
+            "pf_store_destroy": (None, [vp]),
+            "pf_store_size": (i64, [vp]),
+            "pf_draft_lookup": (i32, [vp, vp, i32, i32, i32, i32, vp, vp]),
+            "pf_model_create": (i32, [vp, vp, vp, vp]),
+            "pf_model_destroy": (None, [vp]),
+            "pf_model_bytes": (i64, [vp]),
+            "pf_kv_bytes": (i64, [vp, i64]),
+            "pf_kv_init": (i32, [vp, vp, vp, vp, i64]),
+            "pf_kv_import": (i32, [vp, vp, i64, vp]),
+            "pf_kv_export": (i32, [vp, vp, i64, i64, vp]),
+            "pf_kv_set_len": (i32, [vp, i64, vp]),
+            "pf_kv_sync_bound": (i32, [vp, vp]),
+            "pf_verify_step": (i32, [vp, vp, vp, i32, i32, vp, vp, vp]),
+            "pf_kv_commit": (i32, [vp, vp, vp, vp]),
+            "pf_prefill": (i32, [vp, vp, vp, i32, i32, vp, vp]),
+            "pf_verify_step_profiled": (i32, [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().pf_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != PF_OK:
+        raise PfError(status, last_error())
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        raise RuntimeError("libpf needs a ROCm GPU (torch.cuda.is_available() is False)")
+    return torch
+
+
+def _stream(stream=None) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+# ----------------------------------------------------------------------------
+# objects
+# ----------------------------------------------------------------------------
+
+class Context:
+    """Device token buffer + length of the decoding context."""
+
+    def __init__(self, tokens: np.ndarray, capacity: int, stream=None):
+        torch = _torch()
+        tokens = np.asarray(tokens, np.int32)
+        self.buf = torch.zeros(capacity, dtype=torch.int32, device="cuda")
+        self.buf[:len(tokens)] = torch.from_numpy(tokens).cuda()
+        self.len = torch.zeros(1, dtype=torch.int32, device="cuda")
+        self.c = pf_context()
+        pf_context_init(self, len(tokens), stream)
+
+    def tokens(self) -> np.ndarray:
+        n = int(self.len.item())
+        return self.buf[:n].cpu().numpy()
+
+
+def pf_context_init(ctx: Context, length: int, stream=None) -> None:
+    _check(lib().pf_context_init(ctypes.byref(ctx.c), ctx.buf.data_ptr(), ctx.len.data_ptr(),
+                                 ctx.buf.numel(), int(length), _stream(stream)))
+
+
+def pf_context_sync_bound(ctx: Context, stream=None) -> None:
+    _check(lib().pf_context_sync_bound(ctypes.byref(ctx.c), _stream(stream)))
+
+
+class Store:
+    def __init__(self, handle: int):
+        self.h = handle
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.pf_store_destroy(self.h)
+            self.h = None
+
+    @property
+    def size(self) -> int:
+        return int(lib().pf_store_size(self.h))
+
+
+def pf_store_build(tokens: np.ndarray, seq_offsets: np.ndarray, ngram: int, stream=None) -> Store:
+    tokens = np.ascontiguousarray(tokens, np.int32)
+    offs = np.ascontiguousarray(seq_offsets, np.int64)
+    out = ctypes.c_void_p()
+    _check(lib().pf_store_build(tokens.ctypes.data, offs.ctypes.data, len(offs) - 1, int(ngram),
+                                _stream(stream), ctypes.byref(out)))
+    return Store(out.value)
+
+
+def new_draft():
+    torch = _torch()
+    return torch.zeros(DRAFT_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+
+
+def new_result():
+    torch = _torch()
+    return torch.zeros(RESULT_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+
+
+def read_draft(t) -> np.ndarray:
+    return np.frombuffer(t.cpu().numpy().tobytes(), DRAFT_DTYPE)[0]
+
+
+def read_result(t) -> np.ndarray:
+    return np.frombuffer(t.cpu().numpy().tobytes(), RESULT_DTYPE)[0]
+
+
+def pf_draft_lookup(store: Store, ctx: Context, k_max: int, tree: bool, n_cand: int,
+                    max_nodes: int, draft, stream=None) -> None:
+    _check(lib().pf_draft_lookup(store.h, ctypes.byref(ctx.c), int(k_max), int(bool(tree)),
+                                 int(n_cand), int(max_nodes), draft.data_ptr(), _stream(stream)))
+
+
+class Model:
+    def __init__(self, handle: int, cfg: pf_model_config):
+        self.h = handle
+        self.cfg = cfg
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.pf_model_destroy(self.h)
+            self.h = None
+
+    @property
+    def bytes(self) -> int:
+        return int(lib().pf_model_bytes(self.h))
+
+
+def model_config(shape) -> pf_model_config:
+    """pf_model_config from a shape object with the synth.ModelShape fields."""
+    return pf_model_config(shape.n_layers, shape.hidden, shape.n_heads, shape.n_kv_heads,
+                           shape.head_dim, shape.ffn, shape.vocab,
+                           PF_DTYPE_BF16 if shape.dtype == "bf16" else PF_DTYPE_F32,
+                           float(shape.rope_theta), float(shape.rms_eps))
+
+
+def pf_model_create(cfg: pf_model_config, weights: Dict[str, "object"], stream=None) -> Model:
+    """weights: device tensors named embed, lm_head, wqkv, wo, wgu, wd,
+    attn_norm, ffn_norm, final_norm in the layouts of pf_model_weights."""
+    w = pf_model_weights(*[_ptr(weights[k]) for k in
+                           ("embed", "lm_head", "wqkv", "wo", "wgu", "wd", "attn_norm",
+                            "ffn_norm", "final_norm")])
+    out = ctypes.c_void_p()
+    _check(lib().pf_model_create(ctypes.byref(cfg), ctypes.byref(w), _stream(stream),
+                                 ctypes.byref(out)))
+    return Model(out.value, cfg)
+
+
+class KVCache:
+    def __init__(self, model: Model, capacity: int):
+        torch = _torch()
+        nbytes = int(lib().pf_kv_bytes(model.h, capacity))
+        if nbytes < 0:
+            raise PfError(PF_EINVAL, "pf_kv_bytes failed")
+        self.data = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        self.len = torch.zeros(1, dtype=torch.int32, device="cuda")
+        self.c = pf_kv_cache()
+        _check(lib().pf_kv_init(ctypes.byref(self.c), model.h, self.data.data_ptr(),
+                                self.len.data_ptr(), int(capacity)))
+
+
+def pf_kv_import(kv: KVCache, src, n: int, stream=None) -> None:
+    _check(lib().pf_kv_import(ctypes.byref(kv.c), _ptr(src), int(n), _stream(stream)))
+
+
+def pf_kv_export(kv: KVCache, dst, start: int, n: int, stream=None) -> None:
+    _check(lib().pf_kv_export(ctypes.byref(kv.c), dst.data_ptr(), int(start), int(n),
+                              _stream(stream)))
+
+
+def pf_kv_set_len(kv: KVCache, n: int, stream=None) -> None:
+    _check(lib().pf_kv_set_len(ctypes.byref(kv.c), int(n), _stream(stream)))
+
+
+def pf_kv_sync_bound(kv: KVCache, stream=None) -> None:
+    _check(lib().pf_kv_sync_bound(ctypes.byref(kv.c), _stream(stream)))
+
+
+def pf_verify_step(model: Model, kv: KVCache, draft, rows: int, tree: bool, logits, result,
+                   stream=None) -> None:
+    _check(lib().pf_verify_step(model.h, ctypes.byref(kv.c), draft.data_ptr(), int(rows),
+                                int(bool(tree)), _ptr(logits), result.data_ptr(),
+                                _stream(stream)))
+
+
+def pf_verify_step_profiled(model: Model, kv: KVCache, draft, rows: int, tree: bool, logits,
+                            result, stream=None):
+    """Returns (ms per kernel kind, launches per kind) for one verify step."""
+    ms = np.zeros(PF_PROF_KINDS, np.float64)
+    cnt = np.zeros(PF_PROF_KINDS, np.int32)
+    _check(lib().pf_verify_step_profiled(model.h, ctypes.byref(kv.c), draft.data_ptr(), int(rows),
+                                         int(bool(tree)), _ptr(logits), result.data_ptr(),
+                                         _stream(stream), ms.ctypes.data, cnt.ctypes.data))
+    return ms, cnt
+
+
+def pf_kv_commit(kv: KVCache, result, ctx: Optional[Context], stream=None) -> None:
+    _check(lib().pf_kv_commit(ctypes.byref(kv.c), result.data_ptr(),
+                              ctypes.byref(ctx.c) if ctx is not None else None, _stream(stream)))
+
+
+def pf_prefill(model: Model, kv: KVCache, tokens, n: int, chunk: int, logits_last=None,
+               stream=None) -> None:
+    _check(lib().pf_prefill(model.h, ctypes.byref(kv.c), tokens.data_ptr(), int(n), int(chunk),
+                            _ptr(logits_last), _stream(stream)))
+
+
+# ----------------------------------------------------------------------------
+# host arrays -> device tensors in the pf_model_weights layouts
+# ----------------------------------------------------------------------------
+
+def weights_to_device(w: Dict[str, np.ndarray], dtype: str) -> Dict[str, "object"]:
+    """Copy host weights (bf16 bit patterns as uint16, or fp32) to the GPU."""
+    torch = _torch()
+    out = {}
+    for k, v in w.items():
+        v = np.ascontiguousarray(v)
+        if v.dtype == np.uint16:
+            t = torch.from_numpy(v.view(np.int16)).cuda().view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(v.astype(np.float32, copy=False)).cuda()
+        out[k] = t
+    return out
+
+
+def array_to_device(a: np.ndarray):
+    torch = _torch()
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(a).cuda()

@@ -1,0 +1,685 @@
+// C-ABI layer of libpf: argument checks, the experience-store builder, model
+// creation (weight packing) and the launch sequence of one verify step.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace pf;
+
+static_assert(sizeof(pf_draft) == 1368, "pf_draft layout");
+static_assert(sizeof(pf_verify_result) == 808, "pf_verify_result layout");
+
+namespace {
+
+thread_local std::string g_err;
+
+pf_status fail(pf_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+pf_status ok() {
+  g_err.clear();
+  return PF_OK;
+}
+
+#define HIPCHK(call)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (call);                                                            \
+    if (e_ != hipSuccess) return fail(PF_EHIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+inline hipStream_t st(pf_stream s) { return (hipStream_t)s; }
+inline int64_t roundup(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+inline bool is_bf16(const pf_model *m) { return m->cfg.dtype == PF_DTYPE_BF16; }
+inline int frag_k_of(const pf_model *m) { return is_bf16(m) ? 32 : 16; }
+
+Packed geom(int64_t N, int64_t K, int kf) {
+  Packed p;
+  p.N = N;
+  p.K = K;
+  p.NT = (N + 15) / 16;
+  p.KFr = (K + kf - 1) / kf;
+  return p;
+}
+
+// split-K factor for a partial-sum GEMM: about 1024 blocks, at least two
+// fragments per wave
+int splits_for(int64_t nblocks, int64_t KFr) {
+  int64_t s = (1024 + nblocks - 1) / nblocks;
+  int64_t cap = KFr / 8;
+  if (cap < 1) cap = 1;
+  if (s > cap) s = cap;
+  if (s < 1) s = 1;
+  return (int)s;
+}
+
+int64_t partial_blocks(const Packed &p) {
+  int nt = gemm_tiles_per_block(EPI_PARTIAL);
+  return (p.NT + nt - 1) / nt;
+}
+
+constexpr int kMaxSplitsAttn = 64;
+
+// Optional per-kernel timing of a verify step (events around each launch).
+struct Prof {
+  hipStream_t s;
+  std::vector<hipEvent_t> ev;
+  std::vector<int> kind;
+  hipError_t begin(int k) {
+    hipEvent_t e;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return r;
+    ev.push_back(e);
+    kind.push_back(k);
+    return hipEventRecord(e, s);
+  }
+  hipError_t end() {
+    hipEvent_t e;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return r;
+    ev.push_back(e);
+    kind.push_back(-1);
+    return hipEventRecord(e, s);
+  }
+  ~Prof() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  }
+};
+
+template <typename T> pf_status dev_alloc(T **p, int64_t bytes, int64_t *total) {
+  if (bytes <= 0) bytes = 16;
+  if (hipMalloc((void **)p, (size_t)bytes) != hipSuccess) {
+    *p = nullptr;
+    return fail(PF_ENOMEM, "hipMalloc of %lld bytes failed", (long long)bytes);
+  }
+  if (total) *total += bytes;
+  return PF_OK;
+}
+
+void model_free(pf_model *m) {
+  if (!m) return;
+  void *ptrs[] = {m->wqkv, m->wo, m->wgu, m->wd, m->lm, m->embed, m->attn_norm, m->ffn_norm,
+                  m->final_norm, m->inv_freq, m->x, m->xn, m->qb, m->attn, m->act, m->part,
+                  m->apart_o, m->apart_ml, m->amax, m->rope, m->rowinfo, m->pred, m->flags};
+  for (void *p : ptrs)
+    if (p) (void)hipFree(p);
+  delete m;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *pf_last_error(void) { return g_err.c_str(); }
+const char *pf_version(void) { return "pf 0.1 gfx950"; }
+
+// ---------------------------------------------------------------------------
+// context
+// ---------------------------------------------------------------------------
+
+pf_status pf_context_init(pf_context *ctx, int32_t *tokens_dev, int32_t *len_dev, int64_t capacity,
+                          int64_t len, pf_stream s) {
+  if (!ctx || !tokens_dev || !len_dev) return fail(PF_EINVAL, "pf_context_init: null pointer");
+  if (capacity < 1 || len < 0 || len > capacity || capacity > INT32_MAX)
+    return fail(PF_EINVAL, "pf_context_init: bad capacity %lld / len %lld", (long long)capacity,
+                (long long)len);
+  ctx->tokens = tokens_dev;
+  ctx->len = len_dev;
+  ctx->capacity = capacity;
+  ctx->host_bound = len;
+  HIPCHK(launch_set_int(len_dev, (int32_t)len, st(s)));
+  return ok();
+}
+
+pf_status pf_context_sync_bound(pf_context *ctx, pf_stream s) {
+  if (!ctx || !ctx->len) return fail(PF_EINVAL, "pf_context_sync_bound: null pointer");
+  int32_t v = 0;
+  HIPCHK(hipMemcpyAsync(&v, ctx->len, 4, hipMemcpyDeviceToHost, st(s)));
+  HIPCHK(hipStreamSynchronize(st(s)));
+  ctx->host_bound = v;
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// store
+// ---------------------------------------------------------------------------
+
+pf_status pf_store_build(const int32_t *tokens, const int64_t *offs, int64_t n_seqs, int32_t ngram,
+                         pf_stream s, pf_store **out) {
+  if (!out) return fail(PF_EINVAL, "pf_store_build: null out");
+  *out = nullptr;
+  if (!offs || n_seqs < 0) return fail(PF_EINVAL, "pf_store_build: bad offsets");
+  if (ngram < 1 || ngram > 8) return fail(PF_EINVAL, "pf_store_build: ngram %d not in [1,8]", ngram);
+  if (offs[0] != 0) return fail(PF_EINVAL, "pf_store_build: offsets[0] must be 0");
+  for (int64_t i = 0; i < n_seqs; ++i)
+    if (offs[i + 1] < offs[i]) return fail(PF_EINVAL, "pf_store_build: offsets not monotonic");
+  const int64_t T = offs[n_seqs];
+  if (T > 0 && !tokens) return fail(PF_EINVAL, "pf_store_build: null tokens");
+  if (T >= ((int64_t)1 << 31)) return fail(PF_EUNSUPPORTED, "pf_store_build: T >= 2^31");
+
+  // eligible entries: n-gram inside the sequence and p < last position
+  std::vector<int32_t> pos, rem;
+  for (int64_t q = 0; q < n_seqs; ++q) {
+    const int64_t a = offs[q], last = offs[q + 1] - 1;
+    for (int64_t p = a + ngram - 1; p < last; ++p) {
+      pos.push_back((int32_t)p);
+      rem.push_back((int32_t)(last - p));
+    }
+  }
+  const int64_t E = (int64_t)pos.size();
+  int nb_log2 = 0;
+  while (((int64_t)1 << nb_log2) < E && nb_log2 < 28) ++nb_log2;
+  const int64_t nb = (int64_t)1 << nb_log2;
+  std::vector<uint32_t> bk(E);
+  std::vector<int32_t> off(nb + 1, 0);
+  for (int64_t i = 0; i < E; ++i) {
+    bk[i] = ngram_hash(tokens + pos[i] - ngram + 1, ngram) & (uint32_t)(nb - 1);
+    off[bk[i] + 1]++;
+  }
+  for (int64_t b = 0; b < nb; ++b) off[b + 1] += off[b];
+  std::vector<int32_t> fill(off.begin(), off.end() - 1);
+  std::vector<int32_t> epos(E), erem(E);
+  for (int64_t i = 0; i < E; ++i) {
+    int32_t at = fill[bk[i]]++;
+    epos[at] = pos[i];
+    erem[at] = rem[i];
+  }
+
+  pf_store *S = new pf_store();
+  S->T = T;
+  S->E = E;
+  S->nb_log2 = nb_log2;
+  S->ngram = ngram;
+  pf_status r = PF_OK;
+  if ((r = dev_alloc(&S->tokens, T * 4, nullptr)) || (r = dev_alloc(&S->ent_pos, E * 4, nullptr)) ||
+      (r = dev_alloc(&S->ent_rem, E * 4, nullptr)) ||
+      (r = dev_alloc(&S->bucket_off, (nb + 1) * 4, nullptr))) {
+    pf_store_destroy(S);
+    return r;
+  }
+  hipStream_t hs = st(s);
+  hipError_t e = hipSuccess;
+  if (T) e = hipMemcpyAsync(S->tokens, tokens, T * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && E) e = hipMemcpyAsync(S->ent_pos, epos.data(), E * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && E) e = hipMemcpyAsync(S->ent_rem, erem.data(), E * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(S->bucket_off, off.data(), (nb + 1) * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);  // host vectors die here
+  if (e != hipSuccess) {
+    pf_store_destroy(S);
+    return fail(PF_EHIP, "pf_store_build: copy failed: %s", hipGetErrorString(e));
+  }
+  *out = S;
+  return ok();
+}
+
+void pf_store_destroy(pf_store *S) {
+  if (!S) return;
+  if (S->tokens) (void)hipFree(S->tokens);
+  if (S->ent_pos) (void)hipFree(S->ent_pos);
+  if (S->ent_rem) (void)hipFree(S->ent_rem);
+  if (S->bucket_off) (void)hipFree(S->bucket_off);
+  delete S;
+}
+
+int64_t pf_store_size(const pf_store *S) { return S ? S->T : -1; }
+
+pf_status pf_draft_lookup(const pf_store *S, const pf_context *ctx, int32_t k_max, int32_t tree,
+                          int32_t n_cand, int32_t max_nodes, pf_draft *draft, pf_stream s) {
+  if (!S || !ctx || !ctx->tokens || !ctx->len || !draft)
+    return fail(PF_EINVAL, "pf_draft_lookup: null pointer");
+  if (k_max < 0 || k_max > PF_MAX_DRAFT)
+    return fail(PF_EINVAL, "pf_draft_lookup: k_max %d not in [0,%d]", k_max, PF_MAX_DRAFT);
+  if (tree != 0 && tree != 1) return fail(PF_EINVAL, "pf_draft_lookup: tree must be 0 or 1");
+  if (n_cand < 1 || n_cand > PF_MAX_CAND || (!tree && n_cand != 1))
+    return fail(PF_EINVAL, "pf_draft_lookup: n_cand %d invalid", n_cand);
+  if (tree && (max_nodes < 1 || max_nodes > PF_MAX_TREE_NODES))
+    return fail(PF_EINVAL, "pf_draft_lookup: max_nodes %d not in [1,%d]", max_nodes,
+                PF_MAX_TREE_NODES);
+  if (ctx->host_bound < 1) return fail(PF_ESTATE, "pf_draft_lookup: empty context");
+  LookupArgs a;
+  a.tokens = S->tokens;
+  a.ent_pos = S->ent_pos;
+  a.ent_rem = S->ent_rem;
+  a.bucket_off = S->bucket_off;
+  a.nb_log2 = S->nb_log2;
+  a.ngram = S->ngram;
+  a.ctx = ctx->tokens;
+  a.ctx_len = ctx->len;
+  a.k_max = k_max;
+  a.tree = tree;
+  a.n_cand = n_cand;
+  a.max_nodes = tree ? max_nodes : PF_MAX_DRAFT;
+  a.draft = draft;
+  HIPCHK(launch_lookup(a, st(s)));
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// model
+// ---------------------------------------------------------------------------
+
+pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w, pf_stream s,
+                          pf_model **out) {
+  if (!out) return fail(PF_EINVAL, "pf_model_create: null out");
+  *out = nullptr;
+  if (!cfg || !w) return fail(PF_EINVAL, "pf_model_create: null config or weights");
+  const pf_model_config c = *cfg;
+  if (c.dtype != PF_DTYPE_F32 && c.dtype != PF_DTYPE_BF16)
+    return fail(PF_EINVAL, "pf_model_create: unknown dtype %d", c.dtype);
+  if (c.n_layers < 1 || c.hidden < 16 || c.n_heads < 1 || c.n_kv_heads < 1 || c.ffn < 16 ||
+      c.vocab < 16)
+    return fail(PF_EINVAL, "pf_model_create: bad sizes");
+  if (c.head_dim != 64 && c.head_dim != 128)
+    return fail(PF_EUNSUPPORTED, "pf_model_create: head_dim %d not in {64,128}", c.head_dim);
+  if (c.n_heads % c.n_kv_heads || c.n_heads / c.n_kv_heads > 8)
+    return fail(PF_EUNSUPPORTED, "pf_model_create: n_heads/n_kv_heads must be an integer <= 8");
+  if (c.hidden % 16 || c.ffn % 16 || c.vocab % 16)
+    return fail(PF_EUNSUPPORTED, "pf_model_create: hidden, ffn, vocab must be multiples of 16");
+  if (!(c.rms_eps >= 0) || !(c.rope_theta > 0)) return fail(PF_EINVAL, "pf_model_create: eps/theta");
+  if (!w->embed || !w->lm_head || !w->wqkv || !w->wo || !w->wgu || !w->wd || !w->attn_norm ||
+      !w->ffn_norm || !w->final_norm)
+    return fail(PF_EINVAL, "pf_model_create: null weight pointer");
+
+  pf_model *m = new pf_model();
+  m->cfg = c;
+  const bool bf = c.dtype == PF_DTYPE_BF16;
+  m->esz = bf ? 2 : 4;
+  const int kf = bf ? 32 : 16;
+  const int64_t L = c.n_layers, H = c.hidden, q = (int64_t)c.n_heads * c.head_dim,
+                kv = (int64_t)c.n_kv_heads * c.head_dim, F = c.ffn, V = c.vocab;
+  m->pqkv = geom(q + 2 * kv, H, kf);
+  m->po = geom(H, q, kf);
+  m->pgu = geom(2 * F, H, kf);
+  m->pd = geom(H, F, kf);
+  m->plm = geom(V, H, kf);
+  if (m->plm.bytes() >= ((int64_t)1 << 31) || m->pgu.bytes() >= ((int64_t)1 << 31)) {
+    model_free(m);
+    return fail(PF_EUNSUPPORTED, "pf_model_create: a packed matrix exceeds 2 GiB");
+  }
+  int64_t tot = 0;
+  pf_status r = PF_OK;
+#define ALLOC(ptr, bytes)                          \
+  if ((r = dev_alloc(&(ptr), (bytes), &tot))) {    \
+    model_free(m);                                 \
+    return r;                                      \
+  }
+  ALLOC(m->wqkv, m->pqkv.bytes() * L);
+  ALLOC(m->wo, m->po.bytes() * L);
+  ALLOC(m->wgu, m->pgu.bytes() * L);
+  ALLOC(m->wd, m->pd.bytes() * L);
+  ALLOC(m->lm, m->plm.bytes());
+  ALLOC(m->embed, V * H * m->esz);
+  ALLOC(m->attn_norm, L * H * 4);
+  ALLOC(m->ffn_norm, L * H * 4);
+  ALLOC(m->final_norm, H * 4);
+  ALLOC(m->inv_freq, (c.head_dim / 2) * 8);
+  // step work buffers
+  const int64_t Hp = roundup(H, kf), qp = roundup(q, kf), Fp = roundup(F, kf);
+  int64_t part = 0;
+  const Packed *pg[] = {&m->pqkv, &m->po, &m->pd};
+  for (const Packed *p : pg) {
+    int64_t nb = partial_blocks(*p);
+    int64_t e = (int64_t)splits_for(nb, p->KFr) * kRowPad * p->NT * 16;
+    if (e > part) part = e;
+  }
+  m->part_elems = part;
+  m->apart_rows = (int64_t)c.n_heads * kMaxSplitsAttn * kRowPad;
+  m->amax_elems = ((m->plm.NT + 3) / 4) * kRowPad;
+  ALLOC(m->x, kRowPad * H * 4);
+  ALLOC(m->xn, kRowPad * Hp * m->esz);
+  ALLOC(m->qb, kRowPad * q * m->esz);
+  ALLOC(m->attn, kRowPad * qp * m->esz);
+  ALLOC(m->act, kRowPad * Fp * m->esz);
+  ALLOC(m->part, part * 4);
+  ALLOC(m->apart_o, m->apart_rows * c.head_dim * 4);
+  ALLOC(m->apart_ml, m->apart_rows * 2 * 4);
+  ALLOC(m->amax, m->amax_elems * (int64_t)sizeof(ArgmaxPart));
+  ALLOC(m->rope, kRowPad * c.head_dim * 4);
+  ALLOC(m->rowinfo, kRowPad * 4 * 4 + kRowPad * 8);
+  ALLOC(m->pred, 2 * kRowPad * 4);
+  ALLOC(m->flags, 64);
+#undef ALLOC
+  m->bytes = tot;
+
+  hipStream_t hs = st(s);
+  hipError_t e = hipSuccess;
+  void *zero[] = {m->x, m->xn, m->qb, m->attn, m->act};
+  int64_t zb[] = {kRowPad * H * 4, kRowPad * Hp * m->esz, kRowPad * q * m->esz,
+                  kRowPad * qp * m->esz, kRowPad * Fp * m->esz};
+  for (int i = 0; i < 5 && e == hipSuccess; ++i) e = hipMemsetAsync(zero[i], 0, zb[i], hs);
+  if (e == hipSuccess) e = launch_pack(w->wqkv, q + 2 * kv, H, L, (q + 2 * kv) * H, bf, m->pqkv, m->wqkv, hs);
+  if (e == hipSuccess) e = launch_pack(w->wo, H, q, L, H * q, bf, m->po, m->wo, hs);
+  if (e == hipSuccess) e = launch_pack(w->wgu, 2 * F, H, L, 2 * F * H, bf, m->pgu, m->wgu, hs);
+  if (e == hipSuccess) e = launch_pack(w->wd, H, F, L, H * F, bf, m->pd, m->wd, hs);
+  if (e == hipSuccess) e = launch_pack(w->lm_head, V, H, 1, V * H, bf, m->plm, m->lm, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(m->embed, w->embed, V * H * m->esz, hipMemcpyDeviceToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(m->attn_norm, w->attn_norm, L * H * 4, hipMemcpyDeviceToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(m->ffn_norm, w->ffn_norm, L * H * 4, hipMemcpyDeviceToDevice, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(m->final_norm, w->final_norm, H * 4, hipMemcpyDeviceToDevice, hs);
+  std::vector<double> invf(c.head_dim / 2);
+  for (int i = 0; i < c.head_dim / 2; ++i)
+    invf[i] = std::pow(c.rope_theta, -2.0 * (double)i / (double)c.head_dim);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(m->inv_freq, invf.data(), invf.size() * 8, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) {
+    model_free(m);
+    return fail(PF_EHIP, "pf_model_create: %s", hipGetErrorString(e));
+  }
+  *out = m;
+  return ok();
+}
+
+void pf_model_destroy(pf_model *m) { model_free(m); }
+int64_t pf_model_bytes(const pf_model *m) { return m ? m->bytes : -1; }
+
+// ---------------------------------------------------------------------------
+// KV cache
+// ---------------------------------------------------------------------------
+
+int64_t pf_kv_bytes(const pf_model *m, int64_t capacity) {
+  if (!m || capacity < 0) return -1;
+  return (int64_t)m->cfg.n_layers * 2 * m->cfg.n_kv_heads * capacity * m->cfg.head_dim * m->esz;
+}
+
+pf_status pf_kv_init(pf_kv_cache *kv, const pf_model *m, void *data, int32_t *len_dev,
+                     int64_t capacity) {
+  if (!kv || !m || !data || !len_dev) return fail(PF_EINVAL, "pf_kv_init: null pointer");
+  if (capacity < 64 || capacity % 64 || capacity > INT32_MAX)
+    return fail(PF_EINVAL, "pf_kv_init: capacity %lld must be a positive multiple of 64",
+                (long long)capacity);
+  kv->data = data;
+  kv->len = len_dev;
+  kv->capacity = capacity;
+  kv->host_bound = 0;
+  kv->n_layers = m->cfg.n_layers;
+  kv->n_kv_heads = m->cfg.n_kv_heads;
+  kv->head_dim = m->cfg.head_dim;
+  kv->dtype = m->cfg.dtype;
+  kv->pending = 0;
+  kv->pending_tree = 0;
+  return ok();
+}
+
+static pf_status kv_check(const pf_kv_cache *kv, const char *fn) {
+  if (!kv || !kv->data || !kv->len) return fail(PF_EINVAL, "%s: null cache", fn);
+  if (kv->capacity < 64 || kv->capacity % 64) return fail(PF_EINVAL, "%s: bad capacity", fn);
+  return PF_OK;
+}
+
+pf_status pf_kv_import(pf_kv_cache *kv, const void *src, int64_t n, pf_stream s) {
+  if (pf_status r = kv_check(kv, "pf_kv_import")) return r;
+  if (!src && n > 0) return fail(PF_EINVAL, "pf_kv_import: null source");
+  if (n < 0 || n > kv->capacity) return fail(PF_ECAPACITY, "pf_kv_import: %lld rows", (long long)n);
+  if (n > 0)
+    HIPCHK(launch_kv_copy(kv->dtype == PF_DTYPE_BF16, true, kv->data, src, nullptr, kv->n_layers,
+                          kv->n_kv_heads, kv->head_dim, kv->capacity, 0, n, st(s)));
+  HIPCHK(launch_set_int(kv->len, (int32_t)n, st(s)));
+  kv->host_bound = n;
+  kv->pending = 0;
+  return ok();
+}
+
+pf_status pf_kv_export(const pf_kv_cache *kv, void *dst, int64_t start, int64_t n, pf_stream s) {
+  if (pf_status r = kv_check(kv, "pf_kv_export")) return r;
+  if (!dst || start < 0 || n < 0 || start + n > kv->capacity)
+    return fail(PF_EINVAL, "pf_kv_export: bad range");
+  if (n > 0)
+    HIPCHK(launch_kv_copy(kv->dtype == PF_DTYPE_BF16, false, kv->data, nullptr, dst, kv->n_layers,
+                          kv->n_kv_heads, kv->head_dim, kv->capacity, start, n, st(s)));
+  return ok();
+}
+
+pf_status pf_kv_set_len(pf_kv_cache *kv, int64_t len, pf_stream s) {
+  if (pf_status r = kv_check(kv, "pf_kv_set_len")) return r;
+  if (len < 0 || len > kv->capacity) return fail(PF_ECAPACITY, "pf_kv_set_len: %lld", (long long)len);
+  HIPCHK(launch_set_int(kv->len, (int32_t)len, st(s)));
+  kv->host_bound = len;
+  kv->pending = 0;
+  return ok();
+}
+
+pf_status pf_kv_sync_bound(pf_kv_cache *kv, pf_stream s) {
+  if (pf_status r = kv_check(kv, "pf_kv_sync_bound")) return r;
+  int32_t v = 0;
+  HIPCHK(hipMemcpyAsync(&v, kv->len, 4, hipMemcpyDeviceToHost, st(s)));
+  HIPCHK(hipStreamSynchronize(st(s)));
+  kv->host_bound = v;
+  kv->pending = 0;
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// verify step
+// ---------------------------------------------------------------------------
+
+static pf_status model_kv_match(const pf_model *m, const pf_kv_cache *kv, const char *fn) {
+  if (kv->n_layers != m->cfg.n_layers || kv->n_kv_heads != m->cfg.n_kv_heads ||
+      kv->head_dim != m->cfg.head_dim || kv->dtype != m->cfg.dtype)
+    return fail(PF_EINVAL, "%s: cache does not match the model", fn);
+  return PF_OK;
+}
+
+#define PROF(kind, call)                                                         \
+  do {                                                                           \
+    if (prof) HIPCHK(prof->begin(kind));                                         \
+    HIPCHK(call);                                                                \
+    if (prof) HIPCHK(prof->end());                                               \
+  } while (0)
+
+static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft, int32_t rows,
+                             int32_t tree, float *logits, pf_verify_result *res, pf_stream s,
+                             Prof *prof) {
+  if (!m || !draft || !res) return fail(PF_EINVAL, "pf_verify_step: null pointer");
+  if (pf_status r = kv_check(kv, "pf_verify_step")) return r;
+  if (pf_status r = model_kv_match(m, kv, "pf_verify_step")) return r;
+  if (tree != 0 && tree != 1) return fail(PF_EINVAL, "pf_verify_step: tree must be 0 or 1");
+  if (rows < 1 || rows > (tree ? 64 : kMaxRows))
+    return fail(PF_EINVAL, "pf_verify_step: rows %d out of range", rows);
+  if (kv->host_bound < 0 || kv->host_bound + rows > kv->capacity)
+    return fail(PF_ECAPACITY, "pf_verify_step: cache bound %lld + %d rows > capacity %lld",
+                (long long)kv->host_bound, rows, (long long)kv->capacity);
+  const pf_model_config &c = m->cfg;
+  const bool bf = is_bf16(m);
+  const int kf = frag_k_of(m);
+  const int L = c.n_layers, H = c.hidden, hd = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads;
+  const int64_t q = (int64_t)nq * hd, kvd = (int64_t)nkv * hd, F = c.ffn, V = c.vocab;
+  const int64_t Hp = roundup(H, kf), qp = roundup(q, kf), Fp = roundup(F, kf);
+  const int M = rows, MT = (rows + 15) / 16;
+  hipStream_t hs = st(s);
+  const float eps = (float)c.rms_eps;
+  uint64_t *rowmask = (uint64_t *)(m->rowinfo + kRowPad * 4);
+
+  StepArgs sa;
+  sa.draft = draft;
+  sa.res = res;
+  sa.kv_len = kv->len;
+  sa.rows = rows;
+  sa.tree = tree;
+  sa.L = L; sa.H = H; sa.nq = nq; sa.nkv = nkv; sa.hd = hd; sa.F = (int)F; sa.V = (int)V;
+  sa.eps = eps;
+  sa.inv_freq = m->inv_freq;
+  sa.rowinfo = m->rowinfo;
+  sa.rowmask = rowmask;
+  sa.rope = m->rope;
+  PROF(0, launch_prep(sa, hs));
+  PROF(0, launch_embed_norm(bf, m->embed, m->rowinfo, M, H, m->attn_norm, eps, m->x, m->xn, Hp, hs));
+
+  // attention geometry: key ranges over P + rows keys (P <= host bound)
+  const int64_t keys_max = kv->host_bound + rows;
+  int chunk = (int)roundup((keys_max + kMaxSplitsAttn - 1) / kMaxSplitsAttn, 32);
+  if (chunk < 128) chunk = 128;
+  const int n_splits = (int)((keys_max + chunk - 1) / chunk);
+
+  for (int l = 0; l < L; ++l) {
+    // QKV projection (split-K partials)
+    GemmArgs g{};
+    g.W = (const char *)m->wqkv + (int64_t)l * m->pqkv.bytes();
+    g.W_bytes = m->pqkv.bytes();
+    g.KFr = m->pqkv.KFr;
+    g.NTtot = m->pqkv.NT;
+    g.X = m->xn;
+    g.ldx = Hp;
+    g.M = M;
+    g.splits = splits_for(partial_blocks(m->pqkv), m->pqkv.KFr);
+    g.out = m->part;
+    g.ldo = q + 2 * kvd;
+    PROF(1, launch_gemm(bf, EPI_PARTIAL, MT, g, hs));
+    PROF(2, launch_qkv_post(bf, m->part, g.splits, M, nq, nkv, hd, g.ldo, m->rope, kv->len, m->qb, q,
+                           kv->data, l, kv->capacity, hs));
+    // attention
+    AttnArgs at{};
+    at.q = m->qb;
+    at.ldq = q;
+    at.cache = kv->data;
+    at.plane = kv->capacity * hd;
+    at.cap = kv->capacity;
+    at.layer = l;
+    at.n_kv = nkv;
+    at.group = nq / nkv;
+    at.head_dim = hd;
+    at.M = M;
+    at.kv_len = kv->len;
+    at.n_splits = n_splits;
+    at.chunk_keys = chunk;
+    at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
+    at.tree = tree;
+    at.anc = rowmask;
+    at.part_o = m->apart_o;
+    at.part_ml = m->apart_ml;
+    at.out = m->attn;
+    at.ldout = qp;
+    PROF(3, launch_attn(bf, MT, at, hs));
+    // output projection + residual + FFN norm
+    GemmArgs go{};
+    go.W = (const char *)m->wo + (int64_t)l * m->po.bytes();
+    go.W_bytes = m->po.bytes();
+    go.KFr = m->po.KFr;
+    go.NTtot = m->po.NT;
+    go.X = m->attn;
+    go.ldx = qp;
+    go.M = M;
+    go.splits = splits_for(partial_blocks(m->po), m->po.KFr);
+    go.out = m->part;
+    go.ldo = H;
+    PROF(4, launch_gemm(bf, EPI_PARTIAL, MT, go, hs));
+    PROF(5, launch_residual_norm(bf, m->part, go.splits, M, H, H, m->ffn_norm + (int64_t)l * H, eps,
+                                m->x, m->xn, Hp, hs));
+    // gate/up + SwiGLU
+    GemmArgs gg{};
+    gg.W = (const char *)m->wgu + (int64_t)l * m->pgu.bytes();
+    gg.W_bytes = m->pgu.bytes();
+    gg.KFr = m->pgu.KFr;
+    gg.NTtot = m->pgu.NT;
+    gg.X = m->xn;
+    gg.ldx = Hp;
+    gg.M = M;
+    gg.splits = 1;
+    gg.act = m->act;
+    gg.ldact = Fp;
+    gg.up_tile_off = F / 16;
+    PROF(6, launch_gemm(bf, EPI_SWIGLU, MT, gg, hs));
+    // down projection + residual + next norm
+    GemmArgs gd{};
+    gd.W = (const char *)m->wd + (int64_t)l * m->pd.bytes();
+    gd.W_bytes = m->pd.bytes();
+    gd.KFr = m->pd.KFr;
+    gd.NTtot = m->pd.NT;
+    gd.X = m->act;
+    gd.ldx = Fp;
+    gd.M = M;
+    gd.splits = splits_for(partial_blocks(m->pd), m->pd.KFr);
+    gd.out = m->part;
+    gd.ldo = H;
+    PROF(7, launch_gemm(bf, EPI_PARTIAL, MT, gd, hs));
+    const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
+    PROF(5, launch_residual_norm(bf, m->part, gd.splits, M, H, H, next_gain, eps, m->x, m->xn, Hp,
+                                hs));
+  }
+  // lm_head + greedy argmax partials
+  GemmArgs gl{};
+  gl.W = m->lm;
+  gl.W_bytes = m->plm.bytes();
+  gl.KFr = m->plm.KFr;
+  gl.NTtot = m->plm.NT;
+  gl.X = m->xn;
+  gl.ldx = Hp;
+  gl.M = M;
+  gl.splits = 1;
+  gl.amax = m->amax;
+  gl.logits = logits;
+  gl.ldlog = V;
+  PROF(8, launch_gemm(bf, EPI_ARGMAX, MT, gl, hs));
+  const int nparts = (int)((m->plm.NT + gemm_tiles_per_block(EPI_ARGMAX) - 1) /
+                           gemm_tiles_per_block(EPI_ARGMAX));
+  PROF(9, launch_argmax_accept(m->amax, nparts, rows, tree, draft, m->pred, res, hs));
+  kv->pending = rows;
+  kv->pending_tree = tree;
+  return ok();
+}
+
+pf_status pf_verify_step(pf_model *m, pf_kv_cache *kv, const pf_draft *draft, int32_t rows,
+                         int32_t tree, float *logits, pf_verify_result *res, pf_stream s) {
+  return verify_impl(m, kv, draft, rows, tree, logits, res, s, nullptr);
+}
+
+pf_status pf_verify_step_profiled(pf_model *m, pf_kv_cache *kv, const pf_draft *draft,
+                                  int32_t rows, int32_t tree, float *logits, pf_verify_result *res,
+                                  pf_stream s, double *ms_out, int32_t *count_out) {
+  if (!ms_out || !count_out) return fail(PF_EINVAL, "pf_verify_step_profiled: null outputs");
+  Prof prof;
+  prof.s = st(s);
+  pf_status r = verify_impl(m, kv, draft, rows, tree, logits, res, s, &prof);
+  if (r != PF_OK) return r;
+  HIPCHK(hipStreamSynchronize(prof.s));
+  for (size_t i = 0; i + 1 < prof.ev.size(); i += 2) {
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, prof.ev[i], prof.ev[i + 1]));
+    int k = prof.kind[i];
+    if (k >= 0 && k < PF_PROF_KINDS) {
+      ms_out[k] += ms;
+      count_out[k] += 1;
+    }
+  }
+  return ok();
+}
+
+pf_status pf_kv_commit(pf_kv_cache *kv, const pf_verify_result *res, pf_context *ctx,
+                       pf_stream s) {
+  if (!res) return fail(PF_EINVAL, "pf_kv_commit: null result");
+  if (pf_status r = kv_check(kv, "pf_kv_commit")) return r;
+  if (kv->pending <= 0) return fail(PF_ESTATE, "pf_kv_commit: no verify step to commit");
+  if (ctx && (!ctx->tokens || !ctx->len)) return fail(PF_EINVAL, "pf_kv_commit: bad context");
+  if (ctx && ctx->host_bound + kv->pending > ctx->capacity)
+    return fail(PF_ECAPACITY, "pf_kv_commit: context bound %lld + %d > capacity %lld",
+                (long long)ctx->host_bound, kv->pending, (long long)ctx->capacity);
+  HIPCHK(launch_commit(kv->dtype == PF_DTYPE_BF16, res, kv->data, kv->n_layers, kv->n_kv_heads,
+                       kv->head_dim, kv->capacity, kv->pending_tree, kv->len,
+                       ctx ? ctx->tokens : nullptr,
+                       ctx ? ctx->len : nullptr, ctx ? ctx->capacity : 0, st(s)));
+  kv->host_bound += kv->pending;
+  if (ctx) ctx->host_bound += kv->pending;
+  kv->pending = 0;
+  kv->pending_tree = 0;
+  return ok();
+}
+
+pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_t n, int32_t chunk,
+                     float *logits_last, pf_stream s) {
+  (void)m; (void)kv; (void)tokens; (void)n; (void)chunk; (void)logits_last; (void)s;
+  return fail(PF_EUNSUPPORTED, "pf_prefill: not built yet");
+}
+
+}  // extern "C"

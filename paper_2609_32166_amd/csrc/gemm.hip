@@ -1,0 +1,294 @@
+// Skinny GEMM for the verify step: Y[M x N] = X[M x K] * W[N x K]^T with
+// M <= 80 rows (the current token plus the draft) and N, K in the thousands.
+// The work is bound by streaming W from HBM once; the matrix cores only have
+// to keep up. W is pre-packed so every wave load is one contiguous 1 KiB
+// fragment (16 rows x 32 bf16 or 16 fp32 columns), which goes straight into
+// the MFMA A operand; X rows go into the B operand. Each block of 4 waves owns
+// NT n-tiles and one K range (split-K), the waves split that range four ways
+// and reduce through LDS in a fixed order, so results are deterministic.
+#include "kernels.h"
+
+namespace pf {
+
+// ---------------------------------------------------------------------------
+// weight packing
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__global__ void k_pack(const T *__restrict__ src, int64_t N, int64_t K, int64_t KFr,
+                       int64_t NT, int64_t layers, int64_t src_layer_stride,
+                       uint4 *__restrict__ dst) {
+  constexpr int E = Elem<T>::E;
+  constexpr int KF = 4 * E;
+  const int64_t per_layer = NT * KFr * 64;
+  const int64_t total = per_layer * layers;
+  for (int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; c < total;
+       c += (int64_t)gridDim.x * blockDim.x) {
+    int64_t l = c / per_layer, r = c % per_layer;
+    int lane = (int)(r & 63);
+    int64_t frag = r >> 6;
+    int64_t nt = frag / KFr, kf = frag % KFr;
+    int64_t n = nt * 16 + (lane & 15);
+    int64_t k0 = kf * KF + (lane >> 4) * E;
+    union {
+      uint4 v;
+      T e[E];
+    } u;
+    const T *row = src + l * src_layer_stride + n * K;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      int64_t k = k0 + e;
+      if (n < N && k < K) {
+        u.e[e] = row[k];
+      } else {
+        memset(&u.e[e], 0, sizeof(T));
+      }
+    }
+    dst[c] = u.v;
+  }
+}
+
+hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers,
+                       int64_t src_layer_stride, bool bf16, const Packed &g, void *dst,
+                       hipStream_t s) {
+  int64_t total = g.NT * g.KFr * 64 * layers;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (bf16)
+    k_pack<bf16_t><<<(unsigned)blocks, 256, 0, s>>>((const bf16_t *)src, N, K, g.KFr, g.NT, layers,
+                                                    src_layer_stride, (uint4 *)dst);
+  else
+    k_pack<float><<<(unsigned)blocks, 256, 0, s>>>((const float *)src, N, K, g.KFr, g.NT, layers,
+                                                   src_layer_stride, (uint4 *)dst);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// GEMM
+// ---------------------------------------------------------------------------
+
+constexpr int kU = 4;  // fragments per pipeline stage
+
+template <int EPI> struct EpiTiles;
+template <> struct EpiTiles<EPI_PARTIAL> { static constexpr int NT = 2; };
+template <> struct EpiTiles<EPI_SWIGLU> { static constexpr int NT = 2; };  // 1 gate + 1 up
+template <> struct EpiTiles<EPI_ARGMAX> { static constexpr int NT = 4; };
+
+__device__ inline float silu(float g) { return g / (1.0f + expf(-g)); }
+
+template <typename T, int MT, int EPI>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+  constexpr int NT = EpiTiles<EPI>::NT;
+  constexpr int E = Elem<T>::E;
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+
+  // n tiles of this block
+  int64_t tile[NT];
+  bool tv[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    if (EPI == EPI_SWIGLU) {
+      int64_t t = blockIdx.x;
+      tile[j] = j == 0 ? t : t + a.up_tile_off;
+      tv[j] = t < a.up_tile_off;
+    } else {
+      tile[j] = (int64_t)blockIdx.x * NT + j;
+      tv[j] = tile[j] < a.NTtot;
+    }
+  }
+
+  // k fragment range of this wave
+  const int64_t s = blockIdx.y;
+  const int64_t r0 = s * a.KFr / a.splits, r1 = (s + 1) * a.KFr / a.splits;
+  const int64_t f0 = r0 + wid * (r1 - r0) / 4, f1 = r0 + (wid + 1) * (r1 - r0) / 4;
+  const int64_t n = f1 - f0;
+
+  const rsrc_t wr = make_rsrc(a.W, (uint32_t)a.W_bytes);
+  const rsrc_t xr = make_rsrc(a.X, (uint32_t)(kRowPad * a.ldx * sizeof(T)));
+  uint32_t wbase[NT], xbase[MT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j)
+    wbase[j] = tv[j] ? (uint32_t)(((tile[j] * a.KFr + f0) * 64 + lane) * 16) : kOOB;
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+    xbase[m] = (uint32_t)((((int64_t)(m * 16 + (lane & 15))) * a.ldx + f0 * 4 * E +
+                           (lane >> 4) * E) * sizeof(T));
+
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  uint4 wa[kU][NT], xa[kU][MT], wb[kU][NT], xb[kU][MT];
+  auto load = [&](uint4(&wv)[kU][NT], uint4(&xv)[kU][MT], int64_t blk) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      int64_t i = blk * kU + u;
+      bool in = i < n;
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+        wv[u][j] = bload16(wr, in && wbase[j] != kOOB ? wbase[j] + (uint32_t)(i * 1024) : kOOB);
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+        xv[u][m] = bload16(xr, in ? xbase[m] + (uint32_t)(i * 4 * E * sizeof(T)) : kOOB);
+    }
+  };
+  auto compute = [&](uint4(&wv)[kU][NT], uint4(&xv)[kU][MT]) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[m][j] = mma<T>(wv[u][j], xv[u][m], acc[m][j]);
+  };
+
+  const int64_t nblk = (n + kU - 1) / kU;
+  load(wa, xa, 0);
+  for (int64_t b = 0; b < nblk; b += 2) {
+    load(wb, xb, b + 1);
+    compute(wa, xa);
+    if (b + 1 >= nblk) break;
+    load(wa, xa, b + 2);
+    compute(wb, xb);
+  }
+
+  // reduce the four waves' partial sums in LDS (fixed order: wave 0..3)
+  __shared__ f32x4 red[3][MT][NT][64];
+  if (wid > 0) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) red[wid - 1][m][j][lane] = acc[m][j];
+  }
+  __syncthreads();
+  if (wid != 0) return;
+#pragma unroll
+  for (int w = 0; w < 3; ++w)
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) acc[m][j] += red[w][m][j][lane];
+
+  // lane holds D[n = tile*16 + 4*q + i][row = m*16 + lane%16], q = lane/16
+  const int q = lane >> 4;
+  if (EPI == EPI_PARTIAL) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      int row = m * 16 + (lane & 15);
+      if (row >= a.M) continue;
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        if (!tv[j]) continue;
+        int64_t col = tile[j] * 16 + 4 * q;
+        float4 v = make_float4(acc[m][j][0], acc[m][j][1], acc[m][j][2], acc[m][j][3]);
+        *(float4 *)(a.out + (s * kRowPad + row) * a.ldo + col) = v;
+      }
+    }
+  } else if (EPI == EPI_SWIGLU) {
+    if (!tv[0]) return;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      int row = m * 16 + (lane & 15);
+      if (row >= a.M) continue;
+      int64_t col = tile[0] * 16 + 4 * q;
+      T *dst = (T *)a.act + (int64_t)row * a.ldact + col;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Elem<T>::store(dst, i, silu(acc[m][0][i]) * acc[m][1][i]);
+    }
+  } else {  // EPI_ARGMAX
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      int row = m * 16 + (lane & 15);
+      float bv = -INFINITY;
+      int bi = 0x7FFFFFFF;
+      int nan = 0;
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        if (!tv[j]) continue;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v = acc[m][j][i];
+          int idx = (int)(tile[j] * 16 + 4 * q + i);
+          if (v != v) {
+            nan = 1;
+            continue;
+          }
+          if (v > bv || (v == bv && idx < bi)) {
+            bv = v;
+            bi = idx;
+          }
+        }
+      }
+      if (a.logits && row < a.M) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          if (!tv[j]) continue;
+          int64_t col = tile[j] * 16 + 4 * q;
+          *(float4 *)(a.logits + (int64_t)row * a.ldlog + col) =
+              make_float4(acc[m][j][0], acc[m][j][1], acc[m][j][2], acc[m][j][3]);
+        }
+      }
+      // reduce over the four lane quarters that share this row
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        float ov = __shfl_xor(bv, o, 64);
+        int oi = __shfl_xor(bi, o, 64);
+        nan |= __shfl_xor(nan, o, 64);
+        if (ov > bv || (ov == bv && oi < bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      if (q == 0 && row < a.M) {
+        ArgmaxPart p;
+        p.v = bv;
+        p.idx = bi;
+        p.nan = nan;
+        p.pad = 0;
+        a.amax[(int64_t)blockIdx.x * kRowPad + row] = p;
+      }
+    }
+  }
+}
+
+int gemm_tiles_per_block(int epi) {
+  switch (epi) {
+    case EPI_PARTIAL: return EpiTiles<EPI_PARTIAL>::NT;
+    case EPI_SWIGLU: return 1;
+    default: return EpiTiles<EPI_ARGMAX>::NT;
+  }
+}
+
+template <typename T, int EPI>
+static hipError_t launch_t(int mt, const GemmArgs &a, dim3 grid, hipStream_t s) {
+  switch (mt) {
+    case 1: k_gemm<T, 1, EPI><<<grid, 256, 0, s>>>(a); break;
+    case 2: k_gemm<T, 2, EPI><<<grid, 256, 0, s>>>(a); break;
+    case 3: k_gemm<T, 3, EPI><<<grid, 256, 0, s>>>(a); break;
+    case 4: k_gemm<T, 4, EPI><<<grid, 256, 0, s>>>(a); break;
+    case 5: k_gemm<T, 5, EPI><<<grid, 256, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, hipStream_t s) {
+  int64_t nb;
+  if (epi == EPI_SWIGLU)
+    nb = a.up_tile_off;
+  else
+    nb = (a.NTtot + gemm_tiles_per_block(epi) - 1) / gemm_tiles_per_block(epi);
+  dim3 grid((unsigned)nb, (unsigned)a.splits);
+  if (bf16) {
+    if (epi == EPI_PARTIAL) return launch_t<bf16_t, EPI_PARTIAL>(mt, a, grid, s);
+    if (epi == EPI_SWIGLU) return launch_t<bf16_t, EPI_SWIGLU>(mt, a, grid, s);
+    return launch_t<bf16_t, EPI_ARGMAX>(mt, a, grid, s);
+  }
+  if (epi == EPI_PARTIAL) return launch_t<float, EPI_PARTIAL>(mt, a, grid, s);
+  if (epi == EPI_SWIGLU) return launch_t<float, EPI_SWIGLU>(mt, a, grid, s);
+  return launch_t<float, EPI_ARGMAX>(mt, a, grid, s);
+}
+
+}  // namespace pf

@@ -1,0 +1,123 @@
+// Host-side launchers of the HIP kernels (internal to libpf).
+#pragma once
+
+#include "pf_internal.h"
+
+namespace pf {
+
+// Buffer-resource loads: 16-byte loads whose byte offset is checked against
+// the resource size; an offset past the end returns zeros and fetches
+// nothing. Used for ragged K ranges without branches.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family raw buffer descriptor word 3
+
+__device__ inline rsrc_t make_rsrc(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes,
+                                           kRsrcWord3);
+}
+__device__ inline uint4 bload16(rsrc_t r, uint32_t off) {
+  v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+enum GemmEpi { EPI_PARTIAL = 0, EPI_SWIGLU = 1, EPI_ARGMAX = 2 };
+
+struct GemmArgs {
+  const void *W;      // packed fragments of one matrix
+  int64_t W_bytes;    // bytes of that packed matrix (< 2^31)
+  int64_t KFr;        // k fragments
+  int64_t NTtot;      // n tiles (16 rows of W each) of the output
+  const void *X;      // activations [kRowPad][ldx], model dtype
+  int64_t ldx;        // elements per activation row (multiple of the fragment k)
+  int M;              // valid rows
+  int splits;         // split-K factor (grid.y)
+  // EPI_PARTIAL: out[(split*kRowPad + m)*ldo + n]
+  float *out;
+  int64_t ldo;
+  // EPI_SWIGLU: act[m*ldact + n] = silu(gate)*up, gate tile t, up tile t + up_tile_off
+  void *act;
+  int64_t ldact;
+  int64_t up_tile_off;
+  // EPI_ARGMAX: amax[blockIdx.x*kRowPad + m]; optional logits[m*ldlog + n]
+  ArgmaxPart *amax;
+  float *logits;
+  int64_t ldlog;
+};
+
+struct AttnArgs {
+  const void *q;        // [kRowPad][ldq] queries after RoPE
+  int64_t ldq;
+  const void *cache;    // KV cache data
+  int64_t plane;        // capacity * head_dim
+  int64_t cap;          // capacity
+  int layer, n_kv, group, head_dim;
+  int M;                // verify rows
+  const int32_t *kv_len;  // P (device)
+  int n_splits;         // key ranges (grid.x)
+  int chunk_keys;       // keys per range (multiple of 32)
+  float scale_log2;     // log2(e) / sqrt(head_dim)
+  int tree;
+  const uint64_t *anc;  // [kRowPad] draft-key visibility of each row (tree)
+  float *part_o;        // [n_heads][n_splits][kRowPad][head_dim]
+  float *part_ml;       // [n_heads][n_splits][kRowPad][2]
+  void *out;            // [kRowPad][ldout] attention output (model dtype)
+  int64_t ldout;
+};
+
+hipError_t launch_attn(bool bf16, int rt, const AttnArgs &a, hipStream_t s);
+
+// step kernels (step.hip)
+struct StepArgs {
+  const pf_draft *draft;
+  pf_verify_result *res;
+  int32_t *kv_len;
+  int rows, tree;
+  int L, H, nq, nkv, hd, F, V;
+  float eps;
+  const double *inv_freq;
+  int32_t *rowinfo;     // [kRowPad][4] token, depth, valid, 0
+  uint64_t *rowmask;    // [kRowPad]
+  float *rope;          // [kRowPad][hd/2][2]
+};
+hipError_t launch_prep(const StepArgs &a, hipStream_t s);
+hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
+                             const float *gain, float eps, float *x, void *xn, int64_t ldxn,
+                             hipStream_t s);
+hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int M, int nq, int nkv, int hd,
+                           int64_t ldpart, const float *rope, const int32_t *kv_len, void *qbuf,
+                           int64_t ldq, void *cache, int layer, int64_t cap, hipStream_t s);
+hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int M, int H,
+                                int64_t ldpart, const float *gain, float eps, float *x, void *xn,
+                                int64_t ldxn, hipStream_t s);
+hipError_t launch_argmax_accept(const ArgmaxPart *amax, int nparts, int rows, int tree,
+                                const pf_draft *draft, int32_t *pred, pf_verify_result *res,
+                                hipStream_t s);
+hipError_t launch_commit(bool bf16, const pf_verify_result *res, void *cache, int L, int nkv,
+                         int hd, int64_t cap, int tree, int32_t *kv_len, int32_t *ctx_tokens,
+                         int32_t *ctx_len, int64_t ctx_cap, hipStream_t s);
+hipError_t launch_kv_copy(bool bf16, bool import_, void *cache, const void *logical_src,
+                          void *logical_dst, int L, int nkv, int hd, int64_t cap, int64_t start,
+                          int64_t n, hipStream_t s);
+hipError_t launch_set_int(int32_t *p, int32_t v, hipStream_t s);
+
+// lookup (lookup.hip)
+struct LookupArgs {
+  const int32_t *tokens;
+  const int32_t *ent_pos, *ent_rem, *bucket_off;
+  int nb_log2, ngram;
+  const int32_t *ctx, *ctx_len;
+  int k_max, tree, n_cand, max_nodes;
+  pf_draft *draft;
+};
+hipError_t launch_lookup(const LookupArgs &a, hipStream_t s);
+
+hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers, int64_t src_layer_stride,
+                       bool bf16, const Packed &geom, void *dst, hipStream_t s);
+
+// Tiles per block along N for each epilogue.
+int gemm_tiles_per_block(int epi);
+hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, hipStream_t s);
+
+}  // namespace pf

@@ -1,0 +1,395 @@
+// Small per-step kernels of the verify step: row setup, embedding + RMSNorm,
+// the QKV epilogue (split-K reduction, RoPE, KV append), residual + RMSNorm,
+// greedy argmax + acceptance, and the KV commit / rollback.
+#include "kernels.h"
+
+namespace pf {
+
+// ---------------------------------------------------------------------------
+// row setup: tokens, positions, visibility masks, RoPE table
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_prep(StepArgs a) {
+  const pf_draft *d = a.draft;
+  const int P = *a.kv_len;
+  const int n = d->n_nodes;
+  const int half = a.hd / 2;
+  __shared__ int bad;
+  if (threadIdx.x == 0) bad = 0;
+  __syncthreads();
+  for (int j = threadIdx.x; j < kRowPad; j += blockDim.x) {
+    bool valid = j < n && j < a.rows;
+    int tok = valid ? d->token[j] : 0;
+    if (tok < 0 || tok >= a.V) {  // never index the embedding out of range
+      tok = 0;
+      bad = 1;
+    }
+    int dep = valid ? d->depth[j] : (a.tree ? 1 : j);
+    a.rowinfo[j * 4 + 0] = tok;
+    a.rowinfo[j * 4 + 1] = dep;
+    a.rowinfo[j * 4 + 2] = valid ? 1 : 0;
+    a.rowinfo[j * 4 + 3] = 0;
+    uint64_t m = 0;
+    if (a.tree && j < 64) m = valid ? d->anc[j] : ((1ull << j) | 1ull);
+    a.rowmask[j] = m;
+  }
+  // cos/sin of (P + depth) * theta^(-2i/d), evaluated in fp64
+  for (int t = threadIdx.x; t < a.rows * half; t += blockDim.x) {
+    int j = t / half, i = t % half;
+    bool valid = j < n;
+    int dep = valid ? d->depth[j] : (a.tree ? 1 : j);
+    double ang = (double)(P + dep) * a.inv_freq[i];
+    a.rope[(j * half + i) * 2 + 0] = (float)cos(ang);
+    a.rope[(j * half + i) * 2 + 1] = (float)sin(ang);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    a.res->kv_base = P;
+    a.res->rows = a.rows;
+    a.res->status = bad ? PF_VSTATUS_BAD_TOKEN : 0;
+  }
+}
+
+hipError_t launch_prep(const StepArgs &a, hipStream_t s) {
+  k_prep<<<1, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// RMSNorm helpers (one block of 256 threads per row)
+// ---------------------------------------------------------------------------
+
+__device__ inline float block_sum256(float v, float *sh) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  return sh[0] + sh[1] + sh[2] + sh[3];
+}
+
+template <typename T>
+__device__ void norm_row(const float *x, int H, const float *gain, float eps, T *out) {
+  __shared__ float sh[4];
+  float ss = 0.f;
+  for (int k = threadIdx.x; k < H; k += 256) ss += x[k] * x[k];
+  ss = block_sum256(ss, sh);
+  const float inv = 1.0f / sqrtf(ss / (float)H + eps);
+  for (int k = threadIdx.x; k < H; k += 256) Elem<T>::store(out, k, x[k] * inv * gain[k]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed_norm(const T *embed, const int32_t *rowinfo, int H,
+                                                    const float *gain, float eps, float *x, T *xn,
+                                                    int64_t ldxn) {
+  const int m = blockIdx.x;
+  const int tok = rowinfo[m * 4];
+  float *xr = x + (int64_t)m * H;
+  for (int k = threadIdx.x; k < H; k += 256) xr[k] = Elem<T>::load(embed, (int64_t)tok * H + k);
+  __syncthreads();
+  norm_row<T>(xr, H, gain, eps, xn + (int64_t)m * ldxn);
+}
+
+hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
+                             const float *gain, float eps, float *x, void *xn, int64_t ldxn,
+                             hipStream_t s) {
+  if (bf16)
+    k_embed_norm<bf16_t><<<M, 256, 0, s>>>((const bf16_t *)embed, rowinfo, H, gain, eps, x,
+                                           (bf16_t *)xn, ldxn);
+  else
+    k_embed_norm<float><<<M, 256, 0, s>>>((const float *)embed, rowinfo, H, gain, eps, x,
+                                          (float *)xn, ldxn);
+  return hipGetLastError();
+}
+
+// x += sum of split-K partials; xn = RMSNorm(x) * gain
+template <typename T>
+__global__ __launch_bounds__(256) void k_residual_norm(const float *part, int splits, int H,
+                                                       int64_t ldpart, const float *gain, float eps,
+                                                       float *x, T *xn, int64_t ldxn) {
+  const int m = blockIdx.x;
+  float *xr = x + (int64_t)m * H;
+  for (int k = threadIdx.x; k < H; k += 256) {
+    float acc = 0.f;
+    for (int sp = 0; sp < splits; ++sp) acc += part[((int64_t)sp * kRowPad + m) * ldpart + k];
+    xr[k] += acc;
+  }
+  __syncthreads();
+  norm_row<T>(xr, H, gain, eps, xn + (int64_t)m * ldxn);
+}
+
+hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int M, int H,
+                                int64_t ldpart, const float *gain, float eps, float *x, void *xn,
+                                int64_t ldxn, hipStream_t s) {
+  if (bf16)
+    k_residual_norm<bf16_t><<<M, 256, 0, s>>>(part, splits, H, ldpart, gain, eps, x, (bf16_t *)xn,
+                                              ldxn);
+  else
+    k_residual_norm<float><<<M, 256, 0, s>>>(part, splits, H, ldpart, gain, eps, x, (float *)xn,
+                                             ldxn);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// QKV epilogue: reduce split-K partials, rotate Q and K, round, write Q to
+// the query buffer and K/V of row m to cache slot P + m (values transposed)
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__global__ __launch_bounds__(64) void k_qkv_post(const float *part, int splits, int nq, int nkv,
+                                                 int hd, int64_t ldpart, const float *rope,
+                                                 const int32_t *kv_len, T *qbuf, int64_t ldq,
+                                                 T *cache, int layer, int64_t cap) {
+  const int m = blockIdx.x, hh = blockIdx.y;
+  const int half = hd / 2;
+  const int P = *kv_len;
+  const int64_t slot = P + m;
+  const int64_t plane = cap * hd;
+  auto col_sum = [&](int64_t c) {
+    float acc = 0.f;
+    for (int sp = 0; sp < splits; ++sp) acc += part[((int64_t)sp * kRowPad + m) * ldpart + c];
+    return acc;
+  };
+  const bool isq = hh < nq;
+  const int64_t c0 = isq ? (int64_t)hh * hd : (int64_t)nq * hd + (int64_t)(hh - nq) * hd;
+  for (int i = threadIdx.x; i < half; i += 64) {
+    float a = col_sum(c0 + i), b = col_sum(c0 + i + half);
+    float c = rope[((int64_t)m * half + i) * 2 + 0], s = rope[((int64_t)m * half + i) * 2 + 1];
+    float ra = a * c - b * s, rb = a * s + b * c;
+    if (isq) {
+      Elem<T>::store(qbuf, (int64_t)m * ldq + c0 + i, ra);
+      Elem<T>::store(qbuf, (int64_t)m * ldq + c0 + i + half, rb);
+    } else {
+      const int g = hh - nq;
+      T *kp = cache + ((int64_t)(layer * 2 + 0) * nkv + g) * plane + slot * hd;
+      Elem<T>::store(kp, i, ra);
+      Elem<T>::store(kp, i + half, rb);
+    }
+  }
+  if (!isq) {
+    const int g = hh - nq;
+    const int64_t cv = (int64_t)nq * hd + (int64_t)nkv * hd + (int64_t)g * hd;
+    T *vp = cache + ((int64_t)(layer * 2 + 1) * nkv + g) * plane;
+    for (int i = threadIdx.x; i < hd; i += 64) Elem<T>::store(vp, (int64_t)i * cap + slot, col_sum(cv + i));
+  }
+}
+
+hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int M, int nq, int nkv, int hd,
+                           int64_t ldpart, const float *rope, const int32_t *kv_len, void *qbuf,
+                           int64_t ldq, void *cache, int layer, int64_t cap, hipStream_t s) {
+  dim3 grid(M, nq + nkv);
+  if (bf16)
+    k_qkv_post<bf16_t><<<grid, 64, 0, s>>>(part, splits, nq, nkv, hd, ldpart, rope, kv_len,
+                                           (bf16_t *)qbuf, ldq, (bf16_t *)cache, layer, cap);
+  else
+    k_qkv_post<float><<<grid, 64, 0, s>>>(part, splits, nq, nkv, hd, ldpart, rope, kv_len,
+                                          (float *)qbuf, ldq, (float *)cache, layer, cap);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// greedy argmax per row + acceptance
+// ---------------------------------------------------------------------------
+
+__device__ inline bool better(float v, int i, float bv, int bi) {
+  return v > bv || (v == bv && i < bi);
+}
+
+// one block per row: reduce the lm_head tile partials
+__global__ __launch_bounds__(256) void k_argmax_rows(const ArgmaxPart *amax, int nparts,
+                                                     int32_t *pred, int32_t *nanflag) {
+  const int m = blockIdx.x;
+  float bv = -INFINITY;
+  int bi = 0x7FFFFFFF, nan = 0;
+  for (int t = threadIdx.x; t < nparts; t += 256) {
+    ArgmaxPart p = amax[(int64_t)t * kRowPad + m];
+    nan |= p.nan;
+    if (p.idx != 0x7FFFFFFF && better(p.v, p.idx, bv, bi)) {
+      bv = p.v;
+      bi = p.idx;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    float ov = __shfl_xor(bv, o, 64);
+    int oi = __shfl_xor(bi, o, 64);
+    nan |= __shfl_xor(nan, o, 64);
+    if (better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  __shared__ float sv[4];
+  __shared__ int si[4], sn[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) {
+    sv[w] = bv;
+    si[w] = bi;
+    sn[w] = nan;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < 4; ++k) {
+      nan |= sn[k];
+      if (better(sv[k], si[k], bv, bi)) {
+        bv = sv[k];
+        bi = si[k];
+      }
+    }
+    pred[m] = bi == 0x7FFFFFFF ? -1 : bi;
+    nanflag[m] = nan;
+  }
+}
+
+// single thread: longest matching prefix (linear) or greedy walk (tree)
+__global__ void k_accept(const pf_draft *d, const int32_t *pred, const int32_t *nanflag, int rows,
+                         int tree, pf_verify_result *res) {
+  if (threadIdx.x != 0) return;
+  const int n = min(d->n_nodes, rows);
+  int status = 0;
+  for (int j = 0; j < rows; ++j) {
+    res->pred[j] = pred[j];
+    if (j < n && nanflag[j]) status |= PF_VSTATUS_NAN;
+  }
+  int cur = 0, len = 0;
+  res->path[0] = 0;
+  for (;;) {
+    const int want = pred[cur];
+    int nxt = -1;
+    if (tree) {
+      for (int u = 1; u < n; ++u)
+        if (d->parent[u] == cur && d->token[u] == want) {
+          nxt = u;
+          break;
+        }
+    } else if (cur + 1 < n && d->token[cur + 1] == want) {
+      nxt = cur + 1;
+    }
+    if (nxt < 0) break;
+    ++len;
+    res->path[len] = nxt;
+    res->out_tokens[len - 1] = d->token[nxt];
+    cur = nxt;
+  }
+  res->accept_len = len;
+  res->bonus = pred[cur];
+  res->out_tokens[len] = pred[cur];
+  res->status |= status;
+}
+
+hipError_t launch_argmax_accept(const ArgmaxPart *amax, int nparts, int rows, int tree,
+                                const pf_draft *draft, int32_t *pred, pf_verify_result *res,
+                                hipStream_t s) {
+  k_argmax_rows<<<rows, 256, 0, s>>>(amax, nparts, pred, pred + kRowPad);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_accept<<<1, 64, 0, s>>>(draft, pred, pred + kRowPad, rows, tree, res);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// commit: tree compaction (read every path row, barrier, write), lengths,
+// context append
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_commit(const pf_verify_result *res, T *cache, int nkv,
+                                                int hd, int64_t cap, int tree, int32_t *kv_len,
+                                                int32_t *ctx_tokens, int32_t *ctx_len,
+                                                int64_t ctx_cap) {
+  const int len = res->accept_len;
+  const int64_t P = res->kv_base;
+  if (tree) {
+    // block b: layer b / (2*nkv), plane (b % (2*nkv))
+    const int b = blockIdx.x;
+    const int kvsel = (b / nkv) & 1;
+    T *plane = cache + (int64_t)b * cap * hd;
+    __shared__ float buf[PF_MAX_NODES * 128];
+    const int cnt = (len + 1) * hd;
+    for (int t = threadIdx.x; t < cnt; t += 256) {
+      int d = t / hd, i = t % hd;
+      int64_t src = P + res->path[d];
+      buf[t] = Elem<T>::load(plane, kvsel == 0 ? src * hd + i : (int64_t)i * cap + src);
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < cnt; t += 256) {
+      int d = t / hd, i = t % hd;
+      int64_t dst = P + d;
+      Elem<T>::store(plane, kvsel == 0 ? dst * hd + i : (int64_t)i * cap + dst, buf[t]);
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    *kv_len = (int32_t)(P + len + 1);
+    if (ctx_tokens) {
+      int c = *ctx_len;
+      if (c + len + 1 <= ctx_cap) {
+        for (int t = 0; t <= len; ++t) ctx_tokens[c + t] = res->out_tokens[t];
+        *ctx_len = c + len + 1;
+      }
+    }
+  }
+}
+
+hipError_t launch_commit(bool bf16, const pf_verify_result *res, void *cache, int L, int nkv,
+                         int hd, int64_t cap, int tree, int32_t *kv_len, int32_t *ctx_tokens,
+                         int32_t *ctx_len, int64_t ctx_cap, hipStream_t s) {
+  unsigned grid = tree ? (unsigned)(L * 2 * nkv) : 1u;
+  if (bf16)
+    k_commit<bf16_t><<<grid, 256, 0, s>>>(res, (bf16_t *)cache, nkv, hd, cap, tree, kv_len,
+                                          ctx_tokens, ctx_len, ctx_cap);
+  else
+    k_commit<float><<<grid, 256, 0, s>>>(res, (float *)cache, nkv, hd, cap, tree, kv_len,
+                                         ctx_tokens, ctx_len, ctx_cap);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// KV import / export between the logical layout [L][2][nkv][n][hd] and the
+// cache layout (keys [slot][i], values [i][slot])
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__global__ void k_kv_copy(int import_, T *cache, const T *src, T *dst, int L, int nkv, int hd,
+                          int64_t cap, int64_t start, int64_t n) {
+  const int64_t total = (int64_t)L * 2 * nkv * n * hd;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    int64_t i = t % hd;
+    int64_t r = (t / hd) % n;
+    int64_t p = t / ((int64_t)hd * n);  // plane index (l*2 + kv)*nkv + g
+    int kvsel = (int)((p / nkv) & 1);
+    int64_t slot = start + r;
+    int64_t ci = p * cap * hd + (kvsel == 0 ? slot * hd + i : i * cap + slot);
+    if (import_)
+      cache[ci] = src[t];
+    else
+      dst[t] = cache[ci];
+  }
+}
+
+hipError_t launch_kv_copy(bool bf16, bool import_, void *cache, const void *src, void *dst, int L,
+                          int nkv, int hd, int64_t cap, int64_t start, int64_t n, hipStream_t s) {
+  int64_t total = (int64_t)L * 2 * nkv * n * hd;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) blocks = 1;
+  if (bf16)
+    k_kv_copy<bf16_t><<<(unsigned)blocks, 256, 0, s>>>(import_, (bf16_t *)cache,
+                                                       (const bf16_t *)src, (bf16_t *)dst, L, nkv,
+                                                       hd, cap, start, n);
+  else
+    k_kv_copy<float><<<(unsigned)blocks, 256, 0, s>>>(import_, (float *)cache, (const float *)src,
+                                                      (float *)dst, L, nkv, hd, cap, start, n);
+  return hipGetLastError();
+}
+
+__global__ void k_set_int(int32_t *p, int32_t v) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) *p = v;
+}
+
+hipError_t launch_set_int(int32_t *p, int32_t v, hipStream_t s) {
+  k_set_int<<<1, 64, 0, s>>>(p, v);
+  return hipGetLastError();
+}
+
+}  // namespace pf
