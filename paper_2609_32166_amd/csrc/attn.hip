@@ -30,6 +30,7 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   const int h = blockIdx.y;
   const int g = h / a.group;
   const int s = blockIdx.x;
+  const int row0 = blockIdx.z * RT * 16;  // first query row of this wave
 
   const int P = *a.kv_len;
   const int M = a.M;
@@ -55,64 +56,77 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
     uint4 qf[RT][NDS];
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
-      const T *qrow = (const T *)a.q + (int64_t)(r * 16 + (lane & 15)) * a.ldq + h * HD;
+      const int jr = min(row0 + r * 16 + (lane & 15), kRowPad - 1);
+      const T *qrow = (const T *)a.q + (int64_t)jr * a.ldq + h * HD;
 #pragma unroll
       for (int d = 0; d < NDS; ++d) qf[r][d] = *(const uint4 *)(qrow + d * KF + q * E);
     }
     const T *kplane = (const T *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.n_kv + g) * a.plane;
     const T *vplane = (const T *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.n_kv + g) * a.plane;
+    const uint32_t plane_bytes = (uint32_t)(a.plane * sizeof(T));
+    const rsrc_t kr = make_rsrc(kplane, plane_bytes);
+    const rsrc_t vr = make_rsrc(vplane, plane_bytes);
     const float sc = a.scale_log2;
+    const int nchunks = (k1 - k0 + KC - 1) / KC;
 
-    for (int kc = k0; kc < k1; kc += KC) {
-      // K rows carried by this lane's A-operand row, per key sub-group
-      uint4 kf[NCG][NDS];
+    // two chunk slots: compute one while the other's K/V loads are in flight.
+    // Chunks past the range load out of the resource (zeros, no traffic) and
+    // their keys are masked, so they add nothing.
+    uint4 kf[2][NCG][NDS], vf[2][NDT];
+    auto load = [&](int slot, int c) {
+      const int kc = k0 + c * KC;
+      const bool in = c < nchunks;
 #pragma unroll
-      for (int c = 0; c < NCG; ++c) {
-        int r = lane & 15;
-        int key = kc + E * (r >> 2) + 4 * c + (r & 3);
-        const T *krow = kplane + (int64_t)key * HD;
+      for (int cg = 0; cg < NCG; ++cg) {
+        const int r = lane & 15;
+        const int key = kc + E * (r >> 2) + 4 * cg + (r & 3);
 #pragma unroll
-        for (int d = 0; d < NDS; ++d) kf[c][d] = *(const uint4 *)(krow + d * KF + q * E);
+        for (int d = 0; d < NDS; ++d)
+          kf[slot][cg][d] = bload16(
+              kr, in ? (uint32_t)(((int64_t)key * HD + d * KF + q * E) * sizeof(T)) : kOOB);
       }
-      // V^T fragments: dim t*16 + lane%16, keys kc + q*E .. +E (zero past kend)
-      uint4 vf[NDT];
-      const bool vpart = kc + KC > kend;
 #pragma unroll
-      for (int t = 0; t < NDT; ++t) {
-        const T *vrow = vplane + (int64_t)(t * 16 + (lane & 15)) * a.cap + kc + q * E;
-        vf[t] = *(const uint4 *)vrow;
-        if (vpart) {
+      for (int t = 0; t < NDT; ++t)
+        vf[slot][t] = bload16(
+            vr, in ? (uint32_t)(((int64_t)(t * 16 + (lane & 15)) * a.cap + kc + q * E) * sizeof(T))
+                   : kOOB);
+    };
+    auto compute = [&](int slot, int c) {
+      const int kc = k0 + c * KC;
+      if (kc + KC > kend) {  // zero value columns of keys past the end of the cache
+#pragma unroll
+        for (int t = 0; t < NDT; ++t) {
           union {
             uint4 v;
             T e[E];
           } u;
-          u.v = vf[t];
+          u.v = vf[slot][t];
 #pragma unroll
           for (int e = 0; e < E; ++e)
             if (kc + q * E + e >= kend) memset(&u.e[e], 0, sizeof(T));
-          vf[t] = u.v;
+          vf[slot][t] = u.v;
         }
       }
 #pragma unroll
       for (int r = 0; r < RT; ++r) {
-        const int j = r * 16 + (lane & 15);  // query row of this lane
+        const int j = row0 + r * 16 + (lane & 15);  // query row of this lane
         float sv[E];
 #pragma unroll
-        for (int c = 0; c < NCG; ++c) {
+        for (int cg = 0; cg < NCG; ++cg) {
           f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int d = 0; d < NDS; ++d) acc = mma<T>(kf[c][d], qf[r][d], acc);
+          for (int d = 0; d < NDS; ++d) acc = mma<T>(kf[slot][cg][d], qf[r][d], acc);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) sv[4 * c + i] = acc[i];
+          for (int i = 0; i < 4; ++i) sv[4 * cg + i] = acc[i];
         }
-        // keys of this lane: kc + q*E + e, e = 4*c + i
+        // keys of this lane: kc + q*E + e, e = 4*cg + i
         float cmax = -INFINITY;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          int key = kc + q * E + e;
+          const int key = kc + q * E + e;
           bool vis = key < k1;
           if (vis && key >= P) {
-            int di = key - P;
+            const int di = key - P;
             vis = a.tree ? (j < 64 && ((a.anc[j] >> di) & 1ull)) : (di <= j);
           }
           sv[e] = vis ? sv[e] * sc : -INFINITY;
@@ -129,7 +143,7 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
         float psum = 0.f;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          float p = sv[e] == -INFINITY ? 0.f : exp2f(sv[e] - m_new);
+          const float p = sv[e] == -INFINITY ? 0.f : exp2f(sv[e] - m_new);
           Elem<T>::store(pu.e, e, p);
           psum += p;
         }
@@ -138,9 +152,21 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
 #pragma unroll
         for (int t = 0; t < NDT; ++t) {
           o[r][t] *= alpha;
-          o[r][t] = mma<T>(vf[t], pu.v, o[r][t]);
+          o[r][t] = mma<T>(vf[slot][t], pu.v, o[r][t]);
         }
       }
+    };
+    load(0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    load(1, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int c = 0; c < nchunks; c += 2) {
+      compute(0, c);
+      load(0, c + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1, c + 1);
+      load(1, c + 3);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
@@ -150,7 +176,7 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
     float l = l_run[r];
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);
-    const int j = r * 16 + (lane & 15);
+    const int j = row0 + r * 16 + (lane & 15);
     if (j >= M) continue;
 #pragma unroll
     for (int t = 0; t < NDT; ++t)
@@ -163,7 +189,9 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   }
 }
 
-// Merge the key-range partials of one (row, head) and round the result.
+// Merge the key-range partials of one (row, head) and round the result:
+// lane s reads split s's (max, sum); the output sum over splits keeps eight
+// loads in flight per lane.
 template <typename T, int HD>
 __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
   const int j = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
@@ -171,20 +199,37 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
   const float *po = a.part_o + ((int64_t)h * a.n_splits * kRowPad) * HD;
   const int P = *a.kv_len;
   const int used = min(a.n_splits, (P + a.M + a.chunk_keys - 1) / a.chunk_keys);
-  float mx = -INFINITY;
-  for (int s = 0; s < used; ++s) mx = fmaxf(mx, pml[((int64_t)s * kRowPad + j) * 2]);
-  float den = 0.f;
+  float m = -INFINITY, l = 0.f;
+  if (lane < used) {
+    m = pml[((int64_t)lane * kRowPad + j) * 2];
+    l = pml[((int64_t)lane * kRowPad + j) * 2 + 1];
+  }
+  const float mx = wave_max(m);
+  const float w = m == -INFINITY ? 0.f : exp2f(m - mx);
+  const float den = wave_sum(w * l);
+  __shared__ float ws[64];
+  ws[lane] = w;
+  __syncthreads();
   float acc[HD / 64];
 #pragma unroll
   for (int i = 0; i < HD / 64; ++i) acc[i] = 0.f;
-  for (int s = 0; s < used; ++s) {
-    float m = pml[((int64_t)s * kRowPad + j) * 2];
-    if (m == -INFINITY) continue;
-    float w = exp2f(m - mx);
-    den += w * pml[((int64_t)s * kRowPad + j) * 2 + 1];
+  int s = 0;
+  for (; s + 8 <= used; s += 8) {
+    float v[8][HD / 64];
 #pragma unroll
-    for (int i = 0; i < HD / 64; ++i) acc[i] += w * po[((int64_t)s * kRowPad + j) * HD + lane + 64 * i];
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int i = 0; i < HD / 64; ++i)
+        v[u][i] = po[((int64_t)(s + u) * kRowPad + j) * HD + lane + 64 * i];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int i = 0; i < HD / 64; ++i) acc[i] += ws[s + u] * v[u][i];
   }
+  for (; s < used; ++s)
+#pragma unroll
+    for (int i = 0; i < HD / 64; ++i)
+      acc[i] += ws[s] * po[((int64_t)s * kRowPad + j) * HD + lane + 64 * i];
   T *out = (T *)a.out + (int64_t)j * a.ldout + h * HD;
 #pragma unroll
   for (int i = 0; i < HD / 64; ++i) Elem<T>::store(out, lane + 64 * i, acc[i] / den);
@@ -192,13 +237,15 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
 
 template <typename T, int HD>
 static hipError_t attn_t(int rt, const AttnArgs &a, hipStream_t s) {
-  dim3 grid(a.n_splits, a.n_kv * a.group), block(64);
-  switch (rt) {
+  // at most three 16-row query tiles per wave (register budget); more rows
+  // are spread over blockIdx.z
+  const int per = rt <= 3 ? rt : 2;
+  const int groups = (rt + per - 1) / per;
+  dim3 grid(a.n_splits, a.n_kv * a.group, groups), block(64);
+  switch (per) {
     case 1: k_attn<T, 1, HD><<<grid, block, 0, s>>>(a); break;
     case 2: k_attn<T, 2, HD><<<grid, block, 0, s>>>(a); break;
     case 3: k_attn<T, 3, HD><<<grid, block, 0, s>>>(a); break;
-    case 4: k_attn<T, 4, HD><<<grid, block, 0, s>>>(a); break;
-    case 5: k_attn<T, 5, HD><<<grid, block, 0, s>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();

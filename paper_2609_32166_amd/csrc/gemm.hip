@@ -121,37 +121,37 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  uint4 wa[kU][NT], xa[kU][MT], wb[kU][NT], xb[kU][MT];
-  auto load = [&](uint4(&wv)[kU][NT], uint4(&xv)[kU][MT], int64_t blk) {
+  // ring of kU fragment slots: compute slot u, then refill it with the
+  // fragment kU positions ahead. Loads past the wave's range go out of the
+  // buffer resource's bounds and return zeros without memory traffic, so the
+  // loop body is straight-line and the wait counts stay static.
+  uint4 wv[kU][NT], xv[kU][MT];
+  auto load = [&](int u, int64_t i) {
+    const bool in = i < n;
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+      wv[u][j] = bload16(wr, in && wbase[j] != kOOB ? wbase[j] + (uint32_t)(i * 1024) : kOOB);
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+      xv[u][m] = bload16(xr, in ? xbase[m] + (uint32_t)(i * 4 * E * sizeof(T)) : kOOB);
+  };
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    load(u, u);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int64_t i = 0; i < n; i += kU) {
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
-      int64_t i = blk * kU + u;
-      bool in = i < n;
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-        wv[u][j] = bload16(wr, in && wbase[j] != kOOB ? wbase[j] + (uint32_t)(i * 1024) : kOOB);
-#pragma unroll
-      for (int m = 0; m < MT; ++m)
-        xv[u][m] = bload16(xr, in ? xbase[m] + (uint32_t)(i * 4 * E * sizeof(T)) : kOOB);
-    }
-  };
-  auto compute = [&](uint4(&wv)[kU][NT], uint4(&xv)[kU][MT]) {
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
 #pragma unroll
       for (int m = 0; m < MT; ++m)
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[m][j] = mma<T>(wv[u][j], xv[u][m], acc[m][j]);
-  };
-
-  const int64_t nblk = (n + kU - 1) / kU;
-  load(wa, xa, 0);
-  for (int64_t b = 0; b < nblk; b += 2) {
-    load(wb, xb, b + 1);
-    compute(wa, xa);
-    if (b + 1 >= nblk) break;
-    load(wa, xa, b + 2);
-    compute(wb, xb);
+      load(u, i + kU + u);
+      // keep slot order: the refill of slot u must not sink below later slots,
+      // or the next pass would have to wait for every load in flight
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 
   // reduce the four waves' partial sums in LDS (fixed order: wave 0..3)

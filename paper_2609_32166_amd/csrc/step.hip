@@ -102,20 +102,54 @@ hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinf
   return hipGetLastError();
 }
 
-// x += sum of split-K partials; xn = RMSNorm(x) * gain
+// x += sum of split-K partials (fixed order); xn = RMSNorm(x) * gain. One
+// block per row; every thread keeps eight partial loads in flight.
 template <typename T>
 __global__ __launch_bounds__(256) void k_residual_norm(const float *part, int splits, int H,
                                                        int64_t ldpart, const float *gain, float eps,
                                                        float *x, T *xn, int64_t ldxn) {
   const int m = blockIdx.x;
-  float *xr = x + (int64_t)m * H;
-  for (int k = threadIdx.x; k < H; k += 256) {
-    float acc = 0.f;
-    for (int sp = 0; sp < splits; ++sp) acc += part[((int64_t)sp * kRowPad + m) * ldpart + k];
-    xr[k] += acc;
+  float4 *xr = (float4 *)(x + (int64_t)m * H);
+  const int H4 = H / 4;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < H4; c += 256) {
+    float4 acc = xr[c];
+    int sp = 0;
+    for (; sp + 8 <= splits; sp += 8) {
+      float4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        v[u] = ((const float4 *)(part + ((int64_t)(sp + u) * kRowPad + m) * ldpart))[c];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        acc.x += v[u].x;
+        acc.y += v[u].y;
+        acc.z += v[u].z;
+        acc.w += v[u].w;
+      }
+    }
+    for (; sp < splits; ++sp) {
+      float4 v = ((const float4 *)(part + ((int64_t)sp * kRowPad + m) * ldpart))[c];
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    xr[c] = acc;
+    ss += acc.x * acc.x + acc.y * acc.y + acc.z * acc.z + acc.w * acc.w;
   }
-  __syncthreads();
-  norm_row<T>(xr, H, gain, eps, xn + (int64_t)m * ldxn);
+  __shared__ float sh[4];
+  ss = block_sum256(ss, sh);
+  const float inv = 1.0f / sqrtf(ss / (float)H + eps);
+  T *out = xn + (int64_t)m * ldxn;
+  for (int c = threadIdx.x; c < H4; c += 256) {
+    float4 v = xr[c];
+    float4 g = ((const float4 *)gain)[c];
+    Elem<T>::store(out, 4 * c + 0, v.x * inv * g.x);
+    Elem<T>::store(out, 4 * c + 1, v.y * inv * g.y);
+    Elem<T>::store(out, 4 * c + 2, v.z * inv * g.z);
+    Elem<T>::store(out, 4 * c + 3, v.w * inv * g.w);
+  }
 }
 
 hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int M, int H,
@@ -147,7 +181,15 @@ __global__ __launch_bounds__(64) void k_qkv_post(const float *part, int splits, 
   const int64_t plane = cap * hd;
   auto col_sum = [&](int64_t c) {
     float acc = 0.f;
-    for (int sp = 0; sp < splits; ++sp) acc += part[((int64_t)sp * kRowPad + m) * ldpart + c];
+    int sp = 0;
+    for (; sp + 8 <= splits; sp += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = part[((int64_t)(sp + u) * kRowPad + m) * ldpart + c];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += v[u];
+    }
+    for (; sp < splits; ++sp) acc += part[((int64_t)sp * kRowPad + m) * ldpart + c];
     return acc;
   };
   const bool isq = hh < nq;
