@@ -107,8 +107,20 @@ template <typename T> pf_status dev_alloc(T **p, int64_t bytes, int64_t *total) 
   return PF_OK;
 }
 
+void prefill_free(pf_model *m) {
+  void *ptrs[] = {m->pre_x, m->pre_y, m->pre_rope, m->pre_apo, m->pre_apml, m->pre_xn,
+                  m->pre_qb, m->pre_attn, m->pre_act, m->pre_rowinfo, m->pre_status};
+  for (void *p : ptrs)
+    if (p) (void)hipFree(p);
+  m->pre_x = m->pre_y = m->pre_rope = m->pre_apo = m->pre_apml = nullptr;
+  m->pre_xn = m->pre_qb = m->pre_attn = m->pre_act = nullptr;
+  m->pre_rowinfo = m->pre_status = nullptr;
+  m->pre_rows = 0;
+}
+
 void model_free(pf_model *m) {
   if (!m) return;
+  prefill_free(m);
   void *ptrs[] = {m->wqkv, m->wo, m->wgu, m->wd, m->lm, m->embed, m->attn_norm, m->ffn_norm,
                   m->final_norm, m->inv_freq, m->x, m->xn, m->qb, m->attn, m->act, m->part,
                   m->apart_o, m->apart_ml, m->amax, m->rope, m->rowinfo, m->pred, m->flags};
@@ -537,8 +549,8 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     g.out = m->part;
     g.ldo = q + 2 * kvd;
     PROF(1, launch_gemm(bf, EPI_PARTIAL, MT, g, hs));
-    PROF(2, launch_qkv_post(bf, m->part, g.splits, M, nq, nkv, hd, g.ldo, m->rope, kv->len, m->qb, q,
-                           kv->data, l, kv->capacity, hs));
+    PROF(2, launch_qkv_post(bf, m->part, g.splits, kRowPad, M, nq, nkv, hd, g.ldo, m->rope, kv->len,
+                            m->qb, q, kv->data, l, kv->capacity, hs));
     // attention
     AttnArgs at{};
     at.q = m->qb;
@@ -551,6 +563,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     at.group = nq / nkv;
     at.head_dim = hd;
     at.M = M;
+    at.rowpad = kRowPad;
     at.kv_len = kv->len;
     at.n_splits = n_splits;
     at.chunk_keys = chunk;
@@ -575,7 +588,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     go.out = m->part;
     go.ldo = H;
     PROF(4, launch_gemm(bf, EPI_PARTIAL, MT, go, hs));
-    PROF(5, launch_residual_norm(bf, m->part, go.splits, M, H, H, m->ffn_norm + (int64_t)l * H, eps,
+    PROF(5, launch_residual_norm(bf, m->part, go.splits, kRowPad, M, H, H, m->ffn_norm + (int64_t)l * H, eps,
                                 m->x, m->xn, Hp, hs));
     // gate/up + SwiGLU
     GemmArgs gg{};
@@ -605,7 +618,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     gd.ldo = H;
     PROF(7, launch_gemm(bf, EPI_PARTIAL, MT, gd, hs));
     const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
-    PROF(5, launch_residual_norm(bf, m->part, gd.splits, M, H, H, next_gain, eps, m->x, m->xn, Hp,
+    PROF(5, launch_residual_norm(bf, m->part, gd.splits, kRowPad, M, H, H, next_gain, eps, m->x, m->xn, Hp,
                                 hs));
   }
   // lm_head + greedy argmax partials
@@ -676,10 +689,179 @@ pf_status pf_kv_commit(pf_kv_cache *kv, const pf_verify_result *res, pf_context 
   return ok();
 }
 
+constexpr int kPrefillSplits = 8;
+
+static pf_status prefill_alloc(pf_model *m, int64_t rows) {
+  if (m->pre_rows >= rows) return PF_OK;
+  prefill_free(m);
+  const pf_model_config &c = m->cfg;
+  const int kf = frag_k_of(m);
+  const int64_t R = roundup(rows, 128), H = c.hidden, q = (int64_t)c.n_heads * c.head_dim,
+                kv = (int64_t)c.n_kv_heads * c.head_dim;
+  const int64_t Hp = roundup(H, kf), qp = roundup(q, kf), Fp = roundup(c.ffn, kf);
+  pf_status r;
+#define PALLOC(ptr, bytes)                       \
+  if ((r = dev_alloc(&(ptr), (bytes), nullptr))) { \
+    prefill_free(m);                             \
+    return r;                                    \
+  }
+  PALLOC(m->pre_x, R * H * 4);
+  PALLOC(m->pre_y, R * (q + 2 * kv) * 4);
+  PALLOC(m->pre_rope, R * c.head_dim * 4);
+  PALLOC(m->pre_apo, (int64_t)c.n_heads * kPrefillSplits * R * c.head_dim * 4);
+  PALLOC(m->pre_apml, (int64_t)c.n_heads * kPrefillSplits * R * 2 * 4);
+  PALLOC(m->pre_xn, R * Hp * m->esz);
+  PALLOC(m->pre_qb, R * q * m->esz);
+  PALLOC(m->pre_attn, R * qp * m->esz);
+  PALLOC(m->pre_act, R * Fp * m->esz);
+  PALLOC(m->pre_rowinfo, R * 4 * 4);
+  PALLOC(m->pre_status, 64);
+#undef PALLOC
+  void *zero[] = {m->pre_xn, m->pre_qb, m->pre_attn, m->pre_act, m->pre_status};
+  int64_t zb[] = {R * Hp * m->esz, R * q * m->esz, R * qp * m->esz, R * Fp * m->esz, 64};
+  for (int i = 0; i < 5; ++i) HIPCHK(hipMemset(zero[i], 0, zb[i]));
+  HIPCHK(hipDeviceSynchronize());
+  m->pre_rows = R;
+  return PF_OK;
+}
+
 pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_t n, int32_t chunk,
                      float *logits_last, pf_stream s) {
-  (void)m; (void)kv; (void)tokens; (void)n; (void)chunk; (void)logits_last; (void)s;
-  return fail(PF_EUNSUPPORTED, "pf_prefill: not built yet");
+  if (!m || !tokens) return fail(PF_EINVAL, "pf_prefill: null pointer");
+  if (pf_status r = kv_check(kv, "pf_prefill")) return r;
+  if (pf_status r = model_kv_match(m, kv, "pf_prefill")) return r;
+  if (n < 1 || chunk < 1 || chunk > 4096)
+    return fail(PF_EINVAL, "pf_prefill: n %d / chunk %d out of range", n, chunk);
+  if (kv->pending) return fail(PF_ESTATE, "pf_prefill: a verify step is not committed");
+  if (kv->host_bound + n > kv->capacity)
+    return fail(PF_ECAPACITY, "pf_prefill: cache bound %lld + %d > capacity %lld",
+                (long long)kv->host_bound, n, (long long)kv->capacity);
+  const int C = chunk < n ? chunk : n;
+  if (pf_status r = prefill_alloc(m, C)) return r;
+  const pf_model_config &c = m->cfg;
+  const bool bf = is_bf16(m);
+  const int kf = frag_k_of(m);
+  const int L = c.n_layers, H = c.hidden, hd = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads;
+  const int64_t q = (int64_t)nq * hd, kvd = (int64_t)nkv * hd, F = c.ffn, V = c.vocab;
+  const int64_t Hp = roundup(H, kf), qp = roundup(q, kf), Fp = roundup(F, kf);
+  const int R = (int)m->pre_rows;
+  const float eps = (float)c.rms_eps;
+  hipStream_t hs = st(s);
+  const uint64_t *rowmask = (const uint64_t *)(m->rowinfo + kRowPad * 4);
+
+  for (int c0 = 0; c0 < n; c0 += C) {
+    const int rows = n - c0 < C ? n - c0 : C;
+    HIPCHK(launch_prefill_rows(tokens + c0, rows, (int)V, kv->len, m->inv_freq, hd, m->pre_rowinfo,
+                               m->pre_rope, m->pre_status, hs));
+    HIPCHK(launch_embed_norm(bf, m->embed, m->pre_rowinfo, rows, H, m->attn_norm, eps, m->pre_x,
+                             m->pre_xn, Hp, hs));
+    const int64_t keys_max = kv->host_bound + c0 + rows;
+    int ck = (int)roundup((keys_max + kPrefillSplits - 1) / kPrefillSplits, 32);
+    if (ck < 128) ck = 128;
+    const int nsp = (int)((keys_max + ck - 1) / ck);
+    for (int l = 0; l < L; ++l) {
+      BigGemmArgs g{};
+      g.W = (const char *)m->wqkv + (int64_t)l * m->pqkv.bytes();
+      g.W_bytes = m->pqkv.bytes();
+      g.KFr = m->pqkv.KFr;
+      g.NTtot = m->pqkv.NT;
+      g.X = m->pre_xn;
+      g.ldx = Hp;
+      g.x_rows = R;
+      g.M = rows;
+      g.y = m->pre_y;
+      g.ldy = q + 2 * kvd;
+      HIPCHK(launch_gemm_big(bf, BIG_STORE, g, hs));
+      HIPCHK(launch_qkv_post(bf, m->pre_y, 1, R, rows, nq, nkv, hd, q + 2 * kvd, m->pre_rope,
+                             kv->len, m->pre_qb, q, kv->data, l, kv->capacity, hs));
+      AttnArgs at{};
+      at.q = m->pre_qb;
+      at.ldq = q;
+      at.cache = kv->data;
+      at.plane = kv->capacity * hd;
+      at.cap = kv->capacity;
+      at.layer = l;
+      at.n_kv = nkv;
+      at.group = nq / nkv;
+      at.head_dim = hd;
+      at.M = rows;
+      at.rowpad = R;
+      at.kv_len = kv->len;
+      at.n_splits = nsp;
+      at.chunk_keys = ck;
+      at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
+      at.tree = 0;
+      at.anc = rowmask;
+      at.part_o = m->pre_apo;
+      at.part_ml = m->pre_apml;
+      at.out = m->pre_attn;
+      at.ldout = qp;
+      HIPCHK(launch_attn(bf, (rows + 15) / 16, at, hs));
+      BigGemmArgs go{};
+      go.W = (const char *)m->wo + (int64_t)l * m->po.bytes();
+      go.W_bytes = m->po.bytes();
+      go.KFr = m->po.KFr;
+      go.NTtot = m->po.NT;
+      go.X = m->pre_attn;
+      go.ldx = qp;
+      go.x_rows = R;
+      go.M = rows;
+      go.y = m->pre_x;
+      go.ldy = H;
+      HIPCHK(launch_gemm_big(bf, BIG_RESID, go, hs));
+      HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, m->ffn_norm + (int64_t)l * H, eps,
+                                  m->pre_x, m->pre_xn, Hp, hs));
+      BigGemmArgs gg{};
+      gg.W = (const char *)m->wgu + (int64_t)l * m->pgu.bytes();
+      gg.W_bytes = m->pgu.bytes();
+      gg.KFr = m->pgu.KFr;
+      gg.NTtot = m->pgu.NT;
+      gg.X = m->pre_xn;
+      gg.ldx = Hp;
+      gg.x_rows = R;
+      gg.M = rows;
+      gg.act = m->pre_act;
+      gg.ldact = Fp;
+      gg.up_tile_off = F / 16;
+      HIPCHK(launch_gemm_big(bf, BIG_SWIGLU, gg, hs));
+      BigGemmArgs gd{};
+      gd.W = (const char *)m->wd + (int64_t)l * m->pd.bytes();
+      gd.W_bytes = m->pd.bytes();
+      gd.KFr = m->pd.KFr;
+      gd.NTtot = m->pd.NT;
+      gd.X = m->pre_act;
+      gd.ldx = Fp;
+      gd.x_rows = R;
+      gd.M = rows;
+      gd.y = m->pre_x;
+      gd.ldy = H;
+      HIPCHK(launch_gemm_big(bf, BIG_RESID, gd, hs));
+      const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
+      HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, next_gain, eps, m->pre_x,
+                                  m->pre_xn, Hp, hs));
+    }
+    HIPCHK(launch_add_int(kv->len, rows, hs));
+    if (c0 + rows == n && logits_last) {
+      // last token: final-norm row -> lm_head (one row through the verify GEMM)
+      HIPCHK(launch_copy_row((const char *)m->pre_xn + (int64_t)(rows - 1) * Hp * m->esz, m->xn,
+                             Hp * m->esz, hs));
+      GemmArgs gl{};
+      gl.W = m->lm;
+      gl.W_bytes = m->plm.bytes();
+      gl.KFr = m->plm.KFr;
+      gl.NTtot = m->plm.NT;
+      gl.X = m->xn;
+      gl.ldx = Hp;
+      gl.M = 1;
+      gl.splits = 1;
+      gl.amax = m->amax;
+      gl.logits = logits_last;
+      gl.ldlog = V;
+      HIPCHK(launch_gemm(bf, EPI_ARGMAX, 1, gl, hs));
+    }
+  }
+  kv->host_bound += n;
+  return ok();
 }
 
 }  // extern "C"

@@ -38,8 +38,8 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   const int k0 = s * a.chunk_keys;
   const int k1 = min(k0 + a.chunk_keys, kend);
 
-  float *po = a.part_o + (((int64_t)h * a.n_splits + s) * kRowPad) * HD;
-  float *pml = a.part_ml + (((int64_t)h * a.n_splits + s) * kRowPad) * 2;
+  float *po = a.part_o + (((int64_t)h * a.n_splits + s) * a.rowpad) * HD;
+  float *pml = a.part_ml + (((int64_t)h * a.n_splits + s) * a.rowpad) * 2;
 
   float m_run[RT], l_run[RT];
   f32x4 o[RT][NDT];
@@ -56,7 +56,7 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
     uint4 qf[RT][NDS];
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
-      const int jr = min(row0 + r * 16 + (lane & 15), kRowPad - 1);
+      const int jr = min(row0 + r * 16 + (lane & 15), a.rowpad - 1);
       const T *qrow = (const T *)a.q + (int64_t)jr * a.ldq + h * HD;
 #pragma unroll
       for (int d = 0; d < NDS; ++d) qf[r][d] = *(const uint4 *)(qrow + d * KF + q * E);
@@ -195,14 +195,14 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
 template <typename T, int HD>
 __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
   const int j = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
-  const float *pml = a.part_ml + ((int64_t)h * a.n_splits * kRowPad) * 2;
-  const float *po = a.part_o + ((int64_t)h * a.n_splits * kRowPad) * HD;
+  const float *pml = a.part_ml + ((int64_t)h * a.n_splits * a.rowpad) * 2;
+  const float *po = a.part_o + ((int64_t)h * a.n_splits * a.rowpad) * HD;
   const int P = *a.kv_len;
   const int used = min(a.n_splits, (P + a.M + a.chunk_keys - 1) / a.chunk_keys);
   float m = -INFINITY, l = 0.f;
   if (lane < used) {
-    m = pml[((int64_t)lane * kRowPad + j) * 2];
-    l = pml[((int64_t)lane * kRowPad + j) * 2 + 1];
+    m = pml[((int64_t)lane * a.rowpad + j) * 2];
+    l = pml[((int64_t)lane * a.rowpad + j) * 2 + 1];
   }
   const float mx = wave_max(m);
   const float w = m == -INFINITY ? 0.f : exp2f(m - mx);
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
     for (int u = 0; u < 8; ++u)
 #pragma unroll
       for (int i = 0; i < HD / 64; ++i)
-        v[u][i] = po[((int64_t)(s + u) * kRowPad + j) * HD + lane + 64 * i];
+        v[u][i] = po[((int64_t)(s + u) * a.rowpad + j) * HD + lane + 64 * i];
 #pragma unroll
     for (int u = 0; u < 8; ++u)
 #pragma unroll
@@ -229,7 +229,7 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
   for (; s < used; ++s)
 #pragma unroll
     for (int i = 0; i < HD / 64; ++i)
-      acc[i] += ws[s] * po[((int64_t)s * kRowPad + j) * HD + lane + 64 * i];
+      acc[i] += ws[s] * po[((int64_t)s * a.rowpad + j) * HD + lane + 64 * i];
   T *out = (T *)a.out + (int64_t)j * a.ldout + h * HD;
 #pragma unroll
   for (int i = 0; i < HD / 64; ++i) Elem<T>::store(out, lane + 64 * i, acc[i] / den);

@@ -53,7 +53,9 @@ struct AttnArgs {
   int64_t plane;        // capacity * head_dim
   int64_t cap;          // capacity
   int layer, n_kv, group, head_dim;
-  int M;                // verify rows
+  int M;                // query rows (verify rows or prefill chunk rows)
+  int rowpad;           // row stride of q and of the partial buffers (>= rows, rows of q
+                        // past M must be readable)
   const int32_t *kv_len;  // P (device)
   int n_splits;         // key ranges (grid.x)
   int chunk_keys;       // keys per range (multiple of 32)
@@ -85,12 +87,38 @@ hipError_t launch_prep(const StepArgs &a, hipStream_t s);
 hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
                              const float *gain, float eps, float *x, void *xn, int64_t ldxn,
                              hipStream_t s);
-hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int M, int nq, int nkv, int hd,
-                           int64_t ldpart, const float *rope, const int32_t *kv_len, void *qbuf,
-                           int64_t ldq, void *cache, int layer, int64_t cap, hipStream_t s);
-hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int M, int H,
+hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int rowpad, int M, int nq,
+                           int nkv, int hd, int64_t ldpart, const float *rope, const int32_t *kv_len,
+                           void *qbuf, int64_t ldq, void *cache, int layer, int64_t cap,
+                           hipStream_t s);
+hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
                                 int64_t ldpart, const float *gain, float eps, float *x, void *xn,
                                 int64_t ldxn, hipStream_t s);
+// prefill rows: tokens[i] at position P + i (P = *kv_len), RoPE table, rowinfo
+hipError_t launch_prefill_rows(const int32_t *tokens, int n, int V, const int32_t *kv_len,
+                               const double *inv_freq, int hd, int32_t *rowinfo, float *rope,
+                               int32_t *status, hipStream_t s);
+hipError_t launch_add_int(int32_t *p, int32_t v, hipStream_t s);
+hipError_t launch_copy_row(const void *src, void *dst, int64_t bytes, hipStream_t s);
+
+// tiled GEMM for prefill chunks (gemm_big.hip): Y[M x N] = X[M x K] W^T,
+// 128 x 128 block tiles, epilogues below
+enum BigEpi { BIG_STORE = 0, BIG_RESID = 1, BIG_SWIGLU = 2 };
+struct BigGemmArgs {
+  const void *W;
+  int64_t W_bytes;
+  int64_t KFr, NTtot;
+  const void *X;
+  int64_t ldx;
+  int64_t x_rows;       // rows allocated in X (multiple of 128)
+  int M;                // valid rows
+  float *y;             // BIG_STORE: y[m*ldy + n]; BIG_RESID: y[m*ldy + n] += result
+  int64_t ldy;
+  void *act;            // BIG_SWIGLU: act[m*ldact + n]
+  int64_t ldact;
+  int64_t up_tile_off;  // BIG_SWIGLU: up tile index offset (F/16)
+};
+hipError_t launch_gemm_big(bool bf16, int epi, const BigGemmArgs &a, hipStream_t s);
 hipError_t launch_argmax_accept(const ArgmaxPart *amax, int nparts, int rows, int tree,
                                 const pf_draft *draft, int32_t *pred, pf_verify_result *res,
                                 hipStream_t s);

@@ -149,6 +149,12 @@ struct pf_model {
   int32_t *pred = nullptr;   // [kRowPad]
   int32_t *flags = nullptr;  // [4] device status words
   int64_t bytes = 0;
+  // prefill work buffers (allocated on first use, sized for pre_rows rows)
+  int64_t pre_rows = 0;
+  float *pre_x = nullptr, *pre_y = nullptr, *pre_rope = nullptr, *pre_apo = nullptr,
+        *pre_apml = nullptr;
+  void *pre_xn = nullptr, *pre_qb = nullptr, *pre_attn = nullptr, *pre_act = nullptr;
+  int32_t *pre_rowinfo = nullptr, *pre_status = nullptr;
 };
 
 struct pf_store {

@@ -105,7 +105,7 @@ hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinf
 // x += sum of split-K partials (fixed order); xn = RMSNorm(x) * gain. One
 // block per row; every thread keeps eight partial loads in flight.
 template <typename T>
-__global__ __launch_bounds__(256) void k_residual_norm(const float *part, int splits, int H,
+__global__ __launch_bounds__(256) void k_residual_norm(const float *part, int splits, int rowpad, int H,
                                                        int64_t ldpart, const float *gain, float eps,
                                                        float *x, T *xn, int64_t ldxn) {
   const int m = blockIdx.x;
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(256) void k_residual_norm(const float *part, int sp
       float4 v[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        v[u] = ((const float4 *)(part + ((int64_t)(sp + u) * kRowPad + m) * ldpart))[c];
+        v[u] = ((const float4 *)(part + ((int64_t)(sp + u) * rowpad + m) * ldpart))[c];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         acc.x += v[u].x;
@@ -129,7 +129,7 @@ __global__ __launch_bounds__(256) void k_residual_norm(const float *part, int sp
       }
     }
     for (; sp < splits; ++sp) {
-      float4 v = ((const float4 *)(part + ((int64_t)sp * kRowPad + m) * ldpart))[c];
+      float4 v = ((const float4 *)(part + ((int64_t)sp * rowpad + m) * ldpart))[c];
       acc.x += v.x;
       acc.y += v.y;
       acc.z += v.z;
@@ -152,15 +152,15 @@ __global__ __launch_bounds__(256) void k_residual_norm(const float *part, int sp
   }
 }
 
-hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int M, int H,
+hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
                                 int64_t ldpart, const float *gain, float eps, float *x, void *xn,
                                 int64_t ldxn, hipStream_t s) {
   if (bf16)
-    k_residual_norm<bf16_t><<<M, 256, 0, s>>>(part, splits, H, ldpart, gain, eps, x, (bf16_t *)xn,
-                                              ldxn);
+    k_residual_norm<bf16_t><<<M, 256, 0, s>>>(part, splits, rowpad, H, ldpart, gain, eps, x,
+                                              (bf16_t *)xn, ldxn);
   else
-    k_residual_norm<float><<<M, 256, 0, s>>>(part, splits, H, ldpart, gain, eps, x, (float *)xn,
-                                             ldxn);
+    k_residual_norm<float><<<M, 256, 0, s>>>(part, splits, rowpad, H, ldpart, gain, eps, x,
+                                             (float *)xn, ldxn);
   return hipGetLastError();
 }
 
@@ -170,7 +170,8 @@ hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int M,
 // ---------------------------------------------------------------------------
 
 template <typename T>
-__global__ __launch_bounds__(64) void k_qkv_post(const float *part, int splits, int nq, int nkv,
+__global__ __launch_bounds__(64) void k_qkv_post(const float *part, int splits, int rowpad, int nq,
+                                                 int nkv,
                                                  int hd, int64_t ldpart, const float *rope,
                                                  const int32_t *kv_len, T *qbuf, int64_t ldq,
                                                  T *cache, int layer, int64_t cap) {
@@ -185,11 +186,11 @@ __global__ __launch_bounds__(64) void k_qkv_post(const float *part, int splits, 
     for (; sp + 8 <= splits; sp += 8) {
       float v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = part[((int64_t)(sp + u) * kRowPad + m) * ldpart + c];
+      for (int u = 0; u < 8; ++u) v[u] = part[((int64_t)(sp + u) * rowpad + m) * ldpart + c];
 #pragma unroll
       for (int u = 0; u < 8; ++u) acc += v[u];
     }
-    for (; sp < splits; ++sp) acc += part[((int64_t)sp * kRowPad + m) * ldpart + c];
+    for (; sp < splits; ++sp) acc += part[((int64_t)sp * rowpad + m) * ldpart + c];
     return acc;
   };
   const bool isq = hh < nq;
@@ -216,15 +217,16 @@ __global__ __launch_bounds__(64) void k_qkv_post(const float *part, int splits, 
   }
 }
 
-hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int M, int nq, int nkv, int hd,
-                           int64_t ldpart, const float *rope, const int32_t *kv_len, void *qbuf,
-                           int64_t ldq, void *cache, int layer, int64_t cap, hipStream_t s) {
+hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int rowpad, int M, int nq,
+                           int nkv, int hd, int64_t ldpart, const float *rope, const int32_t *kv_len,
+                           void *qbuf, int64_t ldq, void *cache, int layer, int64_t cap,
+                           hipStream_t s) {
   dim3 grid(M, nq + nkv);
   if (bf16)
-    k_qkv_post<bf16_t><<<grid, 64, 0, s>>>(part, splits, nq, nkv, hd, ldpart, rope, kv_len,
+    k_qkv_post<bf16_t><<<grid, 64, 0, s>>>(part, splits, rowpad, nq, nkv, hd, ldpart, rope, kv_len,
                                            (bf16_t *)qbuf, ldq, (bf16_t *)cache, layer, cap);
   else
-    k_qkv_post<float><<<grid, 64, 0, s>>>(part, splits, nq, nkv, hd, ldpart, rope, kv_len,
+    k_qkv_post<float><<<grid, 64, 0, s>>>(part, splits, rowpad, nq, nkv, hd, ldpart, rope, kv_len,
                                           (float *)qbuf, ldq, (float *)cache, layer, cap);
   return hipGetLastError();
 }
@@ -422,6 +424,60 @@ hipError_t launch_kv_copy(bool bf16, bool import_, void *cache, const void *src,
   else
     k_kv_copy<float><<<(unsigned)blocks, 256, 0, s>>>(import_, (float *)cache, (const float *)src,
                                                       (float *)dst, L, nkv, hd, cap, start, n);
+  return hipGetLastError();
+}
+
+// prefill rows: row i holds tokens[i] at position P + i
+__global__ __launch_bounds__(256) void k_prefill_rows(const int32_t *tokens, int n, int V,
+                                                      const int32_t *kv_len, const double *inv_freq,
+                                                      int hd, int32_t *rowinfo, float *rope,
+                                                      int32_t *status) {
+  const int P = *kv_len;
+  const int half = hd / 2;
+  const int i = blockIdx.x;
+  if (i >= n) return;
+  if (threadIdx.x == 0) {
+    int tok = tokens[i];
+    if (tok < 0 || tok >= V) {  // never index the embedding out of range
+      tok = 0;
+      atomicOr(status, PF_VSTATUS_BAD_TOKEN);
+    }
+    rowinfo[i * 4 + 0] = tok;
+    rowinfo[i * 4 + 1] = i;
+    rowinfo[i * 4 + 2] = 1;
+    rowinfo[i * 4 + 3] = 0;
+  }
+  for (int t = threadIdx.x; t < half; t += blockDim.x) {
+    double ang = (double)(P + i) * inv_freq[t];
+    rope[((int64_t)i * half + t) * 2 + 0] = (float)cos(ang);
+    rope[((int64_t)i * half + t) * 2 + 1] = (float)sin(ang);
+  }
+}
+
+hipError_t launch_prefill_rows(const int32_t *tokens, int n, int V, const int32_t *kv_len,
+                               const double *inv_freq, int hd, int32_t *rowinfo, float *rope,
+                               int32_t *status, hipStream_t s) {
+  k_prefill_rows<<<n, 64, 0, s>>>(tokens, n, V, kv_len, inv_freq, hd, rowinfo, rope, status);
+  return hipGetLastError();
+}
+
+__global__ void k_add_int(int32_t *p, int32_t v) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) *p += v;
+}
+
+hipError_t launch_add_int(int32_t *p, int32_t v, hipStream_t s) {
+  k_add_int<<<1, 64, 0, s>>>(p, v);
+  return hipGetLastError();
+}
+
+__global__ void k_copy_bytes(const uint4 *src, uint4 *dst, int64_t n16) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n16;
+       i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
+hipError_t launch_copy_row(const void *src, void *dst, int64_t bytes, hipStream_t s) {
+  k_copy_bytes<<<1, 256, 0, s>>>((const uint4 *)src, (uint4 *)dst, bytes / 16);
   return hipGetLastError();
 }
 
