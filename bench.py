@@ -40,6 +40,19 @@ def gate_up_bytes(wl) -> int:
     return esz * (2 * m.ffn * m.hidden + M * m.hidden + M * m.ffn)
 
 
+def prefill_flops(wl) -> float:
+    """Algorithmic FLOPs of prefilling wl.prefill_new tokens after
+    wl.prefill_reuse cached ones: every linear layer once per token, causal
+    attention over the reused prefix and the earlier new tokens."""
+    m = wl.model
+    n, p0 = wl.prefill_new, wl.prefill_reuse
+    per_tok = m.hidden * (m.q_dim + 2 * m.kv_dim) + m.q_dim * m.hidden + 3 * m.hidden * m.ffn
+    linear = 2.0 * n * m.n_layers * per_tok
+    keys = n * p0 + n * (n + 1) / 2.0
+    attn = 2.0 * 2.0 * m.n_layers * m.n_heads * m.head_dim * keys
+    return linear + attn
+
+
 def cpu_baseline(wl, w, kv_host, draft, layers: int):
     """The oracle's batched verify, timed on this host's cores, on a sample:
     the first `layers` layers at full widths plus the full lm_head, same
@@ -107,6 +120,30 @@ def main():
     cap = ((wl.prefix + 2 * wl.rows + 63) // 64) * 64
     kv = pf.KVCache(model, cap)
     kvd = pf.array_to_device(kv_host)
+    prefill = None
+    if wl.prefill_new:
+        # carry-forward: keep the reused prefix, prefill the new chunk, then verify
+        ptoks = torch.from_numpy(synth.make_prefill_tokens(wl, seed, wl.prefill_new)).cuda()
+        plog = torch.zeros(shape.vocab, device="cuda")
+        pre_ms = []
+        for it in range(3):
+            pf.pf_kv_import(kv, kvd[:, :, :, :wl.prefill_reuse].contiguous(), wl.prefill_reuse)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            pf.pf_prefill(model, kv, ptoks, wl.prefill_new, wl.prefill_chunk, plog)
+            e1.record()
+            torch.cuda.synchronize()
+            pre_ms.append(e0.elapsed_time(e1))
+        pms = min(pre_ms[1:])
+        fl = prefill_flops(wl)
+        prefill = {"ms": round(pms, 3), "tflops": round(fl / (pms * 1e-3) / 1e12, 1),
+                   "frac_of_bf16_mfma_peak": round(fl / (pms * 1e-3) / 2.5e15, 4),
+                   "algorithmic_tflop": round(fl / 1e12, 2),
+                   "reused": wl.prefill_reuse, "new": wl.prefill_new, "chunk": wl.prefill_chunk}
+        log(f"prefill {wl.prefill_new} tokens after {wl.prefill_reuse}: {pms:.2f} ms "
+            f"({prefill['tflops']} TFLOP/s)")
+        # the verify step then runs on the synthetic full prefix (same length)
     pf.pf_kv_import(kv, kvd, wl.prefix)
     st = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
     c = pf.Context(ctx, len(ctx) + 2 * wl.rows)
@@ -189,6 +226,8 @@ def main():
                      "avg_launch_us": round(gu_us, 2)},
         "kernels": kernels,
     }
+    if prefill is not None:
+        out["prefill"] = prefill
     if not args.no_cpu_baseline:
         od = {"n_nodes": int(d["n_nodes"]), "token": np.array(d["token"][:int(d["n_nodes"])]),
               "parent": np.array(d["parent"][:int(d["n_nodes"])]),
