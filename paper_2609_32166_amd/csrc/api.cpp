@@ -310,9 +310,9 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
     return fail(PF_EUNSUPPORTED, "pf_model_create: head_dim %d not in {64,128}", c.head_dim);
   if (c.n_heads % c.n_kv_heads || c.n_heads / c.n_kv_heads > 8)
     return fail(PF_EUNSUPPORTED, "pf_model_create: n_heads/n_kv_heads must be an integer <= 8");
-  if (c.hidden % 128 || c.ffn % 16 || c.vocab % 16)
+  if (c.hidden % 32 || c.ffn % 16 || c.vocab % 16)
     return fail(PF_EUNSUPPORTED,
-                "pf_model_create: hidden must be a multiple of 128, ffn and vocab of 16");
+                "pf_model_create: hidden must be a multiple of 32, ffn and vocab of 16");
   if (!(c.rms_eps >= 0) || !(c.rope_theta > 0)) return fail(PF_EINVAL, "pf_model_create: eps/theta");
   if (!w->embed || !w->lm_head || !w->wqkv || !w->wo || !w->wgu || !w->wd || !w->attn_norm ||
       !w->ffn_norm || !w->final_norm)
@@ -361,8 +361,10 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
     if (e > part) part = e;
   }
   {
-    const int64_t gq = (m->pqkv.NT + 7) / 8, go = (m->po.NT + 7) / 8, gd = (m->pd.NT + 7) / 8;
-    const int64_t gg = (F / 16 + 3) / 4;
+    const int64_t gq = fgemm_groups(FEPI_QKV, m->pqkv.NT, 0);
+    const int64_t go = fgemm_groups(FEPI_RESID, m->po.NT, 0);
+    const int64_t gd = fgemm_groups(FEPI_RESID, m->pd.NT, 0);
+    const int64_t gg = fgemm_groups(FEPI_SWIGLU, 0, F / 16);
     for (int mt = 1; mt <= 5; ++mt) {
       int64_t e = std::max(
           std::max((int64_t)fused_splits(gq, m->pqkv.KFr, mt) * (q + 2 * kv),
@@ -389,7 +391,7 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
   ALLOC(m->rowinfo, kRowPad * 4 * 4 + kRowPad * 8);
   ALLOC(m->pred, 2 * kRowPad * 4);
   ALLOC(m->flags, 64);
-  ALLOC(m->ssg, ((H + 127) / 128) * kRowPad * 4);
+  ALLOC(m->ssg, ((H + 31) / 32) * kRowPad * 4);
   ALLOC(m->counters, kFusedCounters * 4);
 #undef ALLOC
   m->bytes = tot;
@@ -558,7 +560,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   sa.rowmask = rowmask;
   sa.rope = m->rope;
   PROF(0, launch_prep(sa, hs));
-  const int ssg = H / 128;
+  const int ssg = H / 32;
   PROF(0, launch_embed_ss(bf, m->embed, m->rowinfo, M, H, m->x, m->ssg, hs));
 
   // attention geometry: key ranges over P + rows keys (P <= host bound)
@@ -587,7 +589,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   for (int l = 0; l < L; ++l) {
     // QKV projection: RMSNorm folded into the X staging; RoPE + KV append fused
     FusedArgs g = fused(m->wqkv, m->pqkv, l);
-    g.splits = fused_splits((m->pqkv.NT + 7) / 8, m->pqkv.KFr, MT);
+    g.splits = fused_splits(fgemm_groups(FEPI_QKV, m->pqkv.NT, 0), m->pqkv.KFr, MT);
     g.gain = m->attn_norm + (int64_t)l * H;
     g.ldpart = q + 2 * kvd;
     g.hd = hd;
@@ -626,7 +628,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     PROF(3, launch_attn(bf, MT, at, hs));
     // output projection + residual (+ per-group sums of squares for the next norm)
     FusedArgs go = fused(m->wo, m->po, l);
-    go.splits = fused_splits((m->po.NT + 7) / 8, m->po.KFr, MT);
+    go.splits = fused_splits(fgemm_groups(FEPI_RESID, m->po.NT, 0), m->po.KFr, MT);
     go.xb = m->attn;
     go.ldx = qp;
     go.ldpart = H;
@@ -634,7 +636,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     PROF(4, launch_fgemm(bf, FEPI_RESID, XS_BF16, MT, go, hs));
     // gate/up + SwiGLU, RMSNorm folded into the X staging
     FusedArgs gg = fused(m->wgu, m->pgu, l);
-    gg.splits = fused_splits((F / 16 + 3) / 4, m->pgu.KFr, MT);
+    gg.splits = fused_splits(fgemm_groups(FEPI_SWIGLU, 0, F / 16), m->pgu.KFr, MT);
     gg.gain = m->ffn_norm + (int64_t)l * H;
     gg.ldpart = 2 * F;
     gg.up_tile_off = F / 16;
@@ -643,7 +645,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     PROF(6, launch_fgemm(bf, FEPI_SWIGLU, XS_NORM, MT, gg, hs));
     // down projection + residual
     FusedArgs gd = fused(m->wd, m->pd, l);
-    gd.splits = fused_splits((m->pd.NT + 7) / 8, m->pd.KFr, MT);
+    gd.splits = fused_splits(fgemm_groups(FEPI_RESID, m->pd.NT, 0), m->pd.KFr, MT);
     gd.xb = m->act;
     gd.ldx = Fp;
     gd.ldpart = H;

@@ -15,8 +15,13 @@
 //             RESID-> residual add into x, per-group sum of squares
 //             SWIGLU-> silu(gate) * up, rounded
 //
-// A column group is 8 tiles (128 columns; for SwiGLU 4 gate + 4 up tiles),
-// so a block owns exactly one group and one k range.
+// Two block layouts. SwiGLU: a block owns 4 gate tiles and their 4 up tiles
+// (one pair per wave, all waves on the block's k range, X reused 4x from
+// LDS). QKV / output / down projections (N in the low thousands): a block owns
+// one tile pair and its 4 waves split the block's k range four ways, reducing
+// through LDS; the narrow column group keeps the split count -- and so the
+// last block's reduction -- small. For QKV the pair is tiles j and j+4 of one
+// head, so RoPE's (i, i + head_dim/2) pairs stay inside the group.
 #include "kernels.h"
 
 namespace pf {
@@ -40,7 +45,8 @@ __global__ __launch_bounds__(256) void k_fgemm(FusedArgs a) {
   const int nfr = (int)(r1 - r0);
   const int xrow = nfr * 64 + kXPad;  // LDS bytes per X row
 
-  // weight tiles of this wave
+  constexpr bool WIDE = EPI == FEPI_SWIGLU;
+  // weight tiles of this wave and its k fragments [f0, f1) (relative to r0)
   int64_t tile[2];
   bool tv[2];
 #pragma unroll
@@ -49,21 +55,29 @@ __global__ __launch_bounds__(256) void k_fgemm(FusedArgs a) {
       const int64_t gt = (int64_t)grp * 4 + wid;  // gate tile
       tile[j] = j == 0 ? gt : gt + a.up_tile_off;
       tv[j] = gt < a.up_tile_off;
+    } else if (EPI == FEPI_QKV) {
+      // head grp/(hd/32), tiles j0 and j0 + hd/32 of that head
+      const int half_tiles = a.hd / 32;
+      const int64_t head = grp / half_tiles, j0 = grp % half_tiles;
+      tile[j] = head * (a.hd / 16) + j0 + j * half_tiles;
+      tv[j] = tile[j] < a.NTtot;
     } else {
-      tile[j] = (int64_t)grp * 8 + wid * 2 + j;
+      tile[j] = (int64_t)grp * 2 + j;
       tv[j] = tile[j] < a.NTtot;
     }
   }
+  const int f0 = WIDE ? 0 : wid * nfr / 4, f1 = WIDE ? nfr : (wid + 1) * nfr / 4;
+  const int nw = f1 - f0;
   const rsrc_t wr = make_rsrc(a.W, (uint32_t)a.W_bytes);
   uint32_t wbase[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j)
-    wbase[j] = tv[j] ? (uint32_t)(((tile[j] * a.KFr + r0) * 64 + lane) * 16) : kOOB;
+    wbase[j] = tv[j] ? (uint32_t)(((tile[j] * a.KFr + r0 + f0) * 64 + lane) * 16) : kOOB;
 
   // start the weight stream before staging X: the weights do not depend on it
   uint4 wv[kU][2];
   auto load = [&](int u, int i) {
-    const bool in = i < nfr;
+    const bool in = i < nw;
 #pragma unroll
     for (int j = 0; j < 2; ++j)
       wv[u][j] = bload16(wr, in && wbase[j] != kOOB ? wbase[j] + (uint32_t)i * 1024u : kOOB);
@@ -124,13 +138,13 @@ __global__ __launch_bounds__(256) void k_fgemm(FusedArgs a) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int q = lane >> 4;
-  const unsigned char *xl = lds + (lane & 15) * xrow + q * 16;
-  for (int i = 0; i < nfr; i += kU) {
+  const unsigned char *xl = lds + (lane & 15) * xrow + q * 16 + f0 * 64;
+  for (int i = 0; i < nw; i += kU) {
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       // past the k range the weight slot holds zeros (out-of-bounds loads),
       // so the product adds nothing; the X read is clamped into the slice
-      const int f = i + u < nfr ? i + u : nfr - 1;
+      const int f = i + u < nw ? i + u : (nw > 0 ? nw - 1 : 0);
       uint4 xv[MT];
 #pragma unroll
       for (int m = 0; m < MT; ++m) xv[m] = *(const uint4 *)(xl + m * 16 * xrow + f * 64);
@@ -143,10 +157,33 @@ __global__ __launch_bounds__(256) void k_fgemm(FusedArgs a) {
     }
   }
 
+  if (!WIDE) {
+    // the four waves hold partial sums over different k quarters: reduce in
+    // LDS (fixed order) into wave 0
+    __shared__ f32x4 red[3][MT][2][64];
+    __syncthreads();
+    if (wid > 0) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) red[wid - 1][m][j][lane] = acc[m][j];
+    }
+    __syncthreads();
+    if (wid == 0) {
+#pragma unroll
+      for (int w = 0; w < 3; ++w)
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[m][j] += red[w][m][j][lane];
+    }
+  }
+
   // ---- split partials: lane holds D[n = tile*16 + 4q + i][row = m*16 + lane%16] ----
   float *part = a.part + (int64_t)s * kRowPad * a.ldpart;
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
+    if (!WIDE && wid != 0) break;
     const int row = m * 16 + (lane & 15);
     if (row >= a.M) continue;
 #pragma unroll
@@ -178,24 +215,32 @@ __global__ __launch_bounds__(256) void k_fgemm(FusedArgs a) {
   if (!is_last) return;
 
   const int M = a.M;
+  // sum of the split partials of (row m, column c), eight loads in flight
   auto colsum = [&](int m, int64_t c) {
+    const float *p = a.part + (int64_t)m * a.ldpart + c;
+    const int64_t st = (int64_t)kRowPad * a.ldpart;
     float v = 0.f;
-    for (int sp = 0; sp < a.splits; ++sp) v += a.part[((int64_t)sp * kRowPad + m) * a.ldpart + c];
+    int sp = 0;
+    for (; sp + 8 <= a.splits; sp += 8) {
+      float t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = p[(sp + u) * st];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v += t[u];
+    }
+    for (; sp < a.splits; ++sp) v += p[sp * st];
     return v;
   };
   if (EPI == FEPI_QKV) {
-    // columns [grp*128, grp*128+128) hold whole heads of head_dim hd
+    // columns of tile 0 (i) and tile 1 (i + hd/2) of one head: RoPE pairs
     const int hd = a.hd, half = hd / 2;
-    const int64_t c0 = (int64_t)grp * 128;
     const int64_t qd = (int64_t)a.nq * hd, kvd = (int64_t)a.nkv * hd;
     const int P = *a.kv_len;
     const int64_t plane = a.cap * hd;
-    const int ncol = (int)min((int64_t)128, a.NTtot * 16 - c0);
-    for (int t = threadIdx.x; t < M * ncol / 2; t += 256) {
-      const int m = t / (ncol / 2);
-      const int r = t % (ncol / 2);
-      const int hl = r / half, i = r % half;  // head within the group, pair index
-      const int64_t hc = c0 + (int64_t)hl * hd;  // first column of the head
+    const int64_t hc = (tile[0] / (hd / 16)) * hd;  // first column of the head
+    const int ib = (int)(tile[0] * 16 - hc);        // first pair index of the group
+    for (int t = threadIdx.x; t < M * 16; t += 256) {
+      const int m = t / 16, i = ib + t % 16;
       const float va = colsum(m, hc + i), vb = colsum(m, hc + i + half);
       const int64_t slot = P + m;
       if (hc < qd + kvd) {
@@ -220,15 +265,14 @@ __global__ __launch_bounds__(256) void k_fgemm(FusedArgs a) {
       }
     }
   } else if (EPI == FEPI_RESID) {
-    // x[:, group] += sum of splits; per-row sum of squares of the new x over the group
-    const int64_t c0 = (int64_t)grp * 128;
-    const int ncol = (int)min((int64_t)128, a.NTtot * 16 - c0);
+    // x[:, 32 columns of this group] += sum of splits; per-row sum of squares
+    const int64_t c0 = (int64_t)grp * 32;
     for (int m = wid; m < M; m += 4) {
       float acc2 = 0.f;
-      for (int c = lane; c < ncol; c += 64) {
-        float v = a.xf[(int64_t)m * a.H + c0 + c] + colsum(m, c0 + c);
-        a.xf[(int64_t)m * a.H + c0 + c] = v;
-        acc2 += v * v;
+      if (lane < 32) {
+        const float v = a.xf[(int64_t)m * a.H + c0 + lane] + colsum(m, c0 + lane);
+        a.xf[(int64_t)m * a.H + c0 + lane] = v;
+        acc2 = v * v;
       }
       acc2 = wave_sum(acc2);
       if (lane == 0) a.ss_out[grp * kRowPad + m] = acc2;
@@ -243,6 +287,10 @@ __global__ __launch_bounds__(256) void k_fgemm(FusedArgs a) {
       Elem<T>::store((T *)a.act, (int64_t)m * a.ldact + c0 + c, silu(g) * u);
     }
   }
+}
+
+int64_t fgemm_groups(int epi, int64_t NTtot, int64_t up_tile_off) {
+  return epi == FEPI_SWIGLU ? (up_tile_off + 3) / 4 : (NTtot + 1) / 2;
 }
 
 int fgemm_lds_bytes(bool bf16, int mt, int64_t KFr, int splits) {
@@ -288,7 +336,7 @@ hipError_t fgemm_init() {
 
 template <typename T>
 static hipError_t fg_t(int epi, int xs, int mt, const FusedArgs &a, hipStream_t s) {
-  const int64_t groups = epi == FEPI_SWIGLU ? (a.up_tile_off + 3) / 4 : (a.NTtot + 7) / 8;
+  const int64_t groups = fgemm_groups(epi, a.NTtot, a.up_tile_off);
   dim3 grid((unsigned)groups, (unsigned)a.splits);
   const int lds = fgemm_lds_bytes(sizeof(T) == 2, mt, a.KFr, a.splits);
   if (epi == FEPI_QKV) return fg_mt<T, FEPI_QKV, XS_NORM>(mt, a, grid, lds, s);
@@ -301,7 +349,7 @@ hipError_t launch_fgemm(bool bf16, int epi, int xs, int mt, const FusedArgs &a, 
   return bf16 ? fg_t<bf16_t>(epi, xs, mt, a, s) : fg_t<float>(epi, xs, mt, a, s);
 }
 
-// x[m] = embed[token m]; per-group (128 columns) sums of squares of x
+// x[m] = embed[token m]; per-group (32 columns) sums of squares of x
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed_ss(const T *embed, const int32_t *rowinfo, int H,
                                                   float *x, float *ss) {
@@ -309,12 +357,13 @@ __global__ __launch_bounds__(256) void k_embed_ss(const T *embed, const int32_t 
   const int tok = rowinfo[m * 4];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   float *xr = x + (int64_t)m * H;
-  for (int g = wid; g < (H + 127) / 128; g += 4) {
+  for (int g = wid; g < H / 32; g += 4) {
     float acc2 = 0.f;
-    for (int c = g * 128 + lane; c < min(H, g * 128 + 128); c += 64) {
+    if (lane < 32) {
+      const int c = g * 32 + lane;
       const float v = Elem<T>::load(embed, (int64_t)tok * H + c);
       xr[c] = v;
-      acc2 += v * v;
+      acc2 = v * v;
     }
     acc2 = wave_sum(acc2);
     if (lane == 0) ss[g * kRowPad + m] = acc2;

@@ -179,6 +179,7 @@ struct FusedArgs {
   int64_t ldact;
 };
 int fgemm_lds_bytes(bool bf16, int mt, int64_t KFr, int splits);
+int64_t fgemm_groups(int epi, int64_t NTtot, int64_t up_tile_off);
 hipError_t fgemm_init();
 hipError_t launch_fgemm(bool bf16, int epi, int xs, int mt, const FusedArgs &a, hipStream_t s);
 hipError_t launch_embed_ss(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
