@@ -1,6 +1,5 @@
 // C-ABI layer of libpf: argument checks, the experience-store builder, model
 // creation (weight packing) and the launch sequence of one verify step.
-#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -65,17 +64,6 @@ int splits_for(int64_t nblocks, int64_t KFr) {
   return (int)s;
 }
 
-// split-K factor of a fused GEMM: about 768 blocks, at least two k fragments
-// per split, at most 64 KiB of staged X per block
-constexpr int kFusedCounters = 4096;
-int fused_splits(int64_t groups, int64_t KFr, int mt) {
-  int64_t s = (768 + groups - 1) / groups;
-  if (s > KFr / 2) s = KFr / 2;
-  if (s < 1) s = 1;
-  while (s < KFr && (int64_t)mt * 16 * (((KFr + s - 1) / s) * 64 + 16) > 64 * 1024) ++s;
-  return (int)s;
-}
-
 int64_t partial_blocks(const Packed &p) {
   int nt = gemm_tiles_per_block(EPI_PARTIAL);
   return (p.NT + nt - 1) / nt;
@@ -135,8 +123,7 @@ void model_free(pf_model *m) {
   prefill_free(m);
   void *ptrs[] = {m->wqkv, m->wo, m->wgu, m->wd, m->lm, m->embed, m->attn_norm, m->ffn_norm,
                   m->final_norm, m->inv_freq, m->x, m->xn, m->qb, m->attn, m->act, m->part,
-                  m->apart_o, m->apart_ml, m->amax, m->rope, m->rowinfo, m->pred, m->flags,
-                  m->ssg, m->counters};
+                  m->apart_o, m->apart_ml, m->amax, m->rope, m->rowinfo, m->pred, m->flags};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   delete m;
@@ -310,9 +297,8 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
     return fail(PF_EUNSUPPORTED, "pf_model_create: head_dim %d not in {64,128}", c.head_dim);
   if (c.n_heads % c.n_kv_heads || c.n_heads / c.n_kv_heads > 8)
     return fail(PF_EUNSUPPORTED, "pf_model_create: n_heads/n_kv_heads must be an integer <= 8");
-  if (c.hidden % 32 || c.ffn % 16 || c.vocab % 16)
-    return fail(PF_EUNSUPPORTED,
-                "pf_model_create: hidden must be a multiple of 32, ffn and vocab of 16");
+  if (c.hidden % 16 || c.ffn % 16 || c.vocab % 16)
+    return fail(PF_EUNSUPPORTED, "pf_model_create: hidden, ffn, vocab must be multiples of 16");
   if (!(c.rms_eps >= 0) || !(c.rope_theta > 0)) return fail(PF_EINVAL, "pf_model_create: eps/theta");
   if (!w->embed || !w->lm_head || !w->wqkv || !w->wo || !w->wgu || !w->wd || !w->attn_norm ||
       !w->ffn_norm || !w->final_norm)
@@ -360,21 +346,6 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
     int64_t e = (int64_t)splits_for(nb, p->KFr) * kRowPad * p->NT * 16;
     if (e > part) part = e;
   }
-  {
-    const int64_t gq = fgemm_groups(FEPI_QKV, m->pqkv.NT, 0);
-    const int64_t go = fgemm_groups(FEPI_RESID, m->po.NT, 0);
-    const int64_t gd = fgemm_groups(FEPI_RESID, m->pd.NT, 0);
-    const int64_t gg = fgemm_groups(FEPI_SWIGLU, 0, F / 16);
-    for (int mt = 1; mt <= 5; ++mt) {
-      int64_t e = std::max(
-          std::max((int64_t)fused_splits(gq, m->pqkv.KFr, mt) * (q + 2 * kv),
-                   (int64_t)fused_splits(go, m->po.KFr, mt) * H),
-          std::max((int64_t)fused_splits(gg, m->pgu.KFr, mt) * 2 * F,
-                   (int64_t)fused_splits(gd, m->pd.KFr, mt) * H));
-      e *= kRowPad;
-      if (e > part) part = e;
-    }
-  }
   m->part_elems = part;
   m->apart_rows = (int64_t)c.n_heads * kMaxSplitsAttn * kRowPad;
   m->amax_elems = ((m->plm.NT + 3) / 4) * kRowPad;
@@ -391,8 +362,6 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
   ALLOC(m->rowinfo, kRowPad * 4 * 4 + kRowPad * 8);
   ALLOC(m->pred, 2 * kRowPad * 4);
   ALLOC(m->flags, 64);
-  ALLOC(m->ssg, ((H + 31) / 32) * kRowPad * 4);
-  ALLOC(m->counters, kFusedCounters * 4);
 #undef ALLOC
   m->bytes = tot;
 
@@ -402,8 +371,6 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
   int64_t zb[] = {kRowPad * H * 4, kRowPad * Hp * m->esz, kRowPad * q * m->esz,
                   kRowPad * qp * m->esz, kRowPad * Fp * m->esz};
   for (int i = 0; i < 5 && e == hipSuccess; ++i) e = hipMemsetAsync(zero[i], 0, zb[i], hs);
-  if (e == hipSuccess) e = hipMemsetAsync(m->counters, 0, kFusedCounters * 4, hs);
-  if (e == hipSuccess) e = fgemm_init();
   if (e == hipSuccess) e = launch_pack(w->wqkv, q + 2 * kv, H, L, (q + 2 * kv) * H, bf, m->pqkv, m->wqkv, hs);
   if (e == hipSuccess) e = launch_pack(w->wo, H, q, L, H * q, bf, m->po, m->wo, hs);
   if (e == hipSuccess) e = launch_pack(w->wgu, 2 * F, H, L, 2 * F * H, bf, m->pgu, m->wgu, hs);
@@ -560,8 +527,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   sa.rowmask = rowmask;
   sa.rope = m->rope;
   PROF(0, launch_prep(sa, hs));
-  const int ssg = H / 32;
-  PROF(0, launch_embed_ss(bf, m->embed, m->rowinfo, M, H, m->x, m->ssg, hs));
+  PROF(0, launch_embed_norm(bf, m->embed, m->rowinfo, M, H, m->attn_norm, eps, m->x, m->xn, Hp, hs));
 
   // attention geometry: key ranges over P + rows keys (P <= host bound)
   const int64_t keys_max = kv->host_bound + rows;
@@ -569,39 +535,22 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   if (chunk < 128) chunk = 128;
   const int n_splits = (int)((keys_max + chunk - 1) / chunk);
 
-  auto fused = [&](const void *base, const Packed &pk, int64_t layer) {
-    FusedArgs f{};
-    f.W = (const char *)base + layer * pk.bytes();
-    f.W_bytes = pk.bytes();
-    f.KFr = pk.KFr;
-    f.NTtot = pk.NT;
-    f.M = M;
-    f.xf = m->x;
-    f.ss = m->ssg;
-    f.ss_groups = ssg;
-    f.eps = eps;
-    f.H = H;
-    f.part = m->part;
-    f.counters = m->counters;
-    return f;
-  };
-
   for (int l = 0; l < L; ++l) {
-    // QKV projection: RMSNorm folded into the X staging; RoPE + KV append fused
-    FusedArgs g = fused(m->wqkv, m->pqkv, l);
-    g.splits = fused_splits(fgemm_groups(FEPI_QKV, m->pqkv.NT, 0), m->pqkv.KFr, MT);
-    g.gain = m->attn_norm + (int64_t)l * H;
-    g.ldpart = q + 2 * kvd;
-    g.hd = hd;
-    g.nq = nq;
-    g.nkv = nkv;
-    g.layer = l;
-    g.kv_len = kv->len;
-    g.rope = m->rope;
-    g.qout = m->qb;
-    g.cache = kv->data;
-    g.cap = kv->capacity;
-    PROF(1, launch_fgemm(bf, FEPI_QKV, XS_NORM, MT, g, hs));
+    // QKV projection (split-K partials)
+    GemmArgs g{};
+    g.W = (const char *)m->wqkv + (int64_t)l * m->pqkv.bytes();
+    g.W_bytes = m->pqkv.bytes();
+    g.KFr = m->pqkv.KFr;
+    g.NTtot = m->pqkv.NT;
+    g.X = m->xn;
+    g.ldx = Hp;
+    g.M = M;
+    g.splits = splits_for(partial_blocks(m->pqkv), m->pqkv.KFr);
+    g.out = m->part;
+    g.ldo = q + 2 * kvd;
+    PROF(1, launch_gemm(bf, EPI_PARTIAL, MT, g, hs));
+    PROF(2, launch_qkv_post(bf, m->part, g.splits, kRowPad, M, nq, nkv, hd, g.ldo, m->rope, kv->len,
+                            m->qb, q, kv->data, l, kv->capacity, hs));
     // attention
     AttnArgs at{};
     at.q = m->qb;
@@ -626,33 +575,52 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     at.out = m->attn;
     at.ldout = qp;
     PROF(3, launch_attn(bf, MT, at, hs));
-    // output projection + residual (+ per-group sums of squares for the next norm)
-    FusedArgs go = fused(m->wo, m->po, l);
-    go.splits = fused_splits(fgemm_groups(FEPI_RESID, m->po.NT, 0), m->po.KFr, MT);
-    go.xb = m->attn;
+    // output projection + residual + FFN norm
+    GemmArgs go{};
+    go.W = (const char *)m->wo + (int64_t)l * m->po.bytes();
+    go.W_bytes = m->po.bytes();
+    go.KFr = m->po.KFr;
+    go.NTtot = m->po.NT;
+    go.X = m->attn;
     go.ldx = qp;
-    go.ldpart = H;
-    go.ss_out = m->ssg;
-    PROF(4, launch_fgemm(bf, FEPI_RESID, XS_BF16, MT, go, hs));
-    // gate/up + SwiGLU, RMSNorm folded into the X staging
-    FusedArgs gg = fused(m->wgu, m->pgu, l);
-    gg.splits = fused_splits(fgemm_groups(FEPI_SWIGLU, 0, F / 16), m->pgu.KFr, MT);
-    gg.gain = m->ffn_norm + (int64_t)l * H;
-    gg.ldpart = 2 * F;
-    gg.up_tile_off = F / 16;
+    go.M = M;
+    go.splits = splits_for(partial_blocks(m->po), m->po.KFr);
+    go.out = m->part;
+    go.ldo = H;
+    PROF(4, launch_gemm(bf, EPI_PARTIAL, MT, go, hs));
+    PROF(5, launch_residual_norm(bf, m->part, go.splits, kRowPad, M, H, H, m->ffn_norm + (int64_t)l * H, eps,
+                                m->x, m->xn, Hp, hs));
+    // gate/up + SwiGLU
+    GemmArgs gg{};
+    gg.W = (const char *)m->wgu + (int64_t)l * m->pgu.bytes();
+    gg.W_bytes = m->pgu.bytes();
+    gg.KFr = m->pgu.KFr;
+    gg.NTtot = m->pgu.NT;
+    gg.X = m->xn;
+    gg.ldx = Hp;
+    gg.M = M;
+    gg.splits = 1;
     gg.act = m->act;
     gg.ldact = Fp;
-    PROF(6, launch_fgemm(bf, FEPI_SWIGLU, XS_NORM, MT, gg, hs));
-    // down projection + residual
-    FusedArgs gd = fused(m->wd, m->pd, l);
-    gd.splits = fused_splits(fgemm_groups(FEPI_RESID, m->pd.NT, 0), m->pd.KFr, MT);
-    gd.xb = m->act;
+    gg.up_tile_off = F / 16;
+    PROF(6, launch_gemm(bf, EPI_SWIGLU, MT, gg, hs));
+    // down projection + residual + next norm
+    GemmArgs gd{};
+    gd.W = (const char *)m->wd + (int64_t)l * m->pd.bytes();
+    gd.W_bytes = m->pd.bytes();
+    gd.KFr = m->pd.KFr;
+    gd.NTtot = m->pd.NT;
+    gd.X = m->act;
     gd.ldx = Fp;
-    gd.ldpart = H;
-    gd.ss_out = m->ssg;
-    PROF(7, launch_fgemm(bf, FEPI_RESID, XS_BF16, MT, gd, hs));
+    gd.M = M;
+    gd.splits = splits_for(partial_blocks(m->pd), m->pd.KFr);
+    gd.out = m->part;
+    gd.ldo = H;
+    PROF(7, launch_gemm(bf, EPI_PARTIAL, MT, gd, hs));
+    const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
+    PROF(5, launch_residual_norm(bf, m->part, gd.splits, kRowPad, M, H, H, next_gain, eps, m->x, m->xn, Hp,
+                                hs));
   }
-  PROF(5, launch_norm_ss(bf, m->x, m->ssg, ssg, M, H, m->final_norm, eps, m->xn, Hp, hs));
   // lm_head + greedy argmax partials
   GemmArgs gl{};
   gl.W = m->lm;

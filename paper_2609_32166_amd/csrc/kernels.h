@@ -141,52 +141,6 @@ struct LookupArgs {
 };
 hipError_t launch_lookup(const LookupArgs &a, hipStream_t s);
 
-// fused verify GEMM (fgemm.hip)
-enum FusedEpi { FEPI_QKV = 0, FEPI_RESID = 1, FEPI_SWIGLU = 2 };
-enum XSource { XS_NORM = 0, XS_BF16 = 1 };
-constexpr int kFgemmMaxLds = 96 * 1024;  // dynamic LDS ceiling per block
-struct FusedArgs {
-  const void *W;
-  int64_t W_bytes, KFr, NTtot;
-  int splits, M;
-  // X: XS_NORM reads the fp32 residual stream xf [rows][H] and normalises it
-  // with the per-group sums of squares ss[g*kRowPad + m] (ss_groups groups);
-  // XS_BF16 copies xb [rows][ldx]
-  float *xf;
-  const void *xb;
-  int64_t ldx;
-  const float *ss;
-  int ss_groups;
-  const float *gain;
-  float eps;
-  int H;
-  // split partials [split][kRowPad][ldpart] and per-group arrival counters
-  float *part;
-  int64_t ldpart;
-  unsigned *counters;
-  // FEPI_QKV
-  int hd, nq, nkv, layer;
-  const int32_t *kv_len;
-  const float *rope;
-  void *qout;
-  void *cache;
-  int64_t cap;
-  // FEPI_RESID: per-group sums of squares of the new x
-  float *ss_out;
-  // FEPI_SWIGLU
-  int64_t up_tile_off;
-  void *act;
-  int64_t ldact;
-};
-int fgemm_lds_bytes(bool bf16, int mt, int64_t KFr, int splits);
-int64_t fgemm_groups(int epi, int64_t NTtot, int64_t up_tile_off);
-hipError_t fgemm_init();
-hipError_t launch_fgemm(bool bf16, int epi, int xs, int mt, const FusedArgs &a, hipStream_t s);
-hipError_t launch_embed_ss(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
-                           float *x, float *ss, hipStream_t s);
-hipError_t launch_norm_ss(bool bf16, const float *x, const float *ss, int groups, int M, int H,
-                          const float *gain, float eps, void *xn, int64_t ldxn, hipStream_t s);
-
 hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers, int64_t src_layer_stride,
                        bool bf16, const Packed &geom, void *dst, hipStream_t s);
 

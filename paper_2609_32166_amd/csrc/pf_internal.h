@@ -148,8 +148,6 @@ struct pf_model {
   int32_t *rowinfo = nullptr;// [kRowPad][4]: token, position offset (depth), valid, pad
   int32_t *pred = nullptr;   // [kRowPad]
   int32_t *flags = nullptr;  // [4] device status words
-  float *ssg = nullptr;      // [H/128][kRowPad] per-column-group sums of squares of x
-  unsigned *counters = nullptr;  // arrival counters of the fused GEMM column groups
   int64_t bytes = 0;
   // prefill work buffers (allocated on first use, sized for pre_rows rows)
   int64_t pre_rows = 0;
