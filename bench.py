@@ -89,6 +89,7 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=5)
     ap.add_argument("--cpu-layers", type=int, default=0, help="0: every layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
@@ -171,10 +172,31 @@ def main():
         step()
     stop.record()
     torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
+    ms_eager = start.elapsed_time(stop) / args.steps
+    ms = ms_eager
+    if not args.no_graph:
+        # the whole step (resets, lookup, verify, commit) as one HIP graph
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            graph.replay()
+        stop.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / args.steps
     r = pf.read_result(res)
     d = pf.read_draft(draft)
-    log(f"step {ms:.3f} ms, draft {int(d['n_nodes']) - 1} tokens, accepted {int(r['accept_len'])}")
+    log(f"step {ms:.3f} ms (eager {ms_eager:.3f} ms), draft {int(d['n_nodes']) - 1} tokens, "
+        f"accepted {int(r['accept_len'])}")
 
     # per-kernel durations (event pairs around every launch)
     tot = np.zeros(pf.PF_PROF_KINDS)
@@ -205,6 +227,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_per_step_eager": round(ms_eager, 4),
+        "timing": "HIP graph replay of the whole step" if not args.no_graph else "eager launches",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

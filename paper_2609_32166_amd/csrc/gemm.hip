@@ -67,7 +67,6 @@ hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers,
 // GEMM
 // ---------------------------------------------------------------------------
 
-constexpr int kU = 4;  // fragments per pipeline stage
 
 template <int EPI> struct EpiTiles;
 template <> struct EpiTiles<EPI_PARTIAL> { static constexpr int NT = 2; };
@@ -79,6 +78,7 @@ __device__ inline float silu(float g) { return g / (1.0f + expf(-g)); }
 template <typename T, int MT, int EPI>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int NT = EpiTiles<EPI>::NT;
+  constexpr int kU = NT >= 4 ? 4 : 6;  // fragment slots in flight per wave
   constexpr int E = Elem<T>::E;
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
@@ -110,10 +110,14 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 #pragma unroll
   for (int j = 0; j < NT; ++j)
     wbase[j] = tv[j] ? (uint32_t)(((tile[j] * a.KFr + f0) * 64 + lane) * 16) : kOOB;
+  // rows past M are padding of the last 16-row tile: their lanes load
+  // nothing (out-of-bounds offset gives zeros without memory traffic)
 #pragma unroll
   for (int m = 0; m < MT; ++m)
-    xbase[m] = (uint32_t)((((int64_t)(m * 16 + (lane & 15))) * a.ldx + f0 * 4 * E +
-                           (lane >> 4) * E) * sizeof(T));
+    xbase[m] = m * 16 + (lane & 15) < a.M
+                   ? (uint32_t)((((int64_t)(m * 16 + (lane & 15))) * a.ldx + f0 * 4 * E +
+                                 (lane >> 4) * E) * sizeof(T))
+                   : kOOB;
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -133,7 +137,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
       wv[u][j] = bload16(wr, in && wbase[j] != kOOB ? wbase[j] + (uint32_t)(i * 1024) : kOOB);
 #pragma unroll
     for (int m = 0; m < MT; ++m)
-      xv[u][m] = bload16(xr, in ? xbase[m] + (uint32_t)(i * 4 * E * sizeof(T)) : kOOB);
+      xv[u][m] = bload16(xr, in && xbase[m] != kOOB ? xbase[m] + (uint32_t)(i * 4 * E * sizeof(T))
+                                                      : kOOB);
   };
 #pragma unroll
   for (int u = 0; u < kU; ++u) {

@@ -363,3 +363,53 @@ def test_capacity_and_argument_errors(pf):
         pf.pf_kv_commit(gpu.kv, gpu.res, c)
     assert e.value.status == pf.PF_ECAPACITY
     torch.cuda.synchronize()
+
+
+def test_graph_replay_matches_eager(pf):
+    """The step captured into a HIP graph gives the eager step's results on
+    every replay (with eager work and synchronisation between replays)."""
+    import torch
+    wl = TINY
+    seed = synth.case_seed(wl, 400)
+    w = synth.make_weights(wl.model, seed)
+    kv_host = synth.make_kv_prefix(wl.model, seed, wl.prefix)
+    om = oracle.Model(wl.model, w)
+    store = synth.make_store(wl, seed)
+    ctx, _ = synth.make_context(wl, seed, store, hit=True)
+    store, _ = splice(wl, om, kv_host, store, ctx, seed, 5)
+    gpu = Gpu(wl.model, w, kv_host, wl.prefix, 1024)
+    st = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
+    c = pf.Context(ctx, len(ctx) + 64)
+    logits = torch.zeros(wl.rows, wl.model.vocab, device="cuda")
+
+    def step():
+        pf.pf_kv_set_len(gpu.kv, wl.prefix)
+        pf.pf_context_init(c, len(ctx))
+        pf.pf_draft_lookup(st, c, wl.k_max, False, 1, 64, gpu.draft)
+        pf.pf_verify_step(gpu.model, gpu.kv, gpu.draft, wl.rows, False, logits, gpu.res)
+        pf.pf_kv_commit(gpu.kv, gpu.res, c)
+
+    step()
+    torch.cuda.synchronize()
+    ref_res = pf.read_result(gpu.res).copy()
+    ref_logits = logits.cpu().numpy().copy()
+    ref_ctx = c.tokens().copy()
+    assert int(ref_res["accept_len"]) >= 5
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(4):
+        logits.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        r = pf.read_result(gpu.res)
+        assert r.tobytes() == ref_res.tobytes(), rep
+        assert np.array_equal(logits.cpu().numpy(), ref_logits), rep
+        assert np.array_equal(c.tokens(), ref_ctx), rep
+        assert int(gpu.kv.len.item()) == wl.prefix + int(ref_res["accept_len"]) + 1
