@@ -90,6 +90,8 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=0, help="0: every layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    ap.add_argument("--copy-calibration", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (for counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
@@ -153,6 +155,13 @@ def main():
     del kvd
     log(f"model {model.bytes / 1e9:.2f} GB on device, set up in {time.perf_counter() - t0:.1f} s")
 
+    if args.copy_calibration:
+        # a plain copy of known size: reference for the FETCH_SIZE/WRITE_SIZE counters
+        src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     max_nodes = wl.max_nodes if wl.tree else 64
     n_cand = wl.n_cand if wl.tree else 1
 

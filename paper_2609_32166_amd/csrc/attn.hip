@@ -27,10 +27,18 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   constexpr int NCG = E / 4;      // key sub-groups per chunk
   const int lane = threadIdx.x & 63;
   const int q = lane >> 4;
-  const int h = blockIdx.y;
-  const int g = h / a.group;
-  const int s = blockIdx.x;
-  const int row0 = blockIdx.z * RT * 16;  // first query row of this wave
+  // XCD-aware placement: blocks are dispatched round-robin over the 8 XCDs,
+  // so the `group` query heads that read the same (KV head, key range) get
+  // block ids of equal residue mod 8 and share one L2.
+  const int b = blockIdx.x;
+  const int xcd = b & 7, j = b >> 3;
+  const int hl = j % a.group;
+  const int w = (j / a.group) * 8 + xcd;  // (KV head, key range) work id
+  if (w >= a.n_kv * a.n_splits) return;
+  const int g = w / a.n_splits;
+  const int s = w % a.n_splits;
+  const int h = g * a.group + hl;
+  const int row0 = blockIdx.y * RT * 16;  // first query row of this wave
 
   const int P = *a.kv_len;
   const int M = a.M;
@@ -121,16 +129,24 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
         }
         // keys of this lane: kc + q*E + e, e = 4*cg + i
         float cmax = -INFINITY;
+        if (kc + KC <= min(P, k1)) {  // cached prefix only: every key visible
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const int key = kc + q * E + e;
-          bool vis = key < k1;
-          if (vis && key >= P) {
-            const int di = key - P;
-            vis = a.tree ? (j < 64 && ((a.anc[j] >> di) & 1ull)) : (di <= j);
+          for (int e = 0; e < E; ++e) {
+            sv[e] *= sc;
+            cmax = fmaxf(cmax, sv[e]);
           }
-          sv[e] = vis ? sv[e] * sc : -INFINITY;
-          cmax = fmaxf(cmax, sv[e]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const int key = kc + q * E + e;
+            bool vis = key < k1;
+            if (vis && key >= P) {
+              const int di = key - P;
+              vis = a.tree ? (j < 64 && ((a.anc[j] >> di) & 1ull)) : (di <= j);
+            }
+            sv[e] = vis ? sv[e] * sc : -INFINITY;
+            cmax = fmaxf(cmax, sv[e]);
+          }
         }
         cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
         cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
@@ -241,7 +257,8 @@ static hipError_t attn_t(int rt, const AttnArgs &a, hipStream_t s) {
   // are spread over blockIdx.z
   const int per = rt <= 3 ? rt : 2;
   const int groups = (rt + per - 1) / per;
-  dim3 grid(a.n_splits, a.n_kv * a.group, groups), block(64);
+  const int works = a.n_kv * a.n_splits;
+  dim3 grid(8 * a.group * ((works + 7) / 8), groups), block(64);
   switch (per) {
     case 1: k_attn<T, 1, HD><<<grid, block, 0, s>>>(a); break;
     case 2: k_attn<T, 2, HD><<<grid, block, 0, s>>>(a); break;
