@@ -223,8 +223,8 @@ def main():
             kernels[name] = {"ms_per_step": round(tot[i] / args.profile_steps, 4),
                              "avg_launch_us": round(1000 * tot[i] / cnt[i], 2),
                              "launches_per_step": int(cnt[i] // args.profile_steps)}
-    gu_us = 1000 * tot[6] / max(1, cnt[6])
-    gu_gbs = gate_up_bytes(wl) / (gu_us * 1e-6) / 1e9
+    gu_us = 1000 * tot[6] / cnt[6] if cnt[6] else float("nan")
+    gu_gbs = gate_up_bytes(wl) / (gu_us * 1e-6) / 1e9 if cnt[6] else float("nan")
     nbytes = wl.verify_bytes()
     gbs = nbytes / (ms * 1e-3) / 1e9
     K = wl.k_max
