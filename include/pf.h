@@ -42,7 +42,7 @@ typedef int32_t pf_status;
 #define PF_EHIP (-3)         /* a HIP runtime call failed */
 #define PF_ECAPACITY (-4)    /* KV cache or context capacity would be exceeded */
 #define PF_ESTATE (-5)       /* object in the wrong state for the call */
-#define PF_EUNSUPPORTED (-6) /* shape or dtype this build does not handle */
+#define PF_EUNSUPPORTED (-6) /* shape or dtype the library does not handle */
 
 #define PF_DTYPE_F32 0
 #define PF_DTYPE_BF16 1
