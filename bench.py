@@ -40,6 +40,28 @@ def gate_up_bytes(wl) -> int:
     return esz * (2 * m.ffn * m.hidden + M * m.hidden + M * m.ffn)
 
 
+# HBM traffic of the gate/up kernel per launch, 3B workload, from two
+# rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) scaled by the counters'
+# reading for a 256 MiB device copy; the command and the figures are in
+# profiles/verify_step_3b_hbm_traffic.md. Valid only for the GEMM source it was
+# taken on (its SHA-256 below): after any change to that file it is reported
+# as null until measured again.
+GATE_UP_TRAFFIC = {"workload": "3b",
+                   "gemm_source_sha256": "35ce9f1569190bc2b8d407acfb7f8ef55c74706325ecbe94c61e107c5f2dc86d",
+                   "bytes": 91468459}
+
+
+def measured_traffic(wl):
+    import hashlib
+    src = os.path.join(ROOT, "paper_2609_32166_amd", "csrc", "gemm.hip")
+    with open(src, "rb") as f:
+        digest = hashlib.sha256(f.read()).hexdigest()
+    t = GATE_UP_TRAFFIC
+    if t["bytes"] is None or t["workload"] != wl.name or t["gemm_source_sha256"] != digest:
+        return None, "not measured for this GEMM source and workload"
+    return t["bytes"], "rocprofv3 PMC FETCH_SIZE + WRITE_SIZE, copy-calibrated"
+
+
 def prefill_flops(wl) -> float:
     """Algorithmic FLOPs of prefilling wl.prefill_new tokens after
     wl.prefill_reuse cached ones: every linear layer once per token, causal
@@ -207,7 +229,8 @@ def main():
     log(f"step {ms:.3f} ms (eager {ms_eager:.3f} ms), draft {int(d['n_nodes']) - 1} tokens, "
         f"accepted {int(r['accept_len'])}")
 
-    # per-kernel durations (event pairs around every launch)
+    # per-kernel durations: an event pair around every launch, the stream held
+    # until the step is enqueued, the cost of an empty pair subtracted
     tot = np.zeros(pf.PF_PROF_KINDS)
     cnt = np.zeros(pf.PF_PROF_KINDS, np.int64)
     for _ in range(args.profile_steps):
@@ -224,7 +247,9 @@ def main():
                              "avg_launch_us": round(1000 * tot[i] / cnt[i], 2),
                              "launches_per_step": int(cnt[i] // args.profile_steps)}
     gu_us = 1000 * tot[6] / cnt[6] if cnt[6] else float("nan")
+    pair_us = 1000 * tot[10] / cnt[10] if cnt[10] else float("nan")
     gu_gbs = gate_up_bytes(wl) / (gu_us * 1e-6) / 1e9 if cnt[6] else float("nan")
+    traffic, traffic_note = measured_traffic(wl)
     nbytes = wl.verify_bytes()
     gbs = nbytes / (ms * 1e-3) / 1e9
     K = wl.k_max
@@ -253,10 +278,12 @@ def main():
         "accepted_tokens_per_s": {f"l_acc={l}": round((l + 1) / (ms * 1e-3), 1)
                                   for l in (0, K // 2, K)},
         "roofline": {"bound": "hbm", "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "k_gemm<bf16,*,EPI_SWIGLU> (gate/up projection + SwiGLU)",
                      "bytes_per_launch": gate_up_bytes(wl),
-                     "avg_launch_us": round(gu_us, 2)},
+                     "avg_launch_us": round(gu_us, 2),
+                     "event_pair_us_subtracted": round(pair_us, 2),
+                     "traffic_source": traffic_note},
         "kernels": kernels,
     }
     if prefill is not None:

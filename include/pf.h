@@ -254,13 +254,19 @@ pf_status pf_verify_step(pf_model *model, pf_kv_cache *kv, const pf_draft *draft
                          pf_verify_result *res_dev, pf_stream s);
 
 /*
- * Profiling variant of pf_verify_step: the same work, with a HIP event pair
- * recorded around every kernel launch. It synchronises s, then adds each
+ * Profiling variant of pf_verify_step: the same work, timed per kernel. The
+ * stream is first held by a wait kernel (released by the host once the whole
+ * step is enqueued, and bounded by 500 ms of device wall clock in any case),
+ * so the kernels run back to back instead of waiting on host submission.
+ * Every launch is bracketed by a pair of fenceless HIP events; the cost of a
+ * pair itself is measured in the same call from pairs recorded with no work
+ * between (kind PF_PROF_MARKER: their total ms and their number) and is
+ * subtracted from every launch. The call synchronises s, then adds each
  * launch's duration in ms to ms_out[kind] and 1 to count_out[kind] (host
- * arrays of PF_PROF_KINDS entries, caller-initialised). Allocates events:
- * not for graph capture.
+ * arrays of PF_PROF_KINDS entries, caller-initialised). Allocates events and
+ * a pinned flag: not for graph capture.
  */
-#define PF_PROF_KINDS 10
+#define PF_PROF_KINDS 11
 #define PF_PROF_SETUP 0     /* row setup, embedding + first RMSNorm */
 #define PF_PROF_QKV 1       /* QKV projection */
 #define PF_PROF_QKV_POST 2  /* split-K reduction, RoPE, KV append */
@@ -271,6 +277,7 @@ pf_status pf_verify_step(pf_model *model, pf_kv_cache *kv, const pf_draft *draft
 #define PF_PROF_DOWN 7      /* down projection */
 #define PF_PROF_LM_HEAD 8   /* lm_head + argmax partials */
 #define PF_PROF_ACCEPT 9    /* argmax reduction + acceptance */
+#define PF_PROF_MARKER 10   /* empty event pairs (calibration, not subtracted) */
 pf_status pf_verify_step_profiled(pf_model *model, pf_kv_cache *kv, const pf_draft *draft_dev,
                                   int32_t rows, int32_t tree, float *logits_dev,
                                   pf_verify_result *res_dev, pf_stream s, double *ms_out,

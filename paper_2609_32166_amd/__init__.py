@@ -38,9 +38,9 @@ EXPORTED = ["pf_last_error", "pf_version", "pf_context_init", "pf_context_sync_b
             "pf_kv_import", "pf_kv_export", "pf_kv_set_len", "pf_kv_sync_bound", "pf_verify_step",
             "pf_kv_commit", "pf_prefill", "pf_verify_step_profiled"]
 
-PF_PROF_KINDS = 10
+PF_PROF_KINDS = 11
 PROF_NAMES = ["setup", "qkv", "qkv_post", "attn", "o_proj", "norm", "gate_up", "down",
-              "lm_head", "accept"]
+              "lm_head", "accept", "event_pair"]
 
 
 class PfError(RuntimeError):

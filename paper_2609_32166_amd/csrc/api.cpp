@@ -1,5 +1,6 @@
 // C-ABI layer of libpf: argument checks, the experience-store builder, model
 // creation (weight packing) and the launch sequence of one verify step.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -10,6 +11,8 @@
 #include "kernels.h"
 
 using namespace pf;
+
+thread_local LaunchTimer *pf::t_launch_timer = nullptr;
 
 static_assert(sizeof(pf_draft) == 1368, "pf_draft layout");
 static_assert(sizeof(pf_verify_result) == 808, "pf_verify_result layout");
@@ -71,30 +74,36 @@ int64_t partial_blocks(const Packed &p) {
 
 constexpr int kMaxSplitsAttn = 64;
 
-// Optional per-kernel timing of a verify step (events around each launch).
-struct Prof {
-  hipStream_t s;
+// Collects one (start, stop) event pair per kernel launched while installed,
+// tagged with the profiling kind current at the launch.
+struct Prof final : LaunchTimer {
   std::vector<hipEvent_t> ev;
   std::vector<int> kind;
-  hipError_t begin(int k) {
-    hipEvent_t e;
-    hipError_t r = hipEventCreate(&e);
-    if (r != hipSuccess) return r;
-    ev.push_back(e);
-    kind.push_back(k);
-    return hipEventRecord(e, s);
+  int cur = -1;
+  bool events(hipEvent_t *start, hipEvent_t *stop) override {
+    hipError_t r = hipEventCreateWithFlags(start, hipEventDisableSystemFence);
+    if (r == hipSuccess) {
+      r = hipEventCreateWithFlags(stop, hipEventDisableSystemFence);
+      if (r != hipSuccess) (void)hipEventDestroy(*start);
+    }
+    if (r != hipSuccess) {
+      if (err == hipSuccess) err = r;
+      return false;
+    }
+    ev.push_back(*start);
+    ev.push_back(*stop);
+    kind.push_back(cur);
+    return true;
   }
-  hipError_t end() {
-    hipEvent_t e;
-    hipError_t r = hipEventCreate(&e);
-    if (r != hipSuccess) return r;
-    ev.push_back(e);
-    kind.push_back(-1);
-    return hipEventRecord(e, s);
-  }
-  ~Prof() {
+  ~Prof() override {
     for (hipEvent_t e : ev) (void)hipEventDestroy(e);
   }
+};
+
+// Installs a timer for the lifetime of the scope (no-op for a null timer).
+struct TimerScope {
+  explicit TimerScope(LaunchTimer *t) { t_launch_timer = t; }
+  ~TimerScope() { t_launch_timer = nullptr; }
 };
 
 template <typename T> pf_status dev_alloc(T **p, int64_t bytes, int64_t *total) {
@@ -348,6 +357,13 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
   }
   m->part_elems = part;
   m->apart_rows = (int64_t)c.n_heads * kMaxSplitsAttn * kRowPad;
+  {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus > 0)
+      m->wave_slots = 4 * cus;
+  }
   m->amax_elems = ((m->plm.NT + 3) / 4) * kRowPad;
   ALLOC(m->x, kRowPad * H * 4);
   ALLOC(m->xn, kRowPad * Hp * m->esz);
@@ -484,11 +500,10 @@ static pf_status model_kv_match(const pf_model *m, const pf_kv_cache *kv, const 
   return PF_OK;
 }
 
-#define PROF(kind, call)                                                         \
+#define PROF(k, call)                                                            \
   do {                                                                           \
-    if (prof) HIPCHK(prof->begin(kind));                                         \
+    if (prof) prof->cur = (k);                                                   \
     HIPCHK(call);                                                                \
-    if (prof) HIPCHK(prof->end());                                               \
   } while (0)
 
 static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft, int32_t rows,
@@ -511,6 +526,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   const int64_t Hp = roundup(H, kf), qp = roundup(q, kf), Fp = roundup(F, kf);
   const int M = rows, MT = (rows + 15) / 16;
   hipStream_t hs = st(s);
+  TimerScope timer_scope(prof);
   const float eps = (float)c.rms_eps;
   uint64_t *rowmask = (uint64_t *)(m->rowinfo + kRowPad * 4);
 
@@ -527,12 +543,22 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   sa.rowmask = rowmask;
   sa.rope = m->rope;
   PROF(0, launch_prep(sa, hs));
-  PROF(0, launch_embed_norm(bf, m->embed, m->rowinfo, M, H, m->attn_norm, eps, m->x, m->xn, Hp, hs));
+  PROF(0, launch_embed_norm(bf, m->embed, m->rowinfo, M, H, m->attn_norm, eps, m->x, m->xn, Hp,
+                            true, hs));
 
   // attention geometry: key ranges over P + rows keys (P <= host bound)
   const int64_t keys_max = kv->host_bound + rows;
-  int chunk = (int)roundup((keys_max + kMaxSplitsAttn - 1) / kMaxSplitsAttn, 32);
-  if (chunk < 128) chunk = 128;
+  // key ranges of about five chunks per wave (measured best: shorter ranges
+  // add splits and waves, longer ones leave the straight-line part of the
+  // kernel), longer when needed to keep every attention wave resident at once
+  // (one wave per SIMD at the kernel's register footprint)
+  const int row_groups = (MT + 1) / 2;
+  int max_splits = m->wave_slots / (nq * row_groups);
+  if (max_splits > kMaxSplitsAttn) max_splits = kMaxSplitsAttn;
+  if (max_splits < 1) max_splits = 1;
+  int chunk = (int)roundup((keys_max + max_splits - 1) / max_splits, 32);
+  const int pref = 5 * (bf ? 32 : 16);
+  if (chunk < pref) chunk = pref;
   const int n_splits = (int)((keys_max + chunk - 1) / chunk);
 
   for (int l = 0; l < L; ++l) {
@@ -567,6 +593,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     at.kv_len = kv->len;
     at.n_splits = n_splits;
     at.chunk_keys = chunk;
+    at.keys_bound = (int)keys_max;
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
     at.tree = tree;
     at.anc = rowmask;
@@ -574,6 +601,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     at.part_ml = m->apart_ml;
     at.out = m->attn;
     at.ldout = qp;
+    at.out_packed = 1;
     PROF(3, launch_attn(bf, MT, at, hs));
     // output projection + residual + FFN norm
     GemmArgs go{};
@@ -589,7 +617,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     go.ldo = H;
     PROF(4, launch_gemm(bf, EPI_PARTIAL, MT, go, hs));
     PROF(5, launch_residual_norm(bf, m->part, go.splits, kRowPad, M, H, H, m->ffn_norm + (int64_t)l * H, eps,
-                                m->x, m->xn, Hp, hs));
+                                m->x, m->xn, Hp, true, hs));
     // gate/up + SwiGLU
     GemmArgs gg{};
     gg.W = (const char *)m->wgu + (int64_t)l * m->pgu.bytes();
@@ -619,7 +647,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     PROF(7, launch_gemm(bf, EPI_PARTIAL, MT, gd, hs));
     const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
     PROF(5, launch_residual_norm(bf, m->part, gd.splits, kRowPad, M, H, H, next_gain, eps, m->x, m->xn, Hp,
-                                hs));
+                                true, hs));
   }
   // lm_head + greedy argmax partials
   GemmArgs gl{};
@@ -652,19 +680,57 @@ pf_status pf_verify_step_profiled(pf_model *m, pf_kv_cache *kv, const pf_draft *
                                   int32_t rows, int32_t tree, float *logits, pf_verify_result *res,
                                   pf_stream s, double *ms_out, int32_t *count_out) {
   if (!ms_out || !count_out) return fail(PF_EINVAL, "pf_verify_step_profiled: null outputs");
-  Prof prof;
-  prof.s = st(s);
-  pf_status r = verify_impl(m, kv, draft, rows, tree, logits, res, s, &prof);
-  if (r != PF_OK) return r;
-  HIPCHK(hipStreamSynchronize(prof.s));
-  for (size_t i = 0; i + 1 < prof.ev.size(); i += 2) {
-    float ms = 0.f;
-    HIPCHK(hipEventElapsedTime(&ms, prof.ev[i], prof.ev[i + 1]));
-    int k = prof.kind[i];
-    if (k >= 0 && k < PF_PROF_KINDS) {
-      ms_out[k] += ms;
-      count_out[k] += 1;
+  // Hold the stream until the whole step is enqueued, so that the timed
+  // kernels run back to back as in a graph replay rather than waiting on
+  // host submission (the hold is released on every path, and is bounded by
+  // 500 ms of wall clock on the device in any case).
+  int dev = 0, rate_khz = 0;
+  HIPCHK(hipGetDevice(&dev));
+  HIPCHK(hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, dev));
+  int32_t *flag = nullptr;
+  HIPCHK(hipHostMalloc((void **)&flag, 64, hipHostMallocCoherent));
+  struct Release {
+    int32_t *f;
+    hipStream_t s;
+    ~Release() {
+      __atomic_store_n(f, 1, __ATOMIC_SEQ_CST);
+      (void)hipStreamSynchronize(s);
+      (void)hipHostFree(f);
     }
+  } release{flag, st(s)};
+  __atomic_store_n(flag, 0, __ATOMIC_SEQ_CST);
+  HIPCHK(launch_hold(flag, (uint64_t)rate_khz * 500, st(s)));
+  Prof prof;
+  // the cost of an event pair itself: pairs recorded with no work between
+  constexpr int kMarkerPairs = 16;
+  prof.cur = PF_PROF_MARKER;
+  for (int i = 0; i < kMarkerPairs; ++i) {
+    hipEvent_t e0, e1;
+    if (!prof.events(&e0, &e1)) break;
+    HIPCHK(hipEventRecord(e0, st(s)));
+    HIPCHK(hipEventRecord(e1, st(s)));
+  }
+  pf_status r = verify_impl(m, kv, draft, rows, tree, logits, res, s, &prof);
+  __atomic_store_n(flag, 1, __ATOMIC_SEQ_CST);
+  if (r != PF_OK) return r;
+  HIPCHK(prof.err);
+  HIPCHK(hipStreamSynchronize(st(s)));
+  std::vector<float> ms(prof.kind.size());
+  double marker = 0.0;
+  int n_marker = 0;
+  for (size_t i = 0; i < prof.kind.size(); ++i) {
+    HIPCHK(hipEventElapsedTime(&ms[i], prof.ev[2 * i], prof.ev[2 * i + 1]));
+    if (prof.kind[i] == PF_PROF_MARKER) {
+      marker += ms[i];
+      ++n_marker;
+    }
+  }
+  const double per_pair = n_marker ? marker / n_marker : 0.0;
+  for (size_t i = 0; i < prof.kind.size(); ++i) {
+    const int k = prof.kind[i];
+    if (k < 0 || k >= PF_PROF_KINDS) continue;
+    ms_out[k] += k == PF_PROF_MARKER ? ms[i] : std::max(0.0, ms[i] - per_pair);
+    count_out[k] += 1;
   }
   return ok();
 }
@@ -754,7 +820,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
     HIPCHK(launch_prefill_rows(tokens + c0, rows, (int)V, kv->len, m->inv_freq, hd, m->pre_rowinfo,
                                m->pre_rope, m->pre_status, hs));
     HIPCHK(launch_embed_norm(bf, m->embed, m->pre_rowinfo, rows, H, m->attn_norm, eps, m->pre_x,
-                             m->pre_xn, Hp, hs));
+                             m->pre_xn, Hp, false, hs));
     const int64_t keys_max = kv->host_bound + c0 + rows;
     int ck = (int)roundup((keys_max + kPrefillSplits - 1) / kPrefillSplits, 32);
     if (ck < 128) ck = 128;
@@ -789,6 +855,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       at.kv_len = kv->len;
       at.n_splits = nsp;
       at.chunk_keys = ck;
+      at.keys_bound = (int)keys_max;
       at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
       at.tree = 0;
       at.anc = rowmask;
@@ -810,7 +877,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       go.ldy = H;
       HIPCHK(launch_gemm_big(bf, BIG_RESID, go, hs));
       HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, m->ffn_norm + (int64_t)l * H, eps,
-                                  m->pre_x, m->pre_xn, Hp, hs));
+                                  m->pre_x, m->pre_xn, Hp, false, hs));
       BigGemmArgs gg{};
       gg.W = (const char *)m->wgu + (int64_t)l * m->pgu.bytes();
       gg.W_bytes = m->pgu.bytes();
@@ -838,13 +905,13 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       HIPCHK(launch_gemm_big(bf, BIG_RESID, gd, hs));
       const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
       HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, next_gain, eps, m->pre_x,
-                                  m->pre_xn, Hp, hs));
+                                  m->pre_xn, Hp, false, hs));
     }
     HIPCHK(launch_add_int(kv->len, rows, hs));
     if (c0 + rows == n && logits_last) {
       // last token: final-norm row -> lm_head (one row through the verify GEMM)
-      HIPCHK(launch_copy_row((const char *)m->pre_xn + (int64_t)(rows - 1) * Hp * m->esz, m->xn,
-                             Hp * m->esz, hs));
+      HIPCHK(launch_pack_row(bf, (const char *)m->pre_xn + (int64_t)(rows - 1) * Hp * m->esz, m->xn,
+                             Hp, hs));
       GemmArgs gl{};
       gl.W = m->lm;
       gl.W_bytes = m->plm.bytes();

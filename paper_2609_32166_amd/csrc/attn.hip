@@ -2,9 +2,12 @@
 // attends to the cached keys 0..P-1 and to the draft keys P..P+M-1 it may
 // see (causal for a linear draft, ancestors-or-self for a tree).
 //
-// Work split: one wave per (key range, query head); the heads of a group read
-// the same K/V fragments, which they share through L2. Keys
-// are processed in chunks of 4*E (32 bf16 / 16 fp32). S^T = K Q^T is formed
+// Work split: one wave per (key range, query head, 32 query rows); the heads
+// of a group read the same K/V fragments, which they share through L2. The
+// host sizes the ranges so that every wave of the launch is resident at once
+// (one wave per SIMD at this register footprint). The loop body is kept
+// small (every wave runs it only a few times, so instruction fetch of a long
+// unrolled body would dominate). Keys are processed in chunks of 4*E (32 bf16 / 16 fp32). S^T = K Q^T is formed
 // with K as the MFMA A operand, permuting which key each A row carries so
 // that, after the MFMA, lane quarter q holds the scores of keys q*E..q*E+E-1
 // of its query row (column). That is exactly the B-operand layout of
@@ -16,6 +19,38 @@
 #include "kernels.h"
 
 namespace pf {
+
+// E probabilities in [0, 1] -> one 16-byte MFMA operand chunk in the model
+// dtype (bf16: hardware round-to-nearest-even conversion).
+template <typename T> __device__ inline uint4 pack_probs(const float *p);
+template <> __device__ inline uint4 pack_probs<float>(const float *p) {
+  return make_uint4(__float_as_uint(p[0]), __float_as_uint(p[1]), __float_as_uint(p[2]),
+                    __float_as_uint(p[3]));
+}
+template <> __device__ inline uint4 pack_probs<bf16_t>(const float *p) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    w[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){p[2 * i], p[2 * i + 1]}, b2));
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Keeps the first n (0..E) elements of a 16-byte chunk and zeroes the rest.
+template <typename T> __device__ inline uint4 keep_first(uint4 v, int n) {
+  constexpr int E = Elem<T>::E, PER = E / 4;  // elements per 32-bit word
+  uint32_t m[4];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (PER == 1) {
+      m[w] = w < n ? 0xFFFFFFFFu : 0u;
+    } else {
+      m[w] = (2 * w < n ? 0x0000FFFFu : 0u) | (2 * w + 1 < n ? 0xFFFF0000u : 0u);
+    }
+  }
+  return make_uint4(v.x & m[0], v.y & m[1], v.z & m[2], v.w & m[3]);
+}
 
 template <typename T, int RT, int HD>
 __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
@@ -40,14 +75,13 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   const int h = g * a.group + hl;
   const int row0 = blockIdx.y * RT * 16;  // first query row of this wave
 
-  const int P = *a.kv_len;
   const int M = a.M;
-  const int kend = P + M;
   const int k0 = s * a.chunk_keys;
-  const int k1 = min(k0 + a.chunk_keys, kend);
-
-  float *po = a.part_o + (((int64_t)h * a.n_splits + s) * a.rowpad) * HD;
-  float *pml = a.part_ml + (((int64_t)h * a.n_splits + s) * a.rowpad) * 2;
+  // Loads are bounded by the host's upper bound on P + M, so they are issued
+  // without waiting for the device-side length; keys past the true end are
+  // masked once P has arrived.
+  const int kb = min(k0 + a.chunk_keys, a.keys_bound);
+  const int nchunks = kb > k0 ? (kb - k0 + KC - 1) / KC : 0;
 
   float m_run[RT], l_run[RT];
   f32x4 o[RT][NDT];
@@ -59,148 +93,168 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
     for (int t = 0; t < NDT; ++t) o[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  if (k0 < k1) {
-    // query fragments: row j = r*16 + lane%16, dims ds*KF + q*E .. +E
-    uint4 qf[RT][NDS];
+  // query fragments: row j = r*16 + lane%16, dims ds*KF + q*E .. +E
+  uint4 qf[RT][NDS];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    const int jr = min(row0 + r * 16 + (lane & 15), a.rowpad - 1);
+    const T *qrow = (const T *)a.q + (int64_t)jr * a.ldq + h * HD;
+#pragma unroll
+    for (int d = 0; d < NDS; ++d) qf[r][d] = *(const uint4 *)(qrow + d * KF + q * E);
+  }
+  const T *kplane = (const T *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.n_kv + g) * a.plane;
+  const T *vplane = (const T *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.n_kv + g) * a.plane;
+  const uint32_t plane_bytes = (uint32_t)(a.plane * sizeof(T));
+  const rsrc_t kr = make_rsrc(kplane, plane_bytes);
+  const rsrc_t vr = make_rsrc(vplane, plane_bytes);
+  const float sc = a.scale_log2;
+
+  // two chunk slots: compute one while the other's K/V loads are in flight.
+  // Chunks past the range load out of the resource (zeros, no traffic).
+  uint4 kf[2][NCG][NDS], vf[2][NDT];
+  auto load = [&](int slot, int c) {
+    const int kc = k0 + c * KC;
+    const bool in = c < nchunks;
+#pragma unroll
+    for (int cg = 0; cg < NCG; ++cg) {
+      const int r = lane & 15;
+      const int key = kc + E * (r >> 2) + 4 * cg + (r & 3);
+#pragma unroll
+      for (int d = 0; d < NDS; ++d)
+        kf[slot][cg][d] =
+            bload16(kr, in ? (uint32_t)(((int64_t)key * HD + d * KF + q * E) * sizeof(T)) : kOOB);
+    }
+#pragma unroll
+    for (int t = 0; t < NDT; ++t)
+      vf[slot][t] = bload16(
+          vr, in ? (uint32_t)(((int64_t)(t * 16 + (lane & 15)) * a.cap + kc + q * E) * sizeof(T))
+                 : kOOB);
+  };
+  load(0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  load(1, 1);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // visibility: key < lim[r] (linear drafts: draft key P + i is seen by rows
+  // j >= i), and for a tree also ancestor-or-self among the draft keys
+  const int P = *a.kv_len;
+  const int kend = P + M;
+  const int k1 = min(k0 + a.chunk_keys, kend);
+  int lim[RT];
+  uint64_t anc[RT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    const int jq = row0 + r * 16 + (lane & 15);
+    lim[r] = a.tree ? k1 : min(k1, P + jq + 1);
+    anc[r] = a.tree ? a.anc[min(jq, a.rowpad - 1)] : 0ull;
+  }
+
+  // Online softmax with a deferred rescale: m_run is a reference maximum (raw
+  // score units) that only moves when some row's maximum exceeds it by more
+  // than 2^8 in probability, so probabilities stay below 256 and the
+  // accumulators are rescaled a handful of times per range instead of per
+  // chunk. The result equals the usual update up to rounding.
+  constexpr float kSlack = 8.f;  // log2 headroom of the reference maximum
+  auto compute = [&](int slot, int c) {
+    const int kc = k0 + c * KC;
+    if (c >= nchunks || kc >= k1) return;  // uniform over the wave
+    const int kl = kc + q * E;             // first key of this lane's chunk
+    // value columns of keys past the end of the cache are zeroed (not
+    // initialised there; a zero probability must not meet a NaN)
+    if (kc + KC > kend) {
+      const int n = min(max(kend - kl, 0), E);
+#pragma unroll
+      for (int t = 0; t < NDT; ++t) vf[slot][t] = keep_first<T>(vf[slot][t], n);
+    }
+    const bool all_visible = kc + KC <= min(P, k1);  // cached prefix only (uniform)
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
-      const int jr = min(row0 + r * 16 + (lane & 15), a.rowpad - 1);
-      const T *qrow = (const T *)a.q + (int64_t)jr * a.ldq + h * HD;
-#pragma unroll
-      for (int d = 0; d < NDS; ++d) qf[r][d] = *(const uint4 *)(qrow + d * KF + q * E);
-    }
-    const T *kplane = (const T *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.n_kv + g) * a.plane;
-    const T *vplane = (const T *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.n_kv + g) * a.plane;
-    const uint32_t plane_bytes = (uint32_t)(a.plane * sizeof(T));
-    const rsrc_t kr = make_rsrc(kplane, plane_bytes);
-    const rsrc_t vr = make_rsrc(vplane, plane_bytes);
-    const float sc = a.scale_log2;
-    const int nchunks = (k1 - k0 + KC - 1) / KC;
-
-    // two chunk slots: compute one while the other's K/V loads are in flight.
-    // Chunks past the range load out of the resource (zeros, no traffic) and
-    // their keys are masked, so they add nothing.
-    uint4 kf[2][NCG][NDS], vf[2][NDT];
-    auto load = [&](int slot, int c) {
-      const int kc = k0 + c * KC;
-      const bool in = c < nchunks;
+      float sv[E];
 #pragma unroll
       for (int cg = 0; cg < NCG; ++cg) {
-        const int r = lane & 15;
-        const int key = kc + E * (r >> 2) + 4 * cg + (r & 3);
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int d = 0; d < NDS; ++d)
-          kf[slot][cg][d] = bload16(
-              kr, in ? (uint32_t)(((int64_t)key * HD + d * KF + q * E) * sizeof(T)) : kOOB);
+        for (int d = 0; d < NDS; ++d) acc = mma<T>(kf[slot][cg][d], qf[r][d], acc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sv[4 * cg + i] = acc[i];
       }
-#pragma unroll
-      for (int t = 0; t < NDT; ++t)
-        vf[slot][t] = bload16(
-            vr, in ? (uint32_t)(((int64_t)(t * 16 + (lane & 15)) * a.cap + kc + q * E) * sizeof(T))
-                   : kOOB);
-    };
-    auto compute = [&](int slot, int c) {
-      const int kc = k0 + c * KC;
-      if (kc + KC > kend) {  // zero value columns of keys past the end of the cache
-#pragma unroll
-        for (int t = 0; t < NDT; ++t) {
-          union {
-            uint4 v;
-            T e[E];
-          } u;
-          u.v = vf[slot][t];
-#pragma unroll
-          for (int e = 0; e < E; ++e)
-            if (kc + q * E + e >= kend) memset(&u.e[e], 0, sizeof(T));
-          vf[slot][t] = u.v;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        const int j = row0 + r * 16 + (lane & 15);  // query row of this lane
-        float sv[E];
-#pragma unroll
-        for (int cg = 0; cg < NCG; ++cg) {
-          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int d = 0; d < NDS; ++d) acc = mma<T>(kf[slot][cg][d], qf[r][d], acc);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) sv[4 * cg + i] = acc[i];
-        }
-        // keys of this lane: kc + q*E + e, e = 4*cg + i
-        float cmax = -INFINITY;
-        if (kc + KC <= min(P, k1)) {  // cached prefix only: every key visible
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            sv[e] *= sc;
-            cmax = fmaxf(cmax, sv[e]);
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const int key = kc + q * E + e;
-            bool vis = key < k1;
-            if (vis && key >= P) {
-              const int di = key - P;
-              vis = a.tree ? (j < 64 && ((a.anc[j] >> di) & 1ull)) : (di <= j);
-            }
-            sv[e] = vis ? sv[e] * sc : -INFINITY;
-            cmax = fmaxf(cmax, sv[e]);
-          }
-        }
-        cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
-        cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
-        const float m_new = fmaxf(m_run[r], cmax);
-        const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run[r] - m_new);
-        union {
-          uint4 v;
-          T e[E];
-        } pu;
-        float psum = 0.f;
+      if (!all_visible) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          const float p = sv[e] == -INFINITY ? 0.f : exp2f(sv[e] - m_new);
-          Elem<T>::store(pu.e, e, p);
-          psum += p;
-        }
-        l_run[r] = l_run[r] * alpha + psum;
-        m_run[r] = m_new;
-#pragma unroll
-        for (int t = 0; t < NDT; ++t) {
-          o[r][t] *= alpha;
-          o[r][t] = mma<T>(vf[slot][t], pu.v, o[r][t]);
+          const int key = kl + e;
+          bool vis = key < lim[r];
+          if (a.tree) vis &= (key < P) | (((anc[r] >> ((key - P) & 63)) & 1ull) != 0);
+          sv[e] = vis ? sv[e] : -INFINITY;
         }
       }
-    };
-    load(0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    load(1, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    for (int c = 0; c < nchunks; c += 2) {
-      compute(0, c);
-      load(0, c + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(1, c + 1);
-      load(1, c + 3);
-      __builtin_amdgcn_sched_barrier(0);
+      float cmax = sv[0];
+#pragma unroll
+      for (int e = 1; e < E; ++e) cmax = fmaxf(cmax, sv[e]);
+      cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
+      cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
+      // move the reference when a row outgrows it (wave-uniform decision)
+      const bool grow = m_run[r] == -INFINITY ? cmax > -INFINITY : (cmax - m_run[r]) * sc > kSlack;
+      if (__any(grow)) {
+        const float m_new = fmaxf(m_run[r], cmax);
+        const float alpha =
+            m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f((m_run[r] - m_new) * sc);
+        l_run[r] *= alpha;
+#pragma unroll
+        for (int t = 0; t < NDT; ++t) o[r][t] *= alpha;
+        m_run[r] = m_new;
+      }
+      const float msc = m_run[r] == -INFINITY ? 0.f : m_run[r] * sc;
+      float p[E], psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(fmaf(sv[e], sc, -msc));  // exp2(-inf) = 0
+        psum += p[e];
+      }
+      l_run[r] += psum;
+      const uint4 pu = pack_probs<T>(p);
+#pragma unroll
+      for (int t = 0; t < NDT; ++t) o[r][t] = mma<T>(vf[slot][t], pu, o[r][t]);
     }
+  };
+  // The first kStraight chunks run as straight-line code (no loop-carried
+  // accumulators to shuffle between register files); longer ranges continue
+  // in a loop. Compute of a chunk past the range returns at once.
+  constexpr int kStraight = 6;
+#pragma unroll
+  for (int c = 0; c < kStraight; c += 2) {
+    compute(0, c);
+    load(0, c + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1, c + 1);
+    load(1, c + 3);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int c = kStraight; c < nchunks; c += 2) {
+    compute(0, c);
+    load(0, c + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1, c + 1);
+    load(1, c + 3);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   // write the partial: lane holds O^T[d = t*16 + 4q + i][row lane%16]
+  float *po = a.part_o + (((int64_t)h * a.n_splits + s) * a.rowpad) * HD;
+  float *pml = a.part_ml + (((int64_t)h * a.n_splits + s) * a.rowpad) * 2;
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
     float l = l_run[r];
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);
-    const int j = row0 + r * 16 + (lane & 15);
-    if (j >= M) continue;
+    const int jq = row0 + r * 16 + (lane & 15);
+    if (jq >= M) continue;
 #pragma unroll
     for (int t = 0; t < NDT; ++t)
-      *(float4 *)(po + (int64_t)j * HD + t * 16 + 4 * q) =
+      *(float4 *)(po + (int64_t)jq * HD + t * 16 + 4 * q) =
           make_float4(o[r][t][0], o[r][t][1], o[r][t][2], o[r][t][3]);
-    if (q == 0) {
-      pml[j * 2 + 0] = m_run[r];
-      pml[j * 2 + 1] = l;
+    if (q == 0) {  // (max, sum) in the log2-scaled units the combine uses
+      pml[jq * 2 + 0] = m_run[r] == -INFINITY ? -INFINITY : m_run[r] * sc;
+      pml[jq * 2 + 1] = l;
     }
   }
 }
@@ -246,28 +300,30 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < HD / 64; ++i)
       acc[i] += ws[s] * po[((int64_t)s * a.rowpad + j) * HD + lane + 64 * i];
-  T *out = (T *)a.out + (int64_t)j * a.ldout + h * HD;
+  T *out = (T *)a.out;
 #pragma unroll
-  for (int i = 0; i < HD / 64; ++i) Elem<T>::store(out, lane + 64 * i, acc[i] / den);
+  for (int i = 0; i < HD / 64; ++i) {
+    const int64_t k = h * HD + lane + 64 * i;
+    Elem<T>::store(out, a.out_packed ? act_off<T>(j, k, a.ldout) : (int64_t)j * a.ldout + k,
+                   acc[i] / den);
+  }
 }
 
 template <typename T, int HD>
 static hipError_t attn_t(int rt, const AttnArgs &a, hipStream_t s) {
-  // at most three 16-row query tiles per wave (register budget); more rows
-  // are spread over blockIdx.z
-  const int per = rt <= 3 ? rt : 2;
+  // at most two 16-row query tiles per wave (register budget); more rows
+  // are spread over blockIdx.y
+  const int per = rt <= 2 ? rt : 2;
   const int groups = (rt + per - 1) / per;
   const int works = a.n_kv * a.n_splits;
+  if (a.chunk_keys % (4 * Elem<T>::E) != 0 || a.keys_bound < 0) return hipErrorInvalidValue;
   dim3 grid(8 * a.group * ((works + 7) / 8), groups), block(64);
   switch (per) {
-    case 1: k_attn<T, 1, HD><<<grid, block, 0, s>>>(a); break;
-    case 2: k_attn<T, 2, HD><<<grid, block, 0, s>>>(a); break;
-    case 3: k_attn<T, 3, HD><<<grid, block, 0, s>>>(a); break;
+    case 1: PF_TRY(launch_k(k_attn<T, 1, HD>, grid, block, s, a)); break;
+    case 2: PF_TRY(launch_k(k_attn<T, 2, HD>, grid, block, s, a)); break;
     default: return hipErrorInvalidValue;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  k_attn_combine<T, HD><<<dim3(a.M, a.n_kv * a.group), 64, 0, s>>>(a);
+  PF_TRY(launch_k(k_attn_combine<T, HD>, dim3(a.M, a.n_kv * a.group), 64, s, a));
   return hipGetLastError();
 }
 

@@ -55,11 +55,11 @@ hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers,
   int64_t blocks = (total + 255) / 256;
   if (blocks > 65536) blocks = 65536;
   if (bf16)
-    k_pack<bf16_t><<<(unsigned)blocks, 256, 0, s>>>((const bf16_t *)src, N, K, g.KFr, g.NT, layers,
-                                                    src_layer_stride, (uint4 *)dst);
+    PF_TRY(launch_k(k_pack<bf16_t>, (unsigned)blocks, 256, s, (const bf16_t *)src, N, K, g.KFr, g.NT, layers,
+                                                    src_layer_stride, (uint4 *)dst));
   else
-    k_pack<float><<<(unsigned)blocks, 256, 0, s>>>((const float *)src, N, K, g.KFr, g.NT, layers,
-                                                   src_layer_stride, (uint4 *)dst);
+    PF_TRY(launch_k(k_pack<float>, (unsigned)blocks, 256, s, (const float *)src, N, K, g.KFr, g.NT, layers,
+                                                   src_layer_stride, (uint4 *)dst));
   return hipGetLastError();
 }
 
@@ -110,14 +110,13 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 #pragma unroll
   for (int j = 0; j < NT; ++j)
     wbase[j] = tv[j] ? (uint32_t)(((tile[j] * a.KFr + f0) * 64 + lane) * 16) : kOOB;
-  // rows past M are padding of the last 16-row tile: their lanes load
-  // nothing (out-of-bounds offset gives zeros without memory traffic)
+  // X is fragment-packed: fragment (m, f) is 64 lanes x 16 B, contiguous.
+  // Rows past M are padding of the last 16-row tile: their lanes load
+  // nothing (out-of-bounds offset gives zeros without memory traffic).
+  const int64_t xkfr = a.ldx / (4 * E);
 #pragma unroll
   for (int m = 0; m < MT; ++m)
-    xbase[m] = m * 16 + (lane & 15) < a.M
-                   ? (uint32_t)((((int64_t)(m * 16 + (lane & 15))) * a.ldx + f0 * 4 * E +
-                                 (lane >> 4) * E) * sizeof(T))
-                   : kOOB;
+    xbase[m] = m * 16 + (lane & 15) < a.M ? (uint32_t)(((m * xkfr + f0) * 64 + lane) * 16) : kOOB;
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -134,11 +133,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     const bool in = i < n;
 #pragma unroll
     for (int j = 0; j < NT; ++j)
-      wv[u][j] = bload16(wr, in && wbase[j] != kOOB ? wbase[j] + (uint32_t)(i * 1024) : kOOB);
+      wv[u][j] = bload16_stream(wr, in && wbase[j] != kOOB ? wbase[j] + (uint32_t)(i * 1024) : kOOB);
 #pragma unroll
     for (int m = 0; m < MT; ++m)
-      xv[u][m] = bload16(xr, in && xbase[m] != kOOB ? xbase[m] + (uint32_t)(i * 4 * E * sizeof(T))
-                                                      : kOOB);
+      xv[u][m] = bload16(xr, in && xbase[m] != kOOB ? xbase[m] + (uint32_t)(i * 1024) : kOOB);
   };
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
@@ -197,8 +195,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     for (int m = 0; m < MT; ++m) {
       int row = m * 16 + (lane & 15);
       if (row >= a.M) continue;
+      // act is the next GEMM's X: fragment-packed; the four columns stay in
+      // one E-element chunk
       int64_t col = tile[0] * 16 + 4 * q;
-      T *dst = (T *)a.act + (int64_t)row * a.ldact + col;
+      T *dst = (T *)a.act + act_off<T>(row, col, a.ldact);
 #pragma unroll
       for (int i = 0; i < 4; ++i) Elem<T>::store(dst, i, silu(acc[m][0][i]) * acc[m][1][i]);
     }
@@ -269,11 +269,11 @@ int gemm_tiles_per_block(int epi) {
 template <typename T, int EPI>
 static hipError_t launch_t(int mt, const GemmArgs &a, dim3 grid, hipStream_t s) {
   switch (mt) {
-    case 1: k_gemm<T, 1, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 2: k_gemm<T, 2, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 3: k_gemm<T, 3, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 4: k_gemm<T, 4, EPI><<<grid, 256, 0, s>>>(a); break;
-    case 5: k_gemm<T, 5, EPI><<<grid, 256, 0, s>>>(a); break;
+    case 1: return launch_k(k_gemm<T, 1, EPI>, grid, 256, s, a);
+    case 2: return launch_k(k_gemm<T, 2, EPI>, grid, 256, s, a);
+    case 3: return launch_k(k_gemm<T, 3, EPI>, grid, 256, s, a);
+    case 4: return launch_k(k_gemm<T, 4, EPI>, grid, 256, s, a);
+    case 5: return launch_k(k_gemm<T, 5, EPI>, grid, 256, s, a);
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

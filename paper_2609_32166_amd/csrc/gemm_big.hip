@@ -122,13 +122,13 @@ static hipError_t big_t(int epi, const BigGemmArgs &a, hipStream_t s) {
   const unsigned gy = (unsigned)((a.M + 127) / 128);
   if (epi == BIG_SWIGLU) {
     dim3 grid((unsigned)((a.up_tile_off + 3) / 4), gy);
-    k_gemm_big<T, BIG_SWIGLU><<<grid, 256, 0, s>>>(a);
+    PF_TRY(launch_k(k_gemm_big<T, BIG_SWIGLU>, grid, 256, s, a));
   } else {
     dim3 grid((unsigned)((a.NTtot + 7) / 8), gy);
     if (epi == BIG_STORE)
-      k_gemm_big<T, BIG_STORE><<<grid, 256, 0, s>>>(a);
+      PF_TRY(launch_k(k_gemm_big<T, BIG_STORE>, grid, 256, s, a));
     else
-      k_gemm_big<T, BIG_RESID><<<grid, 256, 0, s>>>(a);
+      PF_TRY(launch_k(k_gemm_big<T, BIG_RESID>, grid, 256, s, a));
   }
   return hipGetLastError();
 }

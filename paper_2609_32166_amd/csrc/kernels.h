@@ -1,9 +1,45 @@
 // Host-side launchers of the HIP kernels (internal to libpf).
 #pragma once
 
+#include <utility>
+
 #include "pf_internal.h"
 
 namespace pf {
+
+// Kernel timing for the profiled verify step. While a timer is installed on
+// the calling thread, every launch is bracketed by its own pair of events
+// recorded on the launch stream (created without the system-scope fence, so
+// a marker does not write back and invalidate the caches). A failure to
+// create events is kept in the timer and reported by its owner.
+struct LaunchTimer {
+  hipError_t err = hipSuccess;
+  virtual bool events(hipEvent_t *start, hipEvent_t *stop) = 0;
+  virtual ~LaunchTimer() = default;
+};
+extern thread_local LaunchTimer *t_launch_timer;
+
+template <typename... P, typename... A>
+inline hipError_t launch_k(void (*k)(P...), dim3 grid, dim3 block, hipStream_t s, A &&...args) {
+  hipEvent_t e0, e1;
+  LaunchTimer *t = t_launch_timer;
+  const bool timed = t && t->events(&e0, &e1);
+  if (timed) {
+    hipError_t r = hipEventRecord(e0, s);
+    if (r != hipSuccess) return r;
+  }
+  k<<<grid, block, 0, s>>>(std::forward<A>(args)...);
+  hipError_t r = hipGetLastError();
+  if (r != hipSuccess || !timed) return r;
+  return hipEventRecord(e1, s);
+}
+
+// Returns the error of a launch helper from the enclosing launcher.
+#define PF_TRY(...)                          \
+  do {                                       \
+    hipError_t e_ = (__VA_ARGS__);           \
+    if (e_ != hipSuccess) return e_;         \
+  } while (0)
 
 // Buffer-resource loads: 16-byte loads whose byte offset is checked against
 // the resource size; an offset past the end returns zeros and fetches
@@ -19,6 +55,13 @@ __device__ inline rsrc_t make_rsrc(const void *p, uint32_t bytes) {
 }
 __device__ inline uint4 bload16(rsrc_t r, uint32_t off) {
   v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+// Same, with the non-temporal cache policy: for data read exactly once per
+// launch (weight streams), so it does not displace reused lines in L2.
+constexpr int kPolicyNT = 2;
+__device__ inline uint4 bload16_stream(rsrc_t r, uint32_t off) {
+  v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kPolicyNT);
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
@@ -58,7 +101,8 @@ struct AttnArgs {
                         // past M must be readable)
   const int32_t *kv_len;  // P (device)
   int n_splits;         // key ranges (grid.x)
-  int chunk_keys;       // keys per range (multiple of 32)
+  int chunk_keys;       // keys per range (multiple of the chunk, 32 bf16 / 16 fp32)
+  int keys_bound;       // host upper bound on P + M (loads stay below it)
   float scale_log2;     // log2(e) / sqrt(head_dim)
   int tree;
   const uint64_t *anc;  // [kRowPad] draft-key visibility of each row (tree)
@@ -66,6 +110,7 @@ struct AttnArgs {
   float *part_ml;       // [n_heads][n_splits][kRowPad][2]
   void *out;            // [kRowPad][ldout] attention output (model dtype)
   int64_t ldout;
+  int out_packed;       // out in the fragment-packed activation layout
 };
 
 hipError_t launch_attn(bool bf16, int rt, const AttnArgs &a, hipStream_t s);
@@ -86,20 +131,20 @@ struct StepArgs {
 hipError_t launch_prep(const StepArgs &a, hipStream_t s);
 hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
                              const float *gain, float eps, float *x, void *xn, int64_t ldxn,
-                             hipStream_t s);
+                             bool packed, hipStream_t s);
 hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int rowpad, int M, int nq,
                            int nkv, int hd, int64_t ldpart, const float *rope, const int32_t *kv_len,
                            void *qbuf, int64_t ldq, void *cache, int layer, int64_t cap,
                            hipStream_t s);
 hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
                                 int64_t ldpart, const float *gain, float eps, float *x, void *xn,
-                                int64_t ldxn, hipStream_t s);
+                                int64_t ldxn, bool packed, hipStream_t s);
 // prefill rows: tokens[i] at position P + i (P = *kv_len), RoPE table, rowinfo
 hipError_t launch_prefill_rows(const int32_t *tokens, int n, int V, const int32_t *kv_len,
                                const double *inv_freq, int hd, int32_t *rowinfo, float *rope,
                                int32_t *status, hipStream_t s);
 hipError_t launch_add_int(int32_t *p, int32_t v, hipStream_t s);
-hipError_t launch_copy_row(const void *src, void *dst, int64_t bytes, hipStream_t s);
+hipError_t launch_pack_row(bool bf16, const void *src, void *dst, int64_t ld, hipStream_t s);
 
 // tiled GEMM for prefill chunks (gemm_big.hip): Y[M x N] = X[M x K] W^T,
 // 128 x 128 block tiles, epilogues below
@@ -129,6 +174,7 @@ hipError_t launch_kv_copy(bool bf16, bool import_, void *cache, const void *logi
                           void *logical_dst, int L, int nkv, int hd, int64_t cap, int64_t start,
                           int64_t n, hipStream_t s);
 hipError_t launch_set_int(int32_t *p, int32_t v, hipStream_t s);
+hipError_t launch_hold(const int32_t *flag, uint64_t max_ticks, hipStream_t s);
 
 // lookup (lookup.hip)
 struct LookupArgs {

@@ -147,7 +147,7 @@ __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
 }
 
 hipError_t launch_lookup(const LookupArgs &a, hipStream_t s) {
-  k_lookup<<<1, 256, 0, s>>>(a);
+  PF_TRY(launch_k(k_lookup, 1, 256, s, a));
   return hipGetLastError();
 }
 

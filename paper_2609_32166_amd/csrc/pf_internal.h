@@ -48,6 +48,17 @@ template <> struct Elem<bf16_t> {
 // quarters x E elements).
 template <typename T> constexpr int frag_k() { return 4 * Elem<T>::E; }
 
+// Activation layout read by the skinny verify GEMM ("fragment-packed"): for
+// every 16-row tile and every k fragment, the 64 lanes' E-element chunks are
+// stored contiguously (lane = row % 16 + 16 * quarter), so one wave's operand
+// fragment is a single coalesced 1 KiB load. `ld` is the padded row length, a
+// multiple of 4E; the buffer size equals that of a row-major [rows][ld] array.
+template <typename T> __device__ inline int64_t act_off(int row, int64_t k, int64_t ld) {
+  constexpr int E = Elem<T>::E, KF = 4 * E;
+  return (((int64_t)(row >> 4) * (ld / KF) + k / KF) * 64 + ((k % KF) / E) * 16 + (row & 15)) * E +
+         k % E;
+}
+
 // ---------------------------------------------------------------------------
 // MFMA step: D(16x16) += A(16 x KF) * B(KF x 16) where every lane supplies
 // one 16-byte chunk of A and of B. Lane l carries row l%16 of A and column
@@ -142,6 +153,7 @@ struct pf_model {
   float *apart_o = nullptr;  // attention partial outputs
   float *apart_ml = nullptr; // attention partial (max, sum)
   int64_t apart_rows = 0;    // capacity in (head, split, row) units
+  int wave_slots = 1024;     // SIMDs of the device: waves resident at once at 1 per SIMD
   pf::ArgmaxPart *amax = nullptr;  // lm_head argmax partials
   int64_t amax_elems = 0;
   float *rope = nullptr;     // [kRowPad][head_dim/2][2] cos, sin of the step's rows
