@@ -102,16 +102,135 @@ def cpu_baseline(wl, w, kv_host, draft, layers: int):
             "seconds": round(dt, 2)}
 
 
+def _capture(torch, fn):
+    """One HIP graph of fn's launches (captured on a side stream after a
+    warm-up call, as torch requires)."""
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    with torch.cuda.graph(g):
+        fn()
+    return g
+
+
+def _time_graph(torch, g, reps, warm=5):
+    for _ in range(warm):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def phase_timings(torch, pf, wl, model, kv, st, c, ctx, draft, res, args, ms_step, step):
+    """Graph-replay timings beside the headline: per-replay percentiles of
+    the whole step, lookup / verify / commit separately, the M = 1 greedy
+    decode step, the verify step over a K sweep, and acceptance on the seeded
+    90/10 hit/miss query mix."""
+    max_nodes = wl.max_nodes if wl.tree else 64
+    n_cand = wl.n_cand if wl.tree else 1
+    out = {}
+    # per-replay percentiles of the whole step (one event pair per replay)
+    g = _capture(torch, step)
+    for _ in range(5):
+        g.replay()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:
+        a.record()
+        g.replay()
+        b.record()
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in ev])
+    out["step_ms_percentiles"] = {"p10": round(float(np.percentile(t, 10)), 4),
+                                  "p50": round(float(np.percentile(t, 50)), 4),
+                                  "p90": round(float(np.percentile(t, 90)), 4),
+                                  "replays": len(t)}
+    del g
+
+    def lookup():
+        pf.pf_context_init(c, len(ctx))
+        pf.pf_draft_lookup(st, c, wl.k_max, wl.tree, n_cand, max_nodes, draft)
+
+    def verify():
+        pf.pf_kv_set_len(kv, wl.prefix)
+        pf.pf_verify_step(model, kv, draft, wl.rows, wl.tree, None, res)
+
+    lookup()
+    t_lookup = _time_graph(torch, _capture(torch, lookup), 50)
+    gv = _capture(torch, verify)
+    t_verify = _time_graph(torch, gv, 50)
+    # the capture left a verify pending on the host side; commit it once
+    pf.pf_kv_commit(kv, res, None)
+    out["phases_ms"] = {"lookup (context reset + lookup)": round(t_lookup, 4),
+                        "verify (length reset + verify)": round(t_verify, 4),
+                        "commit (+ launch overhead, step minus the two)":
+                            round(ms_step - t_lookup - t_verify, 4),
+                        "step": round(ms_step, 4)}
+
+    def step_k(k):
+        rows = k + 1
+
+        def fn():
+            pf.pf_kv_set_len(kv, wl.prefix)
+            pf.pf_context_init(c, len(ctx))
+            pf.pf_draft_lookup(st, c, k, 0, 1, 64, draft)
+            pf.pf_verify_step(model, kv, draft, rows, 0, None, res)
+            pf.pf_kv_commit(kv, res, c)
+        return fn
+
+    if not wl.tree:
+        sweep = {}
+        for k in (0, 4, 8, 16, 32, 64):
+            sweep[str(k)] = round(_time_graph(torch, _capture(torch, step_k(k)), 30), 4)
+        t_greedy = sweep["0"]
+        out["k_sweep_step_ms"] = sweep
+        out["greedy_step_ms"] = t_greedy
+        K = wl.k_max
+        out["speedup_vs_greedy"] = {f"l_acc={l}": round((l + 1) * t_greedy / ms_step, 2)
+                                    for l in (0, K // 2, K)}
+    # acceptance on the seeded query mix (90% store hits, 10% fresh n-grams);
+    # with random-init weights the model's greedy tokens rarely match a draft
+    rng = np.random.default_rng(synth.case_seed(wl, 7))
+    store = synth.make_store(wl, synth.case_seed(wl, 0))
+    accepted = []
+    for i in range(20):
+        hit = bool(rng.random() < 0.9)
+        cx, _ = synth.make_context(wl, synth.case_seed(wl, 100 + i), store, hit=hit)
+        cc = pf.Context(cx, len(cx) + 2 * 65)
+        pf.pf_kv_set_len(kv, wl.prefix)
+        pf.pf_draft_lookup(st, cc, wl.k_max, wl.tree, n_cand, max_nodes, draft)
+        pf.pf_verify_step(model, kv, draft, wl.rows, wl.tree, None, res)
+        pf.pf_kv_commit(kv, res, cc)
+        torch.cuda.synchronize()
+        accepted.append(int(pf.read_result(res)["accept_len"]))
+    mean_acc = float(np.mean(accepted))
+    out["query_mix"] = {"cases": len(accepted), "hit_fraction": 0.9,
+                        "mean_l_acc": round(mean_acc, 3),
+                        "accepted_tokens_per_s": round((mean_acc + 1) / (ms_step * 1e-3), 1)}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="3b", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--profile-steps", type=int, default=5)
     ap.add_argument("--cpu-layers", type=int, default=0, help="0: every layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the phase split, percentiles, greedy and K-sweep timings")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="also run a plain device copy of this many MiB (for counter scaling)")
     args = ap.parse_args()
@@ -142,7 +261,8 @@ def main():
     model = pf.pf_model_create(pf.model_config(shape), wdev)
     del wdev
     torch.cuda.empty_cache()
-    cap = ((wl.prefix + 2 * wl.rows + 63) // 64) * 64
+    # room for the K sweep (up to 64 drafts: 65 rows) on top of the prefix
+    cap = ((wl.prefix + 2 * 65 + 63) // 64) * 64
     kv = pf.KVCache(model, cap)
     kvd = pf.array_to_device(kv_host)
     prefill = None
@@ -171,7 +291,7 @@ def main():
         # the verify step then runs on the synthetic full prefix (same length)
     pf.pf_kv_import(kv, kvd, wl.prefix)
     st = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
-    c = pf.Context(ctx, len(ctx) + 2 * wl.rows)
+    c = pf.Context(ctx, len(ctx) + 2 * 65)
     draft, res = pf.new_draft(), pf.new_result()
     torch.cuda.synchronize()
     del kvd
@@ -228,6 +348,15 @@ def main():
     d = pf.read_draft(draft)
     log(f"step {ms:.3f} ms (eager {ms_eager:.3f} ms), draft {int(d['n_nodes']) - 1} tokens, "
         f"accepted {int(r['accept_len'])}")
+
+    extra = {}
+    if not args.no_graph and not args.no_sweep:
+        extra = phase_timings(torch, pf, wl, model, kv, st, c, ctx, draft, res, args, ms, step)
+        d = pf.read_draft(draft)  # the sweep reuses the buffers; restore the main step
+        step()
+        torch.cuda.synchronize()
+        r = pf.read_result(res)
+        d = pf.read_draft(draft)
 
     # per-kernel durations: an event pair around every launch, the stream held
     # until the step is enqueued, the cost of an empty pair subtracted
@@ -286,6 +415,7 @@ def main():
                      "traffic_source": traffic_note},
         "kernels": kernels,
     }
+    out.update(extra)
     if prefill is not None:
         out["prefill"] = prefill
     if not args.no_cpu_baseline:
