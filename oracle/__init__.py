@@ -17,7 +17,11 @@ It computes, with plain fp64 loops in ``oracle.c``, what the paper
   matching proposal prefix plus the model's next token, which must equal
   greedy decoding ("Single-pass token verification");
 * the KV commit implied by that acceptance, and the prompt-prefix carryover
-  that resumes computation right after a reused prefix (Section 3.4).
+  that resumes computation right after a reused prefix (Section 3.4);
+* the paper's own retrieval keys and lookup: final-layer states projected to
+  256-dimensional int8 keys by a fixed random projection (Section 4) and the
+  cosine argmax over the entries whose stored token matches the query token
+  and that precede their boundary (Section 3.2).
 
 Parity of the forward's logit values is pinned only by the invariants and
 closed forms in the tests; the paper prints no worked numeric example for it.
@@ -66,7 +70,7 @@ def lib():
         vp, i32, i64, f64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
         L.or_forward.restype = i32
         L.or_forward.argtypes = [ctypes.POINTER(_Model), vp, i64, vp, i64, i32, vp, vp, vp, i32,
-                                 vp, vp]
+                                 vp, vp, vp]
         L.or_lookup_candidates.restype = i32
         L.or_lookup_candidates.argtypes = [vp, vp, i64, i32, vp, i64, i32, i32, vp, vp]
         L.or_build_draft.restype = i32
@@ -89,6 +93,11 @@ def lib():
         L.or_attend.argtypes = [vp, vp, vp, i64, i32, f64, vp]
         L.or_argmax.restype = ctypes.c_int32
         L.or_argmax.argtypes = [vp, i64]
+        L.or_key_encode.restype = None
+        L.or_key_encode.argtypes = [vp, i32, i32, vp, i64, vp]
+        L.or_cos_candidates.restype = i32
+        L.or_cos_candidates.argtypes = [vp, vp, i64, vp, i32, ctypes.c_int32, vp, i32, i32, vp,
+                                        vp, vp]
         L.or_set_threads.restype = None
         L.or_set_threads.argtypes = [i32]
         L.or_get_threads.restype = i32
@@ -192,9 +201,11 @@ class Model:
 
     def forward(self, kv_prefix: np.ndarray, tok: Sequence[int], pos: Sequence[int],
                 vis: np.ndarray, kv_extra: Optional[np.ndarray] = None, logits_from: int = 0,
-                want_logits: bool = True, want_kv: bool = True):
+                want_logits: bool = True, want_kv: bool = True, hidden: Optional[np.ndarray] = None):
         """Forward of M new rows. Returns (logits [M][V] fp32 or None, kv_new
-        [L][2][nkv][M][hd] fp64 or None). kv_prefix: [L][2][nkv][P][hd]."""
+        [L][2][nkv][M][hd] fp64 or None). kv_prefix: [L][2][nkv][P][hd].
+        hidden, if given ([M][H] fp64), receives the final-layer states of
+        rows >= logits_from (the lm_head input)."""
         s = self.shape
         kv_prefix = np.ascontiguousarray(kv_prefix)
         P = kv_prefix.shape[3]
@@ -210,9 +221,12 @@ class Model:
         logits = np.zeros((M, s.vocab), np.float32) if want_logits else None
         kv_new = (np.zeros((s.n_layers, 2, s.n_kv_heads, M, s.head_dim), np.float64)
                   if want_kv else None)
+        if hidden is not None:
+            assert hidden.dtype == np.float64 and hidden.shape == (M, s.hidden)
+            assert hidden.flags.c_contiguous
         lib().or_forward(ctypes.byref(self._c), _ptr(kv_prefix), P, _ptr(kv_extra), E, M,
                          _ptr(tok), _ptr(pos), _ptr(vis), int(logits_from), _ptr(logits),
-                         _ptr(kv_new))
+                         _ptr(kv_new), _ptr(hidden))
         return logits, kv_new
 
 
@@ -245,6 +259,51 @@ def lookup(tokens: np.ndarray, seq_offsets: np.ndarray, ngram: int, ctx: np.ndar
     return {"n_nodes": int(n), "token": ntok[:n].copy(), "parent": par[:n].copy(),
             "depth": dep[:n].copy(), "anc": anc[:n].copy(), "n_found": int(found),
             "cand_pos": cpos[:found].copy(), "cand_len": clen[:found].copy()}
+
+
+KEY_DIM = 256  # Section 4: 256-dimensional int8 retrieval keys
+
+
+def key_encode(R: np.ndarray, h: np.ndarray) -> np.ndarray:
+    """int8 retrieval keys of hidden states h [n][H] under the projection R
+    [KEY_DIM][H] (see or_key_encode)."""
+    R = np.ascontiguousarray(R, np.float64)
+    h = np.ascontiguousarray(np.atleast_2d(h), np.float64)
+    kd, H = R.shape
+    assert h.shape[1] == H and kd <= 1024
+    out = np.zeros((h.shape[0], kd), np.int8)
+    lib().or_key_encode(_ptr(R), kd, H, _ptr(h), h.shape[0], _ptr(out))
+    return out
+
+
+def cos_lookup(tokens: np.ndarray, seq_offsets: np.ndarray, keys: np.ndarray, y: int,
+               qkey: np.ndarray, k_max: int, n_cand: int = 1, tree: bool = False,
+               max_nodes: int = 64) -> dict:
+    """Cosine retrieval over keyed store entries (see or_cos_candidates) and
+    the same draft construction as the n-gram lookup; node 0 is y."""
+    tokens = np.ascontiguousarray(tokens, np.int32)
+    seq_offsets = np.ascontiguousarray(seq_offsets, np.int64)
+    keys = np.ascontiguousarray(keys, np.int8)
+    qkey = np.ascontiguousarray(qkey, np.int8).reshape(-1)
+    kd = qkey.shape[0]
+    assert keys.shape == (len(tokens), kd)
+    nc = max(1, n_cand)
+    cpos = np.zeros(nc, np.int64)
+    clen = np.zeros(nc, np.int32)
+    ccos = np.zeros(nc, np.float64)
+    found = lib().or_cos_candidates(_ptr(tokens), _ptr(seq_offsets), len(seq_offsets) - 1,
+                                    _ptr(keys), kd, int(y), _ptr(qkey), k_max, nc, _ptr(cpos),
+                                    _ptr(clen), _ptr(ccos))
+    ntok = np.zeros(MAX_NODES, np.int32)
+    par = np.zeros(MAX_NODES, np.int32)
+    dep = np.zeros(MAX_NODES, np.int32)
+    anc = np.zeros(MAX_NODES, np.uint64)
+    n = lib().or_build_draft(_ptr(tokens), _ptr(cpos), _ptr(clen), found, int(y), int(tree),
+                             max_nodes, _ptr(ntok), _ptr(par), _ptr(dep), _ptr(anc))
+    return {"n_nodes": int(n), "token": ntok[:n].copy(), "parent": par[:n].copy(),
+            "depth": dep[:n].copy(), "anc": anc[:n].copy(), "n_found": int(found),
+            "cand_pos": cpos[:found].copy(), "cand_len": clen[:found].copy(),
+            "cand_cos": ccos[:found].copy()}
 
 
 def visibility(draft: dict, rows: int, tree: bool) -> np.ndarray:
@@ -305,16 +364,18 @@ def accept(draft: dict, pred: Sequence[int], tree: bool) -> dict:
 
 
 def verify_batched(model: Model, kv_prefix: np.ndarray, draft: dict, rows: int, tree: bool,
-                   want_logits: bool = True) -> dict:
-    """One forward over every verify row, then greedy accept."""
+                   want_logits: bool = True, want_hidden: bool = False) -> dict:
+    """One forward over every verify row, then greedy accept. With
+    want_hidden, res["hidden"] holds every row's final-layer state."""
     P = kv_prefix.shape[3]
     tok, dep = draft_rows(draft, rows, tree)
     vis = visibility(draft, rows, tree)
-    logits, kv_new = model.forward(kv_prefix, tok, P + dep, vis)
+    hidden = np.zeros((rows, model.shape.hidden), np.float64) if want_hidden else None
+    logits, kv_new = model.forward(kv_prefix, tok, P + dep, vis, hidden=hidden)
     pred = [argmax(logits[j]) for j in range(rows)]
     res = accept(draft, pred, tree)
     res.update(pred=np.array(pred, np.int32), logits=logits if want_logits else None,
-               kv_new=kv_new, tok=tok, pos=P + dep)
+               kv_new=kv_new, tok=tok, pos=P + dep, hidden=hidden)
     return res
 
 

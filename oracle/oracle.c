@@ -176,11 +176,13 @@ void or_attend(const double *q, const double *const *keys, const double *const *
  *              itself; causal for a linear draft, ancestors for a tree)
  *   logits     [M][V] fp32 for rows >= logits_from (others untouched); NULL ok
  *   kv_new     [L][2][nkv][M][hd] fp64 K/V of the new rows; NULL ok
+ *   hidden     [M][H] final-layer states (the final RMSNorm output, rounded
+ *              as it enters the lm_head) for rows >= logits_from; NULL ok
  * Returns 0.
  */
 int or_forward(const or_model *m, const void *kv_prefix, int64_t P, const double *kv_extra,
                int64_t E, int M, const int32_t *tok, const int64_t *pos, const uint8_t *vis,
-               int logits_from, float *logits, double *kv_new) {
+               int logits_from, float *logits, double *kv_new, double *hidden) {
   const int L = m->L, H = m->H, nq = m->nq, nkv = m->nkv, hd = m->hd, F = m->F;
   const int64_t V = m->V;
   const int qd = nq * hd, kvd = nkv * hd, nqkv = qd + 2 * kvd, grp = nq / nkv;
@@ -281,13 +283,18 @@ int or_forward(const or_model *m, const void *kv_prefix, int64_t P, const double
     for (int64_t i = 0; i < (int64_t)M * H; ++i) x[i] += tmp[i];
   }
 
-  if (logits && logits_from < M) {
+  if ((logits || hidden) && logits_from < M) {
     int nr = M - logits_from;
     for (int r = 0; r < nr; ++r) {
       int rr = logits_from + r;
       or_rmsnorm(x + (int64_t)rr * H, m->final_norm, H, m->eps, xn + (int64_t)r * H);
       for (int k = 0; k < H; ++k) xn[(int64_t)r * H + k] = rnd(m, xn[(int64_t)r * H + k]);
     }
+    if (hidden)
+      for (int64_t i = 0; i < (int64_t)nr * H; ++i) hidden[(int64_t)logits_from * H + i] = xn[i];
+  }
+  if (logits && logits_from < M) {
+    int nr = M - logits_from;
     double *lg = (double *)malloc(sizeof(double) * (size_t)nr * V);
     linear(m, m->lm_head, V, H, nr, xn, lg);
     for (int r = 0; r < nr; ++r)
@@ -406,6 +413,119 @@ int or_build_draft(const int32_t *tokens, const int64_t *cand_pos, const int32_t
     }
   }
   return n;
+}
+
+/*
+ * Retrieval keys (Section 4, "Memory and retrieval": normalized final-layer
+ * states are mapped to 256-dimensional int8 keys through a fixed random
+ * projection). h is the final-layer state as it enters the lm_head (the
+ * final RMSNorm output). v = R h with R [kd][H] row-major, in fp64: each
+ * component is summed as 16 interleaved chains (chain c takes k = c, c+16,
+ * c+32, ... in increasing order, each step a fused multiply-add starting from
+ * 0), then the chains are added in order c = 0..15.
+ * The key is the symmetric int8 quantisation of v with a per-vector scale:
+ * code_j = round-half-even(v_j * 127 / max_i |v_i|); an all-zero v gives the
+ * zero key. (A positive rescaling of h changes neither the direction nor,
+ * up to rounding, the codes, so no further normalisation is applied.)
+ */
+void or_key_encode(const double *R, int kd, int H, const double *h, int64_t n, int8_t *out) {
+  for (int64_t r = 0; r < n; ++r) {
+    const double *hr = h + r * H;
+    double v[1024];
+    double mx = 0.0;
+    for (int j = 0; j < kd; ++j) {
+      double chain[16];
+      for (int c = 0; c < 16; ++c) {
+        double acc = 0.0;
+        for (int k = c; k < H; k += 16) acc = fma(R[(int64_t)j * H + k], hr[k], acc);
+        chain[c] = acc;
+      }
+      double sum = chain[0];
+      for (int c = 1; c < 16; ++c) sum += chain[c];
+      v[j] = sum;
+      if (fabs(sum) > mx) mx = fabs(sum);
+    }
+    for (int j = 0; j < kd; ++j) {
+      double c = mx > 0.0 ? rint((v[j] * 127.0) / mx) : 0.0;
+      if (c > 127.0) c = 127.0;
+      if (c < -127.0) c = -127.0;
+      out[r * kd + j] = (int8_t)c;
+    }
+  }
+}
+
+/*
+ * Cosine order of two entries against one query, decided exactly: cos is
+ * dot / sqrt(|q|^2 |k|^2) with integer dot products and squared norms.
+ * Positive cosines rank above zero (a zero dot product or a zero key) and
+ * zero above negative; two positives compare dot_a^2 |k_b|^2 against
+ * dot_b^2 |k_a|^2 (the query norm is common), two negatives the other way.
+ * Returns > 0 if a ranks above b, < 0 if below, 0 if equal.
+ */
+static int cos_cmp(int64_t da, int64_t na, int64_t db, int64_t nb) {
+  int ca = da > 0 ? 2 : (da == 0 ? 1 : 0);
+  int cb = db > 0 ? 2 : (db == 0 ? 1 : 0);
+  if (ca != cb) return ca - cb;
+  if (ca == 1) return 0;
+  __int128 l = (__int128)da * da * nb, r = (__int128)db * db * na;
+  int c = l > r ? 1 : (l < r ? -1 : 0);
+  return ca == 2 ? c : -c;
+}
+
+/*
+ * Cosine retrieval (Section 3.2, "Context-compatible retrieval"): among the
+ * entries p whose stored token equals the query token y and that precede
+ * their output-sequence boundary (p < b(p)), rank by cosine similarity of
+ * the int8 keys (cos_cmp), then by the proposal length min(k_max, b(p) - p),
+ * then by p, larger first. Writes the best n_cand in rank order with their
+ * cosine (fp64, 0 for a zero key) and returns how many were found.
+ */
+int or_cos_candidates(const int32_t *tokens, const int64_t *seq_off, int64_t n_seqs,
+                      const int8_t *keys, int kd, int32_t y, const int8_t *qkey, int k_max,
+                      int n_cand, int64_t *cand_pos, int32_t *cand_len, double *cand_cos) {
+  int found = 0;
+  int64_t nq = 0;
+  for (int j = 0; j < kd; ++j) nq += (int64_t)qkey[j] * qkey[j];
+  int64_t cdot[8], cnk[8];
+  if (n_cand < 1 || n_cand > 8) return 0;
+  for (int64_t s = 0; s < n_seqs; ++s) {
+    int64_t a = seq_off[s], b = seq_off[s + 1] - 1; /* b: last position */
+    for (int64_t p = a; p < b; ++p) {
+      if (tokens[p] != y) continue;
+      int64_t dot = 0, nk = 0;
+      for (int j = 0; j < kd; ++j) {
+        dot += (int64_t)qkey[j] * keys[p * kd + j];
+        nk += (int64_t)keys[p * kd + j] * keys[p * kd + j];
+      }
+      int64_t rem = b - p;
+      int32_t len = (int32_t)(rem < k_max ? rem : k_max);
+      /* insert into the sorted top list */
+      int at = found;
+      while (at > 0) {
+        int c = cos_cmp(dot, nk, cdot[at - 1], cnk[at - 1]);
+        int above = c > 0 || (c == 0 && (len > cand_len[at - 1] ||
+                                         (len == cand_len[at - 1] && p > cand_pos[at - 1])));
+        if (!above) break;
+        --at;
+      }
+      if (at >= n_cand) continue;
+      int last = found < n_cand ? found : n_cand - 1;
+      for (int i = last; i > at; --i) {
+        cand_len[i] = cand_len[i - 1];
+        cand_pos[i] = cand_pos[i - 1];
+        cdot[i] = cdot[i - 1];
+        cnk[i] = cnk[i - 1];
+      }
+      cand_len[at] = len;
+      cand_pos[at] = p;
+      cdot[at] = dot;
+      cnk[at] = nk;
+      if (found < n_cand) ++found;
+    }
+  }
+  for (int i = 0; i < found; ++i)
+    cand_cos[i] = (nq > 0 && cnk[i] > 0) ? (double)cdot[i] / sqrt((double)nq * (double)cnk[i]) : 0.0;
+  return found;
 }
 
 void or_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }

@@ -396,5 +396,39 @@ def case_seed(wl: Workload, case: int) -> int:
     return 1000 * wl.index + case
 
 
+# tensor ids of the retrieval-key inputs
+_T_KEYPROJ, _T_KEYS, _T_HID = 901, 902, 903
+KEY_DIM = 256
+
+
+def key_projection(hidden: int, seed: int) -> np.ndarray:
+    """The fixed random projection of the retrieval keys: [KEY_DIM][hidden]
+    N(0, 1) values in fp32 (exact in fp64)."""
+    return normal_f32(key(seed, _T_KEYPROJ), KEY_DIM * hidden).reshape(KEY_DIM, hidden)
+
+
+def random_keys(n: int, seed: int, first: int = 0) -> np.ndarray:
+    """Arbitrary int8 key codes in [-127, 127], [n][KEY_DIM] (store keys for
+    lookup tests and timing)."""
+    return (randint(key(seed, _T_KEYS), n * KEY_DIM, -127, 128, first * KEY_DIM)
+            .astype(np.int8).reshape(n, KEY_DIM))
+
+
+def perturb_key(k: np.ndarray, seed: int, changes: int = 8, delta: int = 3) -> np.ndarray:
+    """A near copy of key k: `changes` codes moved by up to +-delta (clipped),
+    for queries that should find k's entry."""
+    out = np.array(k, np.int16).reshape(-1).copy()
+    kk = key(seed, _T_KEYS + 1)
+    idx = randint(kk, changes, 0, out.shape[0])
+    d = randint(kk, changes, -delta, delta + 1, changes)
+    out[idx] = np.clip(out[idx] + d, -127, 127)
+    return out.astype(np.int8)
+
+
+def hidden_states(n: int, hidden: int, seed: int) -> np.ndarray:
+    """Synthetic final-layer states [n][hidden], N(0, 1) in fp32."""
+    return normal_f32(key(seed, _T_HID), n * hidden).reshape(n, hidden)
+
+
 def bf16_bits_to_f32(a: np.ndarray) -> np.ndarray:
     return (a.astype(np.uint32) << np.uint32(16)).view(np.float32)
