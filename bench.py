@@ -116,6 +116,15 @@ def _capture(torch, fn):
     return g
 
 
+def _time_inner(torch, fn, inner=20, reps=20):
+    """GPU time of one call of a short fn: `inner` calls captured back to back
+    in one graph, so the graph's fixed replay cost is spread over them."""
+    def many():
+        for _ in range(inner):
+            fn()
+    return _time_graph(torch, _capture(torch, many), reps) / inner
+
+
 def _time_graph(torch, g, reps, warm=5):
     for _ in range(warm):
         g.replay()
@@ -165,12 +174,12 @@ def phase_timings(torch, pf, wl, model, kv, st, c, ctx, draft, res, args, ms_ste
         pf.pf_verify_step(model, kv, draft, wl.rows, wl.tree, None, res)
 
     lookup()
-    t_lookup = _time_graph(torch, _capture(torch, lookup), 50)
+    t_lookup = _time_inner(torch, lookup)
     gv = _capture(torch, verify)
     t_verify = _time_graph(torch, gv, 50)
     # the capture left a verify pending on the host side; commit it once
     pf.pf_kv_commit(kv, res, None)
-    out["phases_ms"] = {"lookup (context reset + lookup)": round(t_lookup, 4),
+    out["phases_ms"] = {"lookup (context reset + lookup; 20 per graph)": round(t_lookup, 4),
                         "verify (length reset + verify)": round(t_verify, 4),
                         "commit (+ launch overhead, step minus the two)":
                             round(ms_step - t_lookup - t_verify, 4),
@@ -216,6 +225,48 @@ def phase_timings(torch, pf, wl, model, kv, st, c, ctx, draft, res, args, ms_ste
     out["query_mix"] = {"cases": len(accepted), "hit_fraction": 0.9,
                         "mean_l_acc": round(mean_acc, 3),
                         "accepted_tokens_per_s": round((mean_acc + 1) / (ms_step * 1e-3), 1)}
+    return out
+
+
+def cosine_timings(torch, pf, wl, store, model, res, st, ctx):
+    """The paper's own retrieval (Section 3.2 / Section 4): keys of every
+    stored position (seeded int8 codes standing in for the keys of real
+    final-layer states), the cosine lookup timed as graph replays for the
+    most frequent stored token (the longest entry list: the worst case) and
+    for the query context's token, and the query-key encode of a verify
+    step's bonus row."""
+    T = int(store.tokens.shape[0])
+    keys = np.empty((T, pf.KEY_DIM), np.int8)
+    for a in range(0, T, 1 << 18):  # in chunks (the generator's temporaries are 16 B per code)
+        b = min(T, a + (1 << 18))
+        keys[a:b] = synth.random_keys(b - a, synth.case_seed(wl, 11), first=a)
+    pf.pf_store_attach_keys(st, keys)
+    R = synth.key_projection(wl.model.hidden, synth.case_seed(wl, 12))
+    kp = pf.pf_keyproj_create(R)
+    q = torch.zeros(pf.KEY_DIM, dtype=torch.int8, device="cuda")
+    # the query key of the last verify step (also timed below)
+    pf.pf_verify_query_key(model, kp, res, q)
+    draft = pf.new_draft()
+    counts = np.bincount(store.tokens[store.tokens >= 0])
+    out = {"store_positions": T, "key_bytes": T * pf.KEY_DIM}
+    for label, y in (("most_frequent_token", int(np.argmax(counts))),
+                     ("query_context_token", int(ctx[-1]))):
+        cx = np.concatenate([np.asarray(ctx[:-1], np.int32), [y]]).astype(np.int32)
+        c = pf.Context(cx, len(cx) + 8)
+
+        def look():
+            pf.pf_draft_lookup_cosine(st, c, q, wl.k_max, 0, 1, 64, draft)
+        look()
+        torch.cuda.synchronize()
+        d = pf.read_draft(draft)
+        n_ent = int(d["n_eligible"])
+        us = 1e3 * _time_inner(torch, look)
+        out[label] = {"token": y, "entries": n_ent, "us_per_lookup": round(us, 2),
+                      "key_GBps": round(n_ent * pf.KEY_DIM / (us * 1e-6) / 1e9, 1)}
+
+    def enc():
+        pf.pf_verify_query_key(model, kp, res, q)
+    out["query_key_encode_us"] = round(1e3 * _time_inner(torch, enc), 2)
     return out
 
 
@@ -416,6 +467,8 @@ def main():
         "kernels": kernels,
     }
     out.update(extra)
+    if not args.no_graph and not args.no_sweep:
+        out["cosine_retrieval"] = cosine_timings(torch, pf, wl, store, model, res, st, ctx)
     if prefill is not None:
         out["prefill"] = prefill
     if not args.no_cpu_baseline:

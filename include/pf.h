@@ -84,6 +84,8 @@ typedef struct pf_draft {
   uint64_t anc[PF_MAX_NODES];
   int32_t cand_len[PF_MAX_CAND];  /* proposal length of candidate c */
   int64_t cand_pos[PF_MAX_CAND];  /* store position p of candidate c */
+  float cand_score[PF_MAX_CAND];  /* cosine similarity of candidate c (cosine
+                                     lookup; 0 for the n-gram lookup) */
 } pf_draft;
 
 /* Verify result (device memory, written by pf_verify_step). */
@@ -154,6 +156,60 @@ int64_t pf_store_size(const pf_store *store); /* tokens T */
 pf_status pf_draft_lookup(const pf_store *store, const pf_context *ctx, int32_t k_max,
                           int32_t tree, int32_t n_cand, int32_t max_nodes, pf_draft *draft_dev,
                           pf_stream s);
+
+/* ------------------------------------------------------------------------ */
+/* Cosine retrieval over final-layer states (Section 3.2 "Context-compatible */
+/* retrieval"; Section 4 "Memory and retrieval")                            */
+/* ------------------------------------------------------------------------ */
+
+/* Entries are indexed by the decoder's final-layer state h (the final RMSNorm
+ * output as it enters the lm_head), mapped to PF_KEY_DIM int8 codes through
+ * a fixed random projection R [PF_KEY_DIM][hidden]. */
+#define PF_KEY_DIM 256
+
+typedef struct pf_keyproj pf_keyproj;
+
+/* Copy the projection R_host ([PF_KEY_DIM][hidden] fp32 values, row-major)
+ * to the device. hidden in [16, 8192]. */
+pf_status pf_keyproj_create(const float *R_host, int32_t hidden, pf_keyproj **out);
+void pf_keyproj_destroy(pf_keyproj *kp);
+
+/*
+ * Keys of n states: h_dev [n][ld] (PF_DTYPE_F32 or PF_DTYPE_BF16 values, the
+ * first `hidden` of each row used) -> keys_dev int8 [n][PF_KEY_DIM].
+ * v = R h in fp64, each component summed as 16 interleaved fused
+ * multiply-add chains (chain c takes k = c, c+16, ... in increasing order)
+ * added in order c = 0..15; code_j = round-half-even(v_j * 127 / max|v|),
+ * the zero key for v = 0. The codes are therefore identical on any IEEE
+ * fp64 machine that follows the same order. n in [0, 2^20]; ld >= hidden.
+ */
+pf_status pf_key_encode(const pf_keyproj *kp, const void *h_dev, int32_t dtype, int64_t ld,
+                        int64_t n, int8_t *keys_dev, pf_stream s);
+
+/*
+ * Give a store its cosine index: keys_host int8 [T][PF_KEY_DIM], the key of
+ * the state that produced each stored token (T = pf_store_size). An entry is
+ * a position p that precedes its output-sequence boundary (p < b(p)); the
+ * entries are grouped by their stored token. Replaces a previous index. The
+ * host array is copied.
+ */
+pf_status pf_store_attach_keys(pf_store *store, const int8_t *keys_host, pf_stream s);
+
+/*
+ * Cosine draft lookup. The query is (y, q): y the current token (the last
+ * context token, on the device) and q_dev int8 [PF_KEY_DIM] the key of the
+ * state that predicted it. Eligible entries are those whose stored token is
+ * y (and p < b(p)). They rank by cosine similarity of the keys, decided
+ * exactly in integers (a positive cosine above zero -- a zero dot product or
+ * a zero key -- above a negative one; within a sign by dot^2 / |key|^2), then
+ * by proposal length min(k_max, b(p) - p), then by p, larger first. Drafts
+ * are built as in pf_draft_lookup (linear, or a trie of the best n_cand);
+ * cand_score holds each candidate's cosine. No eligible entry gives an
+ * empty proposal. Requires pf_store_attach_keys and *ctx->len >= 1.
+ */
+pf_status pf_draft_lookup_cosine(const pf_store *store, const pf_context *ctx,
+                                 const int8_t *q_dev, int32_t k_max, int32_t tree, int32_t n_cand,
+                                 int32_t max_nodes, pf_draft *draft_dev, pf_stream s);
 
 /* ------------------------------------------------------------------------ */
 /* Model                                                                    */
@@ -282,6 +338,21 @@ pf_status pf_verify_step_profiled(pf_model *model, pf_kv_cache *kv, const pf_dra
                                   int32_t rows, int32_t tree, float *logits_dev,
                                   pf_verify_result *res_dev, pf_stream s, double *ms_out,
                                   int32_t *count_out);
+
+/*
+ * Retrieval keys from the last verify step's final-layer states (they stay
+ * in the model's work buffers until its next verify step or prefill).
+ * pf_verify_query_key: the key of the row whose prediction is the bonus token
+ * (node path[accept_len]), i.e. the query of the next iteration (Section 3.2:
+ * the final token of an iteration and the state that produced it form the
+ * next retrieval query). pf_verify_row_keys: the keys of rows 0..rows-1 (the
+ * contexts of the verified tokens, for adding them to the store). The model's
+ * hidden size must equal the projection's. keys int8 device memory.
+ */
+pf_status pf_verify_query_key(const pf_model *model, const pf_keyproj *kp,
+                              const pf_verify_result *res_dev, int8_t *q_dev, pf_stream s);
+pf_status pf_verify_row_keys(const pf_model *model, const pf_keyproj *kp, int32_t rows,
+                             int8_t *keys_dev, pf_stream s);
 
 /*
  * Commit the accepted rows (Section 3.2: the iteration advances the output

@@ -26,17 +26,21 @@ PF_VSTATUS_NAN, PF_VSTATUS_CTX_FULL = 1, 2
 DRAFT_DTYPE = np.dtype([("n_nodes", "<i4"), ("tree", "<i4"), ("n_found", "<i4"),
                         ("n_eligible", "<i4"), ("token", "<i4", 65), ("parent", "<i4", 65),
                         ("depth", "<i4", 65), ("reserved0", "<i4"), ("anc", "<u8", 65),
-                        ("cand_len", "<i4", 4), ("cand_pos", "<i8", 4)])
+                        ("cand_len", "<i4", 4), ("cand_pos", "<i8", 4),
+                        ("cand_score", "<f4", 4)])
 RESULT_DTYPE = np.dtype([("accept_len", "<i4"), ("bonus", "<i4"), ("rows", "<i4"),
                          ("status", "<i4"), ("kv_base", "<i8"), ("path", "<i4", 65),
                          ("pred", "<i4", 65), ("out_tokens", "<i4", 65), ("reserved0", "<i4")])
-assert DRAFT_DTYPE.itemsize == 1368 and RESULT_DTYPE.itemsize == 808
+assert DRAFT_DTYPE.itemsize == 1384 and RESULT_DTYPE.itemsize == 808
+KEY_DIM = 256
 
 EXPORTED = ["pf_last_error", "pf_version", "pf_context_init", "pf_context_sync_bound",
             "pf_store_build", "pf_store_destroy", "pf_store_size", "pf_draft_lookup",
             "pf_model_create", "pf_model_destroy", "pf_model_bytes", "pf_kv_bytes", "pf_kv_init",
             "pf_kv_import", "pf_kv_export", "pf_kv_set_len", "pf_kv_sync_bound", "pf_verify_step",
-            "pf_kv_commit", "pf_prefill", "pf_verify_step_profiled"]
+            "pf_kv_commit", "pf_prefill", "pf_verify_step_profiled", "pf_keyproj_create",
+            "pf_keyproj_destroy", "pf_key_encode", "pf_store_attach_keys",
+            "pf_draft_lookup_cosine", "pf_verify_query_key", "pf_verify_row_keys"]
 
 PF_PROF_KINDS = 11
 PROF_NAMES = ["setup", "qkv", "qkv_post", "attn", "o_proj", "norm", "gate_up", "down",
@@ -109,6 +113,13 @@ def lib():
             "pf_kv_commit": (i32, [vp, vp, vp, vp]),
             "pf_prefill": (i32, [vp, vp, vp, i32, i32, vp, vp]),
             "pf_verify_step_profiled": (i32, [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]),
+            "pf_keyproj_create": (i32, [vp, i32, vp]),
+            "pf_keyproj_destroy": (None, [vp]),
+            "pf_key_encode": (i32, [vp, vp, i32, i64, i64, vp, vp]),
+            "pf_store_attach_keys": (i32, [vp, vp, vp]),
+            "pf_draft_lookup_cosine": (i32, [vp, vp, vp, i32, i32, i32, i32, vp, vp]),
+            "pf_verify_query_key": (i32, [vp, vp, vp, vp, vp]),
+            "pf_verify_row_keys": (i32, [vp, vp, i32, vp, vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -219,6 +230,60 @@ def pf_draft_lookup(store: Store, ctx: Context, k_max: int, tree: bool, n_cand: 
                     max_nodes: int, draft, stream=None) -> None:
     _check(lib().pf_draft_lookup(store.h, ctypes.byref(ctx.c), int(k_max), int(bool(tree)),
                                  int(n_cand), int(max_nodes), draft.data_ptr(), _stream(stream)))
+
+
+class KeyProj:
+    """Device copy of the fixed random projection of the retrieval keys."""
+
+    def __init__(self, handle: int, hidden: int):
+        self.h = handle
+        self.hidden = hidden
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.pf_keyproj_destroy(self.h)
+            self.h = None
+
+
+def pf_keyproj_create(R: np.ndarray) -> KeyProj:
+    R = np.ascontiguousarray(R, np.float32)
+    assert R.ndim == 2 and R.shape[0] == KEY_DIM
+    out = ctypes.c_void_p()
+    _check(lib().pf_keyproj_create(R.ctypes.data, int(R.shape[1]), ctypes.byref(out)))
+    return KeyProj(out.value, int(R.shape[1]))
+
+
+def pf_key_encode(kp: KeyProj, h, keys, stream=None) -> None:
+    """h: device tensor [n][ld] (float32 or bfloat16); keys: device int8 [n][KEY_DIM]."""
+    torch = _torch()
+    dt = {torch.float32: PF_DTYPE_F32, torch.bfloat16: PF_DTYPE_BF16}[h.dtype]
+    assert h.dim() == 2 and h.stride(1) == 1 and keys.dtype == torch.int8
+    assert keys.shape == (h.shape[0], KEY_DIM) and keys.is_contiguous()
+    _check(lib().pf_key_encode(kp.h, h.data_ptr(), dt, int(h.stride(0)), int(h.shape[0]),
+                               keys.data_ptr(), _stream(stream)))
+
+
+def pf_store_attach_keys(store: "Store", keys: np.ndarray, stream=None) -> None:
+    keys = np.ascontiguousarray(keys, np.int8)
+    assert keys.shape == (store.size, KEY_DIM)
+    _check(lib().pf_store_attach_keys(store.h, keys.ctypes.data, _stream(stream)))
+
+
+def pf_draft_lookup_cosine(store: "Store", ctx: Context, qkey, k_max: int, tree: bool, n_cand: int,
+                           max_nodes: int, draft, stream=None) -> None:
+    """qkey: device int8 [KEY_DIM] (the query state's key)."""
+    _check(lib().pf_draft_lookup_cosine(store.h, ctypes.byref(ctx.c), qkey.data_ptr(), int(k_max),
+                                        int(bool(tree)), int(n_cand), int(max_nodes),
+                                        draft.data_ptr(), _stream(stream)))
+
+
+def pf_verify_query_key(model: "Model", kp: KeyProj, result, qkey, stream=None) -> None:
+    _check(lib().pf_verify_query_key(model.h, kp.h, result.data_ptr(), qkey.data_ptr(),
+                                     _stream(stream)))
+
+
+def pf_verify_row_keys(model: "Model", kp: KeyProj, rows: int, keys, stream=None) -> None:
+    _check(lib().pf_verify_row_keys(model.h, kp.h, int(rows), keys.data_ptr(), _stream(stream)))
 
 
 class Model:

@@ -14,7 +14,7 @@ using namespace pf;
 
 thread_local LaunchTimer *pf::t_launch_timer = nullptr;
 
-static_assert(sizeof(pf_draft) == 1368, "pf_draft layout");
+static_assert(sizeof(pf_draft) == 1384, "pf_draft layout");
 static_assert(sizeof(pf_verify_result) == 808, "pf_verify_result layout");
 
 namespace {
@@ -220,6 +220,10 @@ pf_status pf_store_build(const int32_t *tokens, const int64_t *offs, int64_t n_s
   pf_store *S = new pf_store();
   S->T = T;
   S->E = E;
+  S->h_tokens.assign(tokens, tokens + T);
+  S->h_last.resize(T);
+  for (int64_t q = 0; q < n_seqs; ++q)
+    for (int64_t p = offs[q]; p < offs[q + 1]; ++p) S->h_last[p] = (int32_t)(offs[q + 1] - 1);
   S->nb_log2 = nb_log2;
   S->ngram = ngram;
   pf_status r = PF_OK;
@@ -245,16 +249,192 @@ pf_status pf_store_build(const int32_t *tokens, const int64_t *offs, int64_t n_s
   return ok();
 }
 
+static void store_free_keys(pf_store *S) {
+  void *ptrs[] = {S->keys, S->tok_off, S->cpos, S->crem, S->cnk, S->cpart, S->cpart_elig};
+  for (void *p : ptrs)
+    if (p) (void)hipFree(p);
+  S->keys = nullptr;
+  S->tok_off = S->cpos = S->crem = S->cnk = S->cpart_elig = nullptr;
+  S->cpart = nullptr;
+  S->Ec = 0;
+  S->n_tok = 0;
+}
+
 void pf_store_destroy(pf_store *S) {
   if (!S) return;
   if (S->tokens) (void)hipFree(S->tokens);
   if (S->ent_pos) (void)hipFree(S->ent_pos);
   if (S->ent_rem) (void)hipFree(S->ent_rem);
   if (S->bucket_off) (void)hipFree(S->bucket_off);
+  store_free_keys(S);
   delete S;
 }
 
 int64_t pf_store_size(const pf_store *S) { return S ? S->T : -1; }
+
+// ---------------------------------------------------------------------------
+// cosine retrieval
+// ---------------------------------------------------------------------------
+
+pf_status pf_keyproj_create(const float *R, int32_t hidden, pf_keyproj **out) {
+  if (!out) return fail(PF_EINVAL, "pf_keyproj_create: null out");
+  *out = nullptr;
+  if (!R) return fail(PF_EINVAL, "pf_keyproj_create: null projection");
+  if (hidden < 16 || hidden > kKeyMaxHidden)
+    return fail(PF_EINVAL, "pf_keyproj_create: hidden %d not in [16, %d]", hidden, kKeyMaxHidden);
+  pf_keyproj *kp = new pf_keyproj();
+  kp->H = hidden;
+  kp->Lc = (int32_t)roundup((hidden + 15) / 16, 4);
+  const int64_t nrc = (int64_t)PF_KEY_DIM * 16 * kp->Lc;
+  std::vector<float> rc((size_t)nrc, 0.f);
+  for (int j = 0; j < PF_KEY_DIM; ++j)
+    for (int c = 0; c < 16; ++c)
+      for (int t = 0; t < kp->Lc; ++t) {
+        const int k = c + 16 * t;
+        if (k < hidden) rc[((size_t)j * 16 + c) * kp->Lc + t] = R[(size_t)j * hidden + k];
+      }
+  pf_status r = PF_OK;
+  if ((r = dev_alloc(&kp->Rc, nrc * 4, nullptr)) ||
+      (r = dev_alloc(&kp->v, (int64_t)kKeyBatch * PF_KEY_DIM * 8, nullptr))) {
+    pf_keyproj_destroy(kp);
+    return r;
+  }
+  hipError_t e = hipMemcpy(kp->Rc, rc.data(), (size_t)nrc * 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    pf_keyproj_destroy(kp);
+    return fail(PF_EHIP, "pf_keyproj_create: copy failed: %s", hipGetErrorString(e));
+  }
+  *out = kp;
+  return ok();
+}
+
+void pf_keyproj_destroy(pf_keyproj *kp) {
+  if (!kp) return;
+  if (kp->Rc) (void)hipFree(kp->Rc);
+  if (kp->v) (void)hipFree(kp->v);
+  delete kp;
+}
+
+// keys of n rows in batches that fit the projection's work buffer
+static pf_status encode_rows(const pf_keyproj *kp, bool bf16, bool packed, const void *h,
+                             int64_t ld, int64_t n, int8_t *keys, hipStream_t hs) {
+  const size_t esz = bf16 ? 2 : 4;
+  for (int64_t b = 0; b < n; b += kKeyBatch) {
+    const int nb = (int)std::min<int64_t>(kKeyBatch, n - b);
+    if (packed) {
+      // rows b.. of the packed verify activations: batches start on 16-row
+      // tiles (kKeyBatch is a multiple of 16), so shift by whole tiles
+      const int kf = bf16 ? 32 : 16;
+      const char *hb = (const char *)h + (size_t)(b / 16) * (size_t)(ld / kf) * 1024;
+      HIPCHK(launch_key_project(bf16, true, kp->Rc, kp->H, kp->Lc, hb, ld, nb, nullptr, kp->v, hs));
+    } else {
+      HIPCHK(launch_key_project(bf16, false, kp->Rc, kp->H, kp->Lc,
+                                (const char *)h + (size_t)b * ld * esz, ld, nb, nullptr, kp->v, hs));
+    }
+    HIPCHK(launch_key_quant(kp->v, nb, keys + b * PF_KEY_DIM, hs));
+  }
+  return PF_OK;
+}
+
+pf_status pf_key_encode(const pf_keyproj *kp, const void *h, int32_t dtype, int64_t ld, int64_t n,
+                        int8_t *keys, pf_stream s) {
+  if (!kp || (n > 0 && (!h || !keys))) return fail(PF_EINVAL, "pf_key_encode: null pointer");
+  if (dtype != PF_DTYPE_F32 && dtype != PF_DTYPE_BF16)
+    return fail(PF_EINVAL, "pf_key_encode: dtype %d", dtype);
+  if (n < 0 || n > (1 << 20)) return fail(PF_EINVAL, "pf_key_encode: n %lld out of range", (long long)n);
+  if (ld < kp->H) return fail(PF_EINVAL, "pf_key_encode: ld %lld < hidden %d", (long long)ld, kp->H);
+  if (pf_status r = encode_rows(kp, dtype == PF_DTYPE_BF16, false, h, ld, n, keys, st(s))) return r;
+  return ok();
+}
+
+pf_status pf_store_attach_keys(pf_store *S, const int8_t *keys, pf_stream s) {
+  if (!S) return fail(PF_EINVAL, "pf_store_attach_keys: null store");
+  if (S->T > 0 && !keys) return fail(PF_EINVAL, "pf_store_attach_keys: null keys");
+  const int64_t T = S->T;
+  // entries p < b(p), grouped by token, ascending p within a token
+  int32_t n_tok = 1;
+  for (int64_t p = 0; p < T; ++p) n_tok = std::max(n_tok, S->h_tokens[p] + 1);
+  std::vector<int32_t> off((size_t)n_tok + 1, 0);
+  for (int64_t p = 0; p < T; ++p)
+    if (p < S->h_last[p] && S->h_tokens[p] >= 0) off[(size_t)S->h_tokens[p] + 1]++;
+  for (int32_t t = 0; t < n_tok; ++t) off[(size_t)t + 1] += off[t];
+  const int64_t Ec = off[n_tok];
+  std::vector<int32_t> fill(off.begin(), off.end() - 1), cpos(Ec), crem(Ec), cnk(Ec);
+  for (int64_t p = 0; p < T; ++p) {
+    if (!(p < S->h_last[p] && S->h_tokens[p] >= 0)) continue;
+    const int32_t at = fill[S->h_tokens[p]]++;
+    cpos[at] = (int32_t)p;
+    crem[at] = S->h_last[p] - (int32_t)p;
+    int32_t nk = 0;
+    for (int j = 0; j < PF_KEY_DIM; ++j) nk += (int32_t)keys[p * PF_KEY_DIM + j] * keys[p * PF_KEY_DIM + j];
+    cnk[at] = nk;
+  }
+  store_free_keys(S);
+  pf_status r = PF_OK;
+  if ((r = dev_alloc(&S->keys, T * PF_KEY_DIM, nullptr)) ||
+      (r = dev_alloc(&S->tok_off, ((int64_t)n_tok + 1) * 4, nullptr)) ||
+      (r = dev_alloc(&S->cpos, std::max<int64_t>(Ec, 1) * 4, nullptr)) ||
+      (r = dev_alloc(&S->crem, std::max<int64_t>(Ec, 1) * 4, nullptr)) ||
+      (r = dev_alloc(&S->cnk, std::max<int64_t>(Ec, 1) * 4, nullptr)) ||
+      (r = dev_alloc(&S->cpart, (int64_t)kCosScanBlocks * PF_MAX_CAND * 16, nullptr)) ||
+      (r = dev_alloc(&S->cpart_elig, (int64_t)kCosScanBlocks * 4, nullptr))) {
+    store_free_keys(S);
+    return r;
+  }
+  hipStream_t hs = st(s);
+  hipError_t e = hipSuccess;
+  if (T) e = hipMemcpyAsync(S->keys, keys, T * PF_KEY_DIM, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(S->tok_off, off.data(), ((size_t)n_tok + 1) * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && Ec) e = hipMemcpyAsync(S->cpos, cpos.data(), Ec * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && Ec) e = hipMemcpyAsync(S->crem, crem.data(), Ec * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess && Ec) e = hipMemcpyAsync(S->cnk, cnk.data(), Ec * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);  // host vectors die here
+  if (e != hipSuccess) {
+    store_free_keys(S);
+    return fail(PF_EHIP, "pf_store_attach_keys: copy failed: %s", hipGetErrorString(e));
+  }
+  S->Ec = Ec;
+  S->n_tok = n_tok;
+  return ok();
+}
+
+pf_status pf_draft_lookup_cosine(const pf_store *S, const pf_context *ctx, const int8_t *q,
+                                 int32_t k_max, int32_t tree, int32_t n_cand, int32_t max_nodes,
+                                 pf_draft *draft, pf_stream s) {
+  if (!S || !ctx || !ctx->tokens || !ctx->len || !draft || !q)
+    return fail(PF_EINVAL, "pf_draft_lookup_cosine: null pointer");
+  if (!S->tok_off) return fail(PF_ESTATE, "pf_draft_lookup_cosine: store has no keys");
+  if (k_max < 0 || k_max > PF_MAX_DRAFT)
+    return fail(PF_EINVAL, "pf_draft_lookup_cosine: k_max %d not in [0,%d]", k_max, PF_MAX_DRAFT);
+  if (tree != 0 && tree != 1) return fail(PF_EINVAL, "pf_draft_lookup_cosine: tree must be 0 or 1");
+  if (n_cand < 1 || n_cand > PF_MAX_CAND || (!tree && n_cand != 1))
+    return fail(PF_EINVAL, "pf_draft_lookup_cosine: n_cand %d invalid", n_cand);
+  if (tree && (max_nodes < 1 || max_nodes > PF_MAX_TREE_NODES))
+    return fail(PF_EINVAL, "pf_draft_lookup_cosine: max_nodes %d not in [1,%d]", max_nodes,
+                PF_MAX_TREE_NODES);
+  if (ctx->host_bound < 1) return fail(PF_ESTATE, "pf_draft_lookup_cosine: empty context");
+  CosArgs a;
+  a.tokens = S->tokens;
+  a.keys = S->keys;
+  a.tok_off = S->tok_off;
+  a.ent_pos = S->cpos;
+  a.ent_rem = S->crem;
+  a.ent_nk = S->cnk;
+  a.n_tok = S->n_tok;
+  a.ctx = ctx->tokens;
+  a.ctx_len = ctx->len;
+  a.q = q;
+  a.k_max = k_max;
+  a.tree = tree;
+  a.n_cand = n_cand;
+  a.max_nodes = tree ? max_nodes : PF_MAX_DRAFT;
+  a.part = S->cpart;
+  a.part_elig = S->cpart_elig;
+  a.draft = draft;
+  HIPCHK(launch_cos_lookup(a, st(s)));
+  return ok();
+}
 
 pf_status pf_draft_lookup(const pf_store *S, const pf_context *ctx, int32_t k_max, int32_t tree,
                           int32_t n_cand, int32_t max_nodes, pf_draft *draft, pf_stream s) {
@@ -732,6 +912,33 @@ pf_status pf_verify_step_profiled(pf_model *m, pf_kv_cache *kv, const pf_draft *
     ms_out[k] += k == PF_PROF_MARKER ? ms[i] : std::max(0.0, ms[i] - per_pair);
     count_out[k] += 1;
   }
+  return ok();
+}
+
+pf_status pf_verify_query_key(const pf_model *m, const pf_keyproj *kp, const pf_verify_result *res,
+                              int8_t *q, pf_stream s) {
+  if (!m || !kp || !res || !q) return fail(PF_EINVAL, "pf_verify_query_key: null pointer");
+  if (kp->H != m->cfg.hidden)
+    return fail(PF_EINVAL, "pf_verify_query_key: projection hidden %d != model hidden %d", kp->H,
+                m->cfg.hidden);
+  const bool bf = is_bf16(m);
+  const int64_t Hp = roundup(m->cfg.hidden, frag_k_of(m));
+  hipStream_t hs = st(s);
+  HIPCHK(launch_key_project(bf, true, kp->Rc, kp->H, kp->Lc, m->xn, Hp, 1, res, kp->v, hs));
+  HIPCHK(launch_key_quant(kp->v, 1, q, hs));
+  return ok();
+}
+
+pf_status pf_verify_row_keys(const pf_model *m, const pf_keyproj *kp, int32_t rows, int8_t *keys,
+                             pf_stream s) {
+  if (!m || !kp || !keys) return fail(PF_EINVAL, "pf_verify_row_keys: null pointer");
+  if (kp->H != m->cfg.hidden)
+    return fail(PF_EINVAL, "pf_verify_row_keys: projection hidden %d != model hidden %d", kp->H,
+                m->cfg.hidden);
+  if (rows < 1 || rows > kMaxRows)
+    return fail(PF_EINVAL, "pf_verify_row_keys: rows %d out of range", rows);
+  const int64_t Hp = roundup(m->cfg.hidden, frag_k_of(m));
+  if (pf_status r = encode_rows(kp, is_bf16(m), true, m->xn, Hp, rows, keys, st(s))) return r;
   return ok();
 }
 

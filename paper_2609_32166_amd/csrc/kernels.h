@@ -187,6 +187,112 @@ struct LookupArgs {
 };
 hipError_t launch_lookup(const LookupArgs &a, hipStream_t s);
 
+// Draft nodes from ranked candidates, built by a whole block of 256 threads
+// (every thread calls it with the same arguments): the candidates' proposal
+// tokens are staged in LDS in parallel, one thread builds the nodes there
+// (node 0 is the current token; linear: the best candidate's proposal as a
+// chain; tree: the candidates merged in rank order into a prefix-shared trie,
+// children in creation order, creation stopping for good once max_nodes
+// non-root nodes exist), and the block writes every node slot of d (unused
+// slots zero, parent -1). Returns the node count.
+__device__ inline int build_draft_block(pf_draft *d, const int32_t *tokens, int32_t cur_token,
+                                        const int *cand_pos, const int *cand_len, int found,
+                                        int tree, int max_nodes) {
+  __shared__ int32_t ct[PF_MAX_CAND][PF_MAX_DRAFT];
+  __shared__ int32_t ntok[PF_MAX_NODES], npar[PF_MAX_NODES], ndep[PF_MAX_NODES];
+  __shared__ uint64_t nanc[PF_MAX_NODES];
+  __shared__ int s_nn;
+  const int tid = threadIdx.x;
+  for (int t = tid; t < PF_MAX_CAND * PF_MAX_DRAFT; t += blockDim.x) {
+    const int c = t / PF_MAX_DRAFT, i = t % PF_MAX_DRAFT;
+    ct[c][i] = (c < found && i < cand_len[c]) ? tokens[cand_pos[c] + 1 + i] : 0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int nn = 1;
+    ntok[0] = cur_token;
+    npar[0] = -1;
+    ndep[0] = 0;
+    nanc[0] = 1ull;
+    if (!tree) {
+      if (found > 0) {
+        for (int i = 0; i < cand_len[0]; ++i) {
+          ntok[nn] = ct[0][i];
+          npar[nn] = nn - 1;
+          ndep[nn] = nn;
+          nanc[nn] = nn < 64 ? (nanc[nn - 1] | (1ull << nn)) : 0ull;
+          ++nn;
+        }
+      }
+    } else {
+      bool full = false;
+      for (int c = 0; c < found && !full; ++c) {
+        int cur = 0;
+        for (int i = 0; i < cand_len[c]; ++i) {
+          const int t = ct[c][i];
+          int child = -1;
+          for (int u = 1; u < nn; ++u)
+            if (npar[u] == cur && ntok[u] == t) {
+              child = u;
+              break;
+            }
+          if (child < 0) {
+            if (nn - 1 >= max_nodes) {
+              full = true;
+              break;
+            }
+            child = nn++;
+            ntok[child] = t;
+            npar[child] = cur;
+            ndep[child] = ndep[cur] + 1;
+            nanc[child] = nanc[cur] | (1ull << child);
+          }
+          cur = child;
+        }
+      }
+    }
+    s_nn = nn;
+  }
+  __syncthreads();
+  const int nn = s_nn;
+  for (int j = tid; j < PF_MAX_NODES; j += blockDim.x) {
+    const bool u = j < nn;
+    d->token[j] = u ? ntok[j] : 0;
+    d->parent[j] = u ? npar[j] : -1;
+    d->depth[j] = u ? ndep[j] : 0;
+    d->anc[j] = u ? nanc[j] : 0ull;
+  }
+  return nn;
+}
+
+// cosine retrieval (keys.hip)
+constexpr int kKeyDim = PF_KEY_DIM;
+constexpr int kKeyRowsPerBlock = 2;   // rows per projection block
+constexpr int kKeyMaxHidden = 8192;   // padded hidden sizes the projection stages in LDS
+constexpr int kKeyBatch = 64;         // rows per projection launch (work buffer)
+constexpr int kCosScanBlocks = 256;   // blocks of the cosine scan
+struct CosArgs {
+  const int32_t *tokens;
+  const int8_t *keys;                  // [T][kKeyDim]
+  const int32_t *tok_off;              // [n_tok + 1]
+  const int32_t *ent_pos, *ent_rem, *ent_nk;
+  int n_tok;
+  const int32_t *ctx, *ctx_len;
+  const int8_t *q;                     // [kKeyDim]
+  int k_max, tree, n_cand, max_nodes;
+  int4 *part;                          // [kCosScanBlocks][PF_MAX_CAND] (dot, nk, len, pos)
+  int32_t *part_elig;                  // [kCosScanBlocks]
+  pf_draft *draft;
+};
+hipError_t launch_cos_lookup(const CosArgs &a, hipStream_t s);
+// v[r][j] (fp64) of rows of h: plain [n][ld] rows, or rows of the packed
+// verify activations (ld = padded hidden); with sel, the single row
+// sel->path[sel->accept_len]. Rc: the projection chain-major (pf_keyproj).
+hipError_t launch_key_project(bool bf16, bool packed, const float *Rc, int H, int Lc,
+                              const void *h, int64_t ld, int n, const pf_verify_result *sel,
+                              double *v, hipStream_t s);
+hipError_t launch_key_quant(const double *v, int n, int8_t *keys, hipStream_t s);
+
 hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers, int64_t src_layer_stride,
                        bool bf16, const Packed &geom, void *dst, hipStream_t s);
 

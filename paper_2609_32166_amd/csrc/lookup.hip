@@ -31,12 +31,6 @@ __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
   const bool have = len >= n && n >= 1 && a.k_max >= 0;
   if (tid < n && have) q[tid] = a.ctx[len - n + tid];
   pf_draft *d = a.draft;
-  for (int j = tid; j < PF_MAX_NODES; j += 256) {
-    d->token[j] = 0;
-    d->parent[j] = -1;
-    d->depth[j] = 0;
-    d->anc[j] = 0;
-  }
   __syncthreads();
 
   int b0 = 0, b1 = 0;
@@ -89,59 +83,22 @@ __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
   }
   __syncthreads();
 
+  int cpos[PF_MAX_CAND], clen[PF_MAX_CAND];
+  for (int c = 0; c < PF_MAX_CAND; ++c) {
+    const bool ok = c < found;
+    clen[c] = ok ? (int)(cand[c] >> 40) - 1 : 0;
+    cpos[c] = ok ? (int)(cand[c] & ((1ull << 40) - 1)) : -1;
+  }
+  const int nn = build_draft_block(d, a.tokens, len >= 1 ? a.ctx[len - 1] : 0, cpos, clen, found,
+                                   a.tree, a.max_nodes);
   if (tid != 0) return;
   d->n_found = found;
   d->n_eligible = nelig;
   d->tree = a.tree;
   for (int c = 0; c < PF_MAX_CAND; ++c) {
-    d->cand_len[c] = c < found ? (int)(cand[c] >> 40) - 1 : 0;
-    d->cand_pos[c] = c < found ? (int64_t)(cand[c] & ((1ull << 40) - 1)) : -1;
-  }
-  int nn = 1;
-  d->token[0] = len >= 1 ? a.ctx[len - 1] : 0;
-  d->parent[0] = -1;
-  d->depth[0] = 0;
-  d->anc[0] = 1ull;
-  if (!a.tree) {
-    if (found > 0) {
-      const int L = (int)(cand[0] >> 40) - 1;
-      const int p = (int)(cand[0] & ((1ull << 40) - 1));
-      for (int i = 0; i < L; ++i) {
-        d->token[nn] = a.tokens[p + 1 + i];
-        d->parent[nn] = nn - 1;
-        d->depth[nn] = nn;
-        d->anc[nn] = nn < 64 ? (d->anc[nn - 1] | (1ull << nn)) : 0ull;
-        ++nn;
-      }
-    }
-  } else {
-    bool full = false;
-    for (int c = 0; c < found && !full; ++c) {
-      const int L = (int)(cand[c] >> 40) - 1;
-      const int p = (int)(cand[c] & ((1ull << 40) - 1));
-      int cur = 0;
-      for (int i = 0; i < L; ++i) {
-        const int t = a.tokens[p + 1 + i];
-        int child = -1;
-        for (int u = 1; u < nn; ++u)
-          if (d->parent[u] == cur && d->token[u] == t) {
-            child = u;
-            break;
-          }
-        if (child < 0) {
-          if (nn - 1 >= a.max_nodes) {
-            full = true;
-            break;
-          }
-          child = nn++;
-          d->token[child] = t;
-          d->parent[child] = cur;
-          d->depth[child] = d->depth[cur] + 1;
-          d->anc[child] = d->anc[cur] | (1ull << child);
-        }
-        cur = child;
-      }
-    }
+    d->cand_len[c] = clen[c];
+    d->cand_pos[c] = c < found ? (int64_t)cpos[c] : -1;
+    d->cand_score[c] = 0.f;
   }
   d->n_nodes = nn;
 }

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "pf.h"
 
 namespace pf {
@@ -177,6 +179,25 @@ struct pf_store {
   int64_t T = 0, E = 0;
   int32_t nb_log2 = 0;
   int32_t ngram = 0;
+  // cosine index (pf_store_attach_keys): entries p < b(p) grouped by token
+  int8_t *keys = nullptr;        // [T][PF_KEY_DIM]
+  int32_t *tok_off = nullptr;    // [n_tok + 1]
+  int32_t *cpos = nullptr;       // [Ec] positions, ascending within a token
+  int32_t *crem = nullptr;       // [Ec] b(p) - p
+  int32_t *cnk = nullptr;        // [Ec] squared norm of the key
+  int4 *cpart = nullptr;         // lookup scratch: per-block best candidates
+  int32_t *cpart_elig = nullptr; // lookup scratch: per-block eligible counts
+  int64_t Ec = 0;
+  int32_t n_tok = 0;
+  // host copies kept for attaching keys: tokens and each position's
+  // sequence-last position b(p)
+  std::vector<int32_t> h_tokens, h_last;
+};
+
+struct pf_keyproj {
+  float *Rc = nullptr;   // [PF_KEY_DIM][16][Lc]: R[j][c + 16 t] at [j][c][t], zeros past H
+  double *v = nullptr;   // work: projections of one batch of rows
+  int32_t H = 0, Lc = 0;
 };
 
 namespace pf {

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_record_layouts_match_header():
-    assert pf.DRAFT_DTYPE.itemsize == 1368
+    assert pf.DRAFT_DTYPE.itemsize == 1384
     assert pf.RESULT_DTYPE.itemsize == 808
     assert ctypes.sizeof(pf.pf_kv_cache) == 56
     assert ctypes.sizeof(pf.pf_context) == 32
