@@ -270,6 +270,88 @@ def cosine_timings(torch, pf, wl, store, model, res, st, ctx):
     return out
 
 
+def decode_loop(torch, pf, wl, model, kv_host, store, ctx, gen=256, mutate=0.05):
+    """Closed-loop decoding (Section 3.2, steps 2-7) through
+    pf_decode_iteration: the paper's cosine retrieval, the proposal length
+    (fixed, or Eq. (1) through the controller), verify, commit, next query.
+
+    Workload: a repeated task. A first greedy run of `gen` tokens records the
+    outputs and the keys of the states that produced them; the store then
+    holds that run as a prior execution with a fraction `mutate` of its
+    tokens replaced (the run drifted), next to the seeded base store with
+    seeded keys. Every mode then decodes the same `gen` tokens from the same
+    start; tokens/s counts every emitted token over the wall time of the
+    iterations (both host synchronisations of each iteration included)."""
+    shape, P = wl.model, wl.prefix
+    cap = ((P + gen + 65 + 63) // 64) * 64
+    kv = pf.KVCache(model, cap)
+    kvd = pf.array_to_device(kv_host)
+    R = synth.key_projection(shape.hidden, synth.case_seed(wl, 12))
+    kp = pf.pf_keyproj_create(R)
+    q = torch.zeros(pf.KEY_DIM, dtype=torch.int8, device="cuda")
+    draft, res = pf.new_draft(), pf.new_result()
+    T = int(store.tokens.shape[0])
+    base_keys = np.empty((T, pf.KEY_DIM), np.int8)
+    for a in range(0, T, 1 << 18):
+        b = min(T, a + (1 << 18))
+        base_keys[a:b] = synth.random_keys(b - a, synth.case_seed(wl, 11), first=a)
+    st0 = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
+    pf.pf_store_attach_keys(st0, base_keys)
+
+    def run(st, ctl, l_fixed, record=False):
+        pf.pf_kv_import(kv, kvd, P)
+        c = pf.Context(ctx, len(ctx) + gen + 70)
+        q.zero_()
+        torch.cuda.synchronize()
+        its, keys, produced, wall = [], [], 0, 0.0
+        while produced < gen:
+            it = pf.pf_decode_iteration(model, kv, c, st, kp, ctl, l_fixed, q, draft, res)
+            wall += it["ms"]
+            if record:
+                keys.append(q.cpu().numpy())
+            its.append(it)
+            produced += it["accepted"] + 1
+        return c.tokens()[len(ctx):len(ctx) + gen], its, keys, wall
+
+    run(st0, None, 0)                      # warm-up (first-call allocations)
+    first, _, keys, wall0 = run(st0, None, 0, record=True)
+    tokens, offs, skeys = synth.replay_store(store, base_keys, int(ctx[-1]), first,
+                                             np.stack(keys), mutate, synth.case_seed(wl, 13),
+                                             shape.vocab)
+    del base_keys
+    st = pf.pf_store_build(tokens, offs, wl.ngram)
+    pf.pf_store_attach_keys(st, skeys)
+    del skeys
+    out = {"tokens": gen, "mutated_fraction": mutate, "l_max": 64,
+           "first_run_greedy_ms_per_token": round(wall0 / gen, 4), "modes": {}}
+    modes = [("greedy", None, 0)] + [(f"fixed_{l}", None, l) for l in (4, 8, 16, 32, 64)]
+    ctl = pf.pf_ctl_create(l_max=64, explore_every=16, lr=0.05, forget=0.98, prior_var=100.0)
+    modes += [("controller_cold", ctl, 0), ("controller_warm", ctl, 0)]
+    for name, cl, lf in modes:
+        toks, its, _, wall = run(st, cl, lf)
+        same = int(np.argmax(toks != first)) if (toks != first).any() else gen
+        ls = [it["l"] for it in its]
+        acc = [it["accepted"] for it in its]
+        out["modes"][name] = {
+            "tokens_per_s": round(sum(a + 1 for a in acc) / (wall * 1e-3), 1),
+            "iterations": len(its), "mean_l": round(float(np.mean(ls)), 2),
+            "mean_accepted": round(float(np.mean(acc)), 2),
+            "ms_per_iteration": round(wall / len(its), 4),
+            "identical_to_greedy_tokens": same}
+        log(f"decode loop {name}: {out['modes'][name]}")
+    g = out["modes"]["greedy"]["tokens_per_s"]
+    for v in out["modes"].values():
+        v["speedup_vs_greedy"] = round(v["tokens_per_s"] / g, 3)
+    st_ = pf.pf_ctl_get_state(ctl)
+    out["controller_state"] = {"w_first": [round(x, 4) for x in st_.w_first],
+                               "w_cont": [round(x, 4) for x in st_.w_cont],
+                               "theta": [round(x, 4) for x in st_.theta],
+                               "T_ms_predicted": {str(l): round(float(np.exp(
+                                   st_.theta[0] + st_.theta[1] * l / 64
+                                   + st_.theta[2] * (l / 64) ** 2)), 3) for l in (0, 16, 64)}}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -282,6 +364,7 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the phase split, percentiles, greedy and K-sweep timings")
+    ap.add_argument("--no-loop", action="store_true", help="skip the closed-loop decode timings")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="also run a plain device copy of this many MiB (for counter scaling)")
     args = ap.parse_args()
@@ -471,6 +554,8 @@ def main():
         out["cosine_retrieval"] = cosine_timings(torch, pf, wl, store, model, res, st, ctx)
     if prefill is not None:
         out["prefill"] = prefill
+    if not args.no_loop and not wl.tree:
+        out["decode_loop"] = decode_loop(torch, pf, wl, model, kv_host, store, ctx)
     if not args.no_cpu_baseline:
         od = {"n_nodes": int(d["n_nodes"]), "token": np.array(d["token"][:int(d["n_nodes"])]),
               "parent": np.array(d["parent"][:int(d["n_nodes"])]),

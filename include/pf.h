@@ -378,6 +378,104 @@ pf_status pf_kv_commit(pf_kv_cache *kv, const pf_verify_result *res_dev, pf_cont
 pf_status pf_prefill(pf_model *model, pf_kv_cache *kv, const int32_t *tokens_dev, int32_t n,
                      int32_t chunk, float *logits_last_dev, pf_stream s);
 
+/* ------------------------------------------------------------------------ */
+/* Proposal-length controller (Section 3.2, "Runtime-adaptive proposal-     */
+/* length controller", Eq. (1))                                             */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Host-side, fp64. For an eligible retrieval of similarity s (the draft's
+ * cand_score[0] for the cosine lookup) whose proposal holds `avail` tokens,
+ * the length l in 0..L, L = min(l_max, avail), that minimises
+ *     J(l) = T(l) / (A(l, s) + 1)
+ * (ties: the shorter). l = 0 is a greedy pass; verify with rows = l + 1 (the
+ * verify step ignores draft nodes at or beyond `rows`).
+ *   A(l, s) = sum_{j=1..l} prod_{i=1..j} q_i, the expected accepted proposal
+ *     tokens; q_1 = sigmoid(w_first . (1, s, 1/l_max)) is the first token's
+ *     acceptance probability and q_j = sigmoid(w_cont . (1, s, j/l_max)) the
+ *     probability that token j >= 2 passes given that token j-1 did.
+ *   T(l) = exp(theta . (1, u, u^2)), u = l/l_max: the predicted iteration
+ *     latency in ms.
+ * pf_ctl_observe learns from one finished iteration that proposed l tokens
+ * at similarity s, accepted `accepted` of them and took latency_ms: one
+ * logistic-regression gradient step (w += lr * (y - q) * x) for the first
+ * token when l >= 1 and for each token j = 2..min(l, accepted+1) (y: token j
+ * accepted), then one recursive-least-squares step of log(latency_ms) on
+ * (1, u, u^2) with forgetting factor `forget` (from theta = 0, covariance
+ * prior_var * I). Every explore_every-th pf_ctl_choose (0: never) returns a
+ * neighbour of the best length instead, alternately the one above and the
+ * one below (the other one where that leaves 0..L; none when L = 0).
+ * Errors: PF_EINVAL for a null pointer, a parameter out of its range, a
+ * non-finite similarity or latency, or an observation with accepted outside
+ * 0..l or l outside 0..l_max. A controller is not thread-safe.
+ */
+typedef struct pf_ctl_params {
+  int32_t l_max;         /* 1..64 */
+  int32_t explore_every; /* >= 0 */
+  double lr;             /* > 0 */
+  double forget;         /* (0, 1] */
+  double prior_var;      /* > 0 */
+} pf_ctl_params;
+
+typedef struct pf_ctl_state {
+  double w_first[3];
+  double w_cont[3];
+  double theta[3];
+  double P[9]; /* latency-fit covariance, row-major */
+  int64_t n_choose, n_explore, n_observe;
+} pf_ctl_state;
+
+typedef struct pf_ctl pf_ctl;
+
+pf_status pf_ctl_create(const pf_ctl_params *params, pf_ctl **out);
+void pf_ctl_destroy(pf_ctl *ctl);
+pf_status pf_ctl_get_state(const pf_ctl *ctl, pf_ctl_state *out);
+/* Replace the estimator states and counters (all values finite, counters >= 0). */
+pf_status pf_ctl_set_state(pf_ctl *ctl, const pf_ctl_state *in);
+/* J(0..L) into objective_out (NULL, or host double[L + 1]) and the argmin
+ * into best_out (nullable); changes nothing. */
+pf_status pf_ctl_objective(const pf_ctl *ctl, double s, int32_t avail, double *objective_out,
+                           int32_t *best_out);
+pf_status pf_ctl_choose(pf_ctl *ctl, double s, int32_t avail, int32_t *l_out);
+pf_status pf_ctl_observe(pf_ctl *ctl, int32_t l, double s, int32_t accepted, double latency_ms);
+
+/* ------------------------------------------------------------------------ */
+/* One decoding iteration, host-driven (Section 3.2, steps 2-7)             */
+/* ------------------------------------------------------------------------ */
+
+typedef struct pf_iteration {
+  int32_t n_found;  /* eligible entries the retrieval ranked (0: greedy pass) */
+  int32_t avail;    /* tokens of the retrieved proposal (cut at its boundary and the cap) */
+  int32_t l;        /* proposal length verified (rows = l + 1) */
+  int32_t accepted; /* l_acc */
+  int32_t bonus;    /* the model's token after the accepted prefix: the new current token */
+  int32_t status;   /* pf_verify_result.status */
+  double s;         /* cosine similarity of the retrieved entry (0 when none) */
+  double ms;        /* host wall time of the whole call */
+} pf_iteration;
+
+/*
+ * Cosine retrieval for the current token with query key q_dev (linear
+ * proposal, cap ctl's l_max, or l_fixed without a controller) -> the length
+ * l: Eq. (1) through pf_ctl_choose, or min(l_fixed, retrieved length), or 0
+ * when nothing is eligible -> pf_verify_step over l + 1 rows ->
+ * pf_kv_commit (appends the accepted tokens and the bonus to ctx) ->
+ * pf_verify_query_key into q_dev (the next iteration's query) -> with a
+ * controller, pf_ctl_observe(l, s, accepted, ms) (also for greedy passes,
+ * which teach the latency fit T(0)). ctl: nullable. store must have keys
+ * attached; the projection's hidden size must be the model's. draft_dev,
+ * res_dev: device buffers the iteration writes. The call synchronises s
+ * twice (after the retrieval and at the end) and tightens kv and ctx
+ * host bounds to the exact lengths; on the model's first call it allocates
+ * a small pinned host buffer, so it is not for graph capture. Errors: those
+ * of the calls it makes, PF_EINVAL for null pointers or l_fixed outside
+ * 0..64.
+ */
+pf_status pf_decode_iteration(pf_model *model, pf_kv_cache *kv, pf_context *ctx,
+                              const pf_store *store, const pf_keyproj *kp, pf_ctl *ctl,
+                              int32_t l_fixed, int8_t *q_dev, pf_draft *draft_dev,
+                              pf_verify_result *res_dev, pf_iteration *out, pf_stream s);
+
 #ifdef __cplusplus
 }
 #endif

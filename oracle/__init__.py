@@ -416,19 +416,30 @@ def verify_sequential(model: Model, kv_prefix: np.ndarray, draft: dict, tree: bo
             "logits": np.stack(step_logits)}
 
 
-def greedy_decode(model: Model, kv_prefix: np.ndarray, first_token: int, steps: int) -> dict:
-    """`steps` plain greedy decodes starting from `first_token` at position P."""
+def greedy_decode(model: Model, kv_prefix: np.ndarray, first_token: int, steps: int,
+                  want_hidden: bool = False) -> dict:
+    """`steps` plain greedy decodes starting from `first_token` at position P.
+    Also returns each step's top-2 logit gap relative to the largest |logit|
+    ("margin") and, with want_hidden, the final-layer state that produced
+    each output token ("hidden", [steps][H])."""
     P = kv_prefix.shape[3]
     extra = None
     tok = int(first_token)
-    out = []
+    out, margin = [], []
+    hid = np.zeros((steps, model.shape.hidden), np.float64) if want_hidden else None
     one = np.ones((1, 1), np.uint8)
     for d in range(steps):
-        lg, kv1 = model.forward(kv_prefix, [tok], [P + d], one, kv_extra=extra)
+        h = np.zeros((1, model.shape.hidden), np.float64) if want_hidden else None
+        lg, kv1 = model.forward(kv_prefix, [tok], [P + d], one, kv_extra=extra, hidden=h)
         tok = argmax(lg[0])
         out.append(tok)
+        top2 = np.sort(lg[0].astype(np.float64))[-2:]
+        margin.append((top2[1] - top2[0]) / max(np.abs(lg[0]).max(), 1e-30))
+        if want_hidden:
+            hid[d] = h[0]
         extra = kv1 if extra is None else np.concatenate([extra, kv1], axis=3)
-    return {"tokens": np.array(out, np.int32), "kv": extra}
+    return {"tokens": np.array(out, np.int32), "kv": extra, "margin": np.array(margin),
+            "hidden": hid}
 
 
 def commit(kv_new: np.ndarray, path: Sequence[int]) -> np.ndarray:

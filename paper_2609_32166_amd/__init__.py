@@ -40,7 +40,9 @@ EXPORTED = ["pf_last_error", "pf_version", "pf_context_init", "pf_context_sync_b
             "pf_kv_import", "pf_kv_export", "pf_kv_set_len", "pf_kv_sync_bound", "pf_verify_step",
             "pf_kv_commit", "pf_prefill", "pf_verify_step_profiled", "pf_keyproj_create",
             "pf_keyproj_destroy", "pf_key_encode", "pf_store_attach_keys",
-            "pf_draft_lookup_cosine", "pf_verify_query_key", "pf_verify_row_keys"]
+            "pf_draft_lookup_cosine", "pf_verify_query_key", "pf_verify_row_keys",
+            "pf_ctl_create", "pf_ctl_destroy", "pf_ctl_get_state", "pf_ctl_set_state",
+            "pf_ctl_objective", "pf_ctl_choose", "pf_ctl_observe", "pf_decode_iteration"]
 
 PF_PROF_KINDS = 11
 PROF_NAMES = ["setup", "qkv", "qkv_post", "attn", "o_proj", "norm", "gate_up", "down",
@@ -120,6 +122,14 @@ def lib():
             "pf_draft_lookup_cosine": (i32, [vp, vp, vp, i32, i32, i32, i32, vp, vp]),
             "pf_verify_query_key": (i32, [vp, vp, vp, vp, vp]),
             "pf_verify_row_keys": (i32, [vp, vp, i32, vp, vp]),
+            "pf_ctl_create": (i32, [vp, vp]),
+            "pf_ctl_destroy": (None, [vp]),
+            "pf_ctl_get_state": (i32, [vp, vp]),
+            "pf_ctl_set_state": (i32, [vp, vp]),
+            "pf_ctl_objective": (i32, [vp, ctypes.c_double, i32, vp, vp]),
+            "pf_ctl_choose": (i32, [vp, ctypes.c_double, i32, vp]),
+            "pf_ctl_observe": (i32, [vp, i32, ctypes.c_double, i32, ctypes.c_double]),
+            "pf_decode_iteration": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -230,6 +240,86 @@ def pf_draft_lookup(store: Store, ctx: Context, k_max: int, tree: bool, n_cand: 
                     max_nodes: int, draft, stream=None) -> None:
     _check(lib().pf_draft_lookup(store.h, ctypes.byref(ctx.c), int(k_max), int(bool(tree)),
                                  int(n_cand), int(max_nodes), draft.data_ptr(), _stream(stream)))
+
+
+class pf_ctl_params(ctypes.Structure):
+    _fields_ = [("l_max", ctypes.c_int32), ("explore_every", ctypes.c_int32),
+                ("lr", ctypes.c_double), ("forget", ctypes.c_double),
+                ("prior_var", ctypes.c_double)]
+
+
+class pf_ctl_state(ctypes.Structure):
+    _fields_ = [("w_first", ctypes.c_double * 3), ("w_cont", ctypes.c_double * 3),
+                ("theta", ctypes.c_double * 3), ("P", ctypes.c_double * 9),
+                ("n_choose", ctypes.c_int64), ("n_explore", ctypes.c_int64),
+                ("n_observe", ctypes.c_int64)]
+
+
+class Controller:
+    """Handle of a proposal-length controller (host state in the library)."""
+
+    def __init__(self, handle: int, l_max: int):
+        self.h = handle
+        self.l_max = l_max
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.pf_ctl_destroy(self.h)
+            self.h = None
+
+
+def pf_ctl_create(l_max: int = 64, explore_every: int = 16, lr: float = 0.05,
+                  forget: float = 0.98, prior_var: float = 100.0) -> Controller:
+    p = pf_ctl_params(int(l_max), int(explore_every), float(lr), float(forget), float(prior_var))
+    out = ctypes.c_void_p()
+    _check(lib().pf_ctl_create(ctypes.byref(p), ctypes.byref(out)))
+    return Controller(out.value, int(l_max))
+
+
+def pf_ctl_get_state(ctl: Controller) -> pf_ctl_state:
+    st = pf_ctl_state()
+    _check(lib().pf_ctl_get_state(ctl.h, ctypes.byref(st)))
+    return st
+
+
+def pf_ctl_set_state(ctl: Controller, st: pf_ctl_state) -> None:
+    _check(lib().pf_ctl_set_state(ctl.h, ctypes.byref(st)))
+
+
+def pf_ctl_objective(ctl: Controller, s: float, avail: int):
+    """(objective values for l = 0..L as an array, argmin)."""
+    L = max(0, min(ctl.l_max, int(avail)))
+    out = np.zeros(L + 1, np.float64)
+    best = ctypes.c_int32()
+    _check(lib().pf_ctl_objective(ctl.h, float(s), int(avail), out.ctypes.data, ctypes.byref(best)))
+    return out, int(best.value)
+
+
+def pf_ctl_choose(ctl: Controller, s: float, avail: int) -> int:
+    l = ctypes.c_int32()
+    _check(lib().pf_ctl_choose(ctl.h, float(s), int(avail), ctypes.byref(l)))
+    return int(l.value)
+
+
+def pf_ctl_observe(ctl: Controller, l: int, s: float, accepted: int, latency_ms: float) -> None:
+    _check(lib().pf_ctl_observe(ctl.h, int(l), float(s), int(accepted), float(latency_ms)))
+
+
+class pf_iteration(ctypes.Structure):
+    _fields_ = [("n_found", ctypes.c_int32), ("avail", ctypes.c_int32), ("l", ctypes.c_int32),
+                ("accepted", ctypes.c_int32), ("bonus", ctypes.c_int32),
+                ("status", ctypes.c_int32), ("s", ctypes.c_double), ("ms", ctypes.c_double)]
+
+
+def pf_decode_iteration(model: "Model", kv: "KVCache", ctx: "Context", store: "Store",
+                        kp: "KeyProj", ctl: Optional[Controller], l_fixed: int, qkey, draft,
+                        result, stream=None) -> dict:
+    it = pf_iteration()
+    _check(lib().pf_decode_iteration(model.h, ctypes.byref(kv.c), ctypes.byref(ctx.c), store.h,
+                                     kp.h, ctl.h if ctl is not None else None, int(l_fixed),
+                                     qkey.data_ptr(), draft.data_ptr(), result.data_ptr(),
+                                     ctypes.byref(it), _stream(stream)))
+    return {k: getattr(it, k) for k, _ in pf_iteration._fields_}
 
 
 class KeyProj:

@@ -17,11 +17,9 @@ thread_local LaunchTimer *pf::t_launch_timer = nullptr;
 static_assert(sizeof(pf_draft) == 1384, "pf_draft layout");
 static_assert(sizeof(pf_verify_result) == 808, "pf_verify_result layout");
 
-namespace {
+static thread_local std::string g_err;
 
-thread_local std::string g_err;
-
-pf_status fail(pf_status st, const char *fmt, ...) {
+pf_status pf::fail(pf_status st, const char *fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -31,10 +29,12 @@ pf_status fail(pf_status st, const char *fmt, ...) {
   return st;
 }
 
-pf_status ok() {
+pf_status pf::ok() {
   g_err.clear();
   return PF_OK;
 }
+
+namespace {
 
 #define HIPCHK(call)                                                                   \
   do {                                                                                 \
@@ -135,6 +135,7 @@ void model_free(pf_model *m) {
                   m->apart_o, m->apart_ml, m->amax, m->rope, m->rowinfo, m->pred, m->flags};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
+  if (m->stage) (void)hipHostFree(m->stage);
   delete m;
 }
 
@@ -686,6 +687,25 @@ static pf_status model_kv_match(const pf_model *m, const pf_kv_cache *kv, const 
     HIPCHK(call);                                                                \
   } while (0)
 
+// Keys per attention key range. Ranges start at multiples of this length,
+// and the length depends on the row count of the step only through the key
+// bound's band, so a query row is reduced over the same ranges in the same
+// order whatever rows share its step: a verify row reproduces, bit for bit,
+// the single-row step at its position (greedy decoding), except when the two
+// steps' key bounds fall in different bands. The length is five 32-key (bf16;
+// 16-key fp32) chunks per range (measured best: shorter ranges add splits and
+// waves, longer ones leave the kernel's straight-line part), doubled until
+// the ranges of one query row per head fit the resident waves (one per SIMD)
+// and the combine's 64 lanes.
+static int attn_range_keys(int64_t keys_max, bool bf, int nq, int wave_slots) {
+  int max_splits = wave_slots / nq;
+  if (max_splits > kMaxSplitsAttn) max_splits = kMaxSplitsAttn;
+  if (max_splits < 1) max_splits = 1;
+  int64_t chunk = 5 * (bf ? 32 : 16);
+  while ((keys_max + chunk - 1) / chunk > max_splits) chunk *= 2;
+  return (int)chunk;
+}
+
 static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft, int32_t rows,
                              int32_t tree, float *logits, pf_verify_result *res, pf_stream s,
                              Prof *prof) {
@@ -728,18 +748,13 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
 
   // attention geometry: key ranges over P + rows keys (P <= host bound)
   const int64_t keys_max = kv->host_bound + rows;
-  // key ranges of about five chunks per wave (measured best: shorter ranges
-  // add splits and waves, longer ones leave the straight-line part of the
-  // kernel), longer when needed to keep every attention wave resident at once
-  // (one wave per SIMD at the kernel's register footprint)
-  const int row_groups = (MT + 1) / 2;
-  int max_splits = m->wave_slots / (nq * row_groups);
-  if (max_splits > kMaxSplitsAttn) max_splits = kMaxSplitsAttn;
-  if (max_splits < 1) max_splits = 1;
-  int chunk = (int)roundup((keys_max + max_splits - 1) / max_splits, 32);
-  const int pref = 5 * (bf ? 32 : 16);
-  if (chunk < pref) chunk = pref;
+  const int chunk = attn_range_keys(keys_max, bf, nq, m->wave_slots);
   const int n_splits = (int)((keys_max + chunk - 1) / chunk);
+  // rows beyond two 16-row tiles take more waves per range; those waves then
+  // reduce several consecutive ranges each, to stay within the resident waves
+  const int row_groups = (MT + 1) / 2;
+  const int per_wave =
+      (int)(((int64_t)nq * row_groups * n_splits + m->wave_slots - 1) / m->wave_slots);
 
   for (int l = 0; l < L; ++l) {
     // QKV projection (split-K partials)
@@ -773,6 +788,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     at.kv_len = kv->len;
     at.n_splits = n_splits;
     at.chunk_keys = chunk;
+    at.per_wave = per_wave;
     at.keys_bound = (int)keys_max;
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
     at.tree = tree;
@@ -1062,6 +1078,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       at.kv_len = kv->len;
       at.n_splits = nsp;
       at.chunk_keys = ck;
+      at.per_wave = 1;
       at.keys_bound = (int)keys_max;
       at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
       at.tree = 0;

@@ -65,22 +65,29 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   // XCD-aware placement: blocks are dispatched round-robin over the 8 XCDs,
   // so the `group` query heads that read the same (KV head, key range) get
   // block ids of equal residue mod 8 and share one L2.
+  // A wave reduces per_wave consecutive key ranges, one after the other,
+  // and writes one partial per range: every range is reduced from fresh
+  // accumulators in the same order whichever wave takes it, so the result
+  // does not depend on how ranges are spread over waves.
   const int b = blockIdx.x;
   const int xcd = b & 7, j = b >> 3;
   const int hl = j % a.group;
-  const int w = (j / a.group) * 8 + xcd;  // (KV head, key range) work id
-  if (w >= a.n_kv * a.n_splits) return;
-  const int g = w / a.n_splits;
-  const int s = w % a.n_splits;
+  const int nwr = (a.n_splits + a.per_wave - 1) / a.per_wave;  // wave ranges per KV head
+  const int w = (j / a.group) * 8 + xcd;  // (KV head, wave range) work id
+  if (w >= a.n_kv * nwr) return;
+  const int g = w / nwr;
+  const int s0 = (w % nwr) * a.per_wave;  // first key range of this wave
   const int h = g * a.group + hl;
   const int row0 = blockIdx.y * RT * 16;  // first query row of this wave
 
   const int M = a.M;
-  const int k0 = s * a.chunk_keys;
+  const int k0 = s0 * a.chunk_keys;
+  const int kw = k0 + a.per_wave * a.chunk_keys;  // end of the wave's keys
+  const int cps = a.chunk_keys / KC;              // chunks per key range
   // Loads are bounded by the host's upper bound on P + M, so they are issued
   // without waiting for the device-side length; keys past the true end are
   // masked once P has arrived.
-  const int kb = min(k0 + a.chunk_keys, a.keys_bound);
+  const int kb = min(kw, a.keys_bound);
   const int nchunks = kb > k0 ? (kb - k0 + KC - 1) / KC : 0;
 
   float m_run[RT], l_run[RT];
@@ -139,7 +146,7 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   // j >= i), and for a tree also ancestor-or-self among the draft keys
   const int P = *a.kv_len;
   const int kend = P + M;
-  const int k1 = min(k0 + a.chunk_keys, kend);
+  const int k1 = min(kw, kend);
   int lim[RT];
   uint64_t anc[RT];
 #pragma unroll
@@ -149,11 +156,11 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
     anc[r] = a.tree ? a.anc[min(jq, a.rowpad - 1)] : 0ull;
   }
 
-  // Online softmax with a deferred rescale: m_run is a reference maximum (raw
-  // score units) that only moves when some row's maximum exceeds it by more
-  // than 2^8 in probability, so probabilities stay below 256 and the
-  // accumulators are rescaled a handful of times per range instead of per
-  // chunk. The result equals the usual update up to rounding.
+  // Online softmax with a deferred rescale: m_run is a row's reference
+  // maximum (raw score units) that only moves when the row's maximum exceeds
+  // it by more than 2^8 in probability, so probabilities stay below 256 and
+  // the accumulators are rescaled a handful of times per range instead of
+  // per chunk. The result equals the usual update up to rounding.
   constexpr float kSlack = 8.f;  // log2 headroom of the reference maximum
   auto compute = [&](int slot, int c) {
     const int kc = k0 + c * KC;
@@ -192,12 +199,15 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
       for (int e = 1; e < E; ++e) cmax = fmaxf(cmax, sv[e]);
       cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
       cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
-      // move the reference when a row outgrows it (wave-uniform decision)
+      // move the reference of the rows that outgrew it. The branch is taken
+      // by the whole wave, but every row decides for itself (the others keep
+      // their reference and scale by exactly 1), so a row's arithmetic never
+      // depends on the other rows of its tile.
       const bool grow = m_run[r] == -INFINITY ? cmax > -INFINITY : (cmax - m_run[r]) * sc > kSlack;
       if (__any(grow)) {
-        const float m_new = fmaxf(m_run[r], cmax);
+        const float m_new = grow ? fmaxf(m_run[r], cmax) : m_run[r];
         const float alpha =
-            m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f((m_run[r] - m_new) * sc);
+            grow ? __builtin_amdgcn_exp2f((m_run[r] - m_new) * sc) : 1.f;  // exp2(-inf) = 0
         l_run[r] *= alpha;
 #pragma unroll
         for (int t = 0; t < NDT; ++t) o[r][t] *= alpha;
@@ -216,47 +226,65 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
       for (int t = 0; t < NDT; ++t) o[r][t] = mma<T>(vf[slot][t], pu, o[r][t]);
     }
   };
+  // write the partial of key range sp and restart the accumulators: lane
+  // holds O^T[d = t*16 + 4q + i][row lane%16]
+  auto flush = [&](int sp) {
+    float *po = a.part_o + (((int64_t)h * a.n_splits + sp) * a.rowpad) * HD;
+    float *pml = a.part_ml + (((int64_t)h * a.n_splits + sp) * a.rowpad) * 2;
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      float l = l_run[r];
+      l += __shfl_xor(l, 16, 64);
+      l += __shfl_xor(l, 32, 64);
+      const int jq = row0 + r * 16 + (lane & 15);
+      if (jq < M) {
+#pragma unroll
+        for (int t = 0; t < NDT; ++t)
+          *(float4 *)(po + (int64_t)jq * HD + t * 16 + 4 * q) =
+              make_float4(o[r][t][0], o[r][t][1], o[r][t][2], o[r][t][3]);
+        if (q == 0) {  // (max, sum) in the log2-scaled units the combine uses
+          pml[jq * 2 + 0] = m_run[r] == -INFINITY ? -INFINITY : m_run[r] * sc;
+          pml[jq * 2 + 1] = l;
+        }
+      }
+      m_run[r] = -INFINITY;
+      l_run[r] = 0.f;
+#pragma unroll
+      for (int t = 0; t < NDT; ++t) o[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  int sp = s0, next_flush = cps - 1;  // key range being reduced, its last chunk
+  auto step = [&](int slot, int c) {
+    compute(slot, c);
+    if (c == next_flush && c < nchunks) {  // uniform over the wave
+      flush(sp++);
+      next_flush += cps;
+    }
+  };
+
   // The first kStraight chunks run as straight-line code (no loop-carried
   // accumulators to shuffle between register files); longer ranges continue
   // in a loop. Compute of a chunk past the range returns at once.
   constexpr int kStraight = 6;
 #pragma unroll
   for (int c = 0; c < kStraight; c += 2) {
-    compute(0, c);
+    step(0, c);
     load(0, c + 2);
     __builtin_amdgcn_sched_barrier(0);
-    compute(1, c + 1);
+    step(1, c + 1);
     load(1, c + 3);
     __builtin_amdgcn_sched_barrier(0);
   }
   for (int c = kStraight; c < nchunks; c += 2) {
-    compute(0, c);
+    step(0, c);
     load(0, c + 2);
     __builtin_amdgcn_sched_barrier(0);
-    compute(1, c + 1);
+    step(1, c + 1);
     load(1, c + 3);
     __builtin_amdgcn_sched_barrier(0);
   }
-
-  // write the partial: lane holds O^T[d = t*16 + 4q + i][row lane%16]
-  float *po = a.part_o + (((int64_t)h * a.n_splits + s) * a.rowpad) * HD;
-  float *pml = a.part_ml + (((int64_t)h * a.n_splits + s) * a.rowpad) * 2;
-#pragma unroll
-  for (int r = 0; r < RT; ++r) {
-    float l = l_run[r];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
-    const int jq = row0 + r * 16 + (lane & 15);
-    if (jq >= M) continue;
-#pragma unroll
-    for (int t = 0; t < NDT; ++t)
-      *(float4 *)(po + (int64_t)jq * HD + t * 16 + 4 * q) =
-          make_float4(o[r][t][0], o[r][t][1], o[r][t][2], o[r][t][3]);
-    if (q == 0) {  // (max, sum) in the log2-scaled units the combine uses
-      pml[jq * 2 + 0] = m_run[r] == -INFINITY ? -INFINITY : m_run[r] * sc;
-      pml[jq * 2 + 1] = l;
-    }
-  }
+  // the last range ends before a whole number of chunks (key bound)
+  if (nchunks % cps != 0) flush(sp);
 }
 
 // Merge the key-range partials of one (row, head) and round the result:
@@ -315,8 +343,9 @@ static hipError_t attn_t(int rt, const AttnArgs &a, hipStream_t s) {
   // are spread over blockIdx.y
   const int per = rt <= 2 ? rt : 2;
   const int groups = (rt + per - 1) / per;
-  const int works = a.n_kv * a.n_splits;
-  if (a.chunk_keys % (4 * Elem<T>::E) != 0 || a.keys_bound < 0) return hipErrorInvalidValue;
+  if (a.chunk_keys % (4 * Elem<T>::E) != 0 || a.keys_bound < 0 || a.per_wave < 1)
+    return hipErrorInvalidValue;
+  const int works = a.n_kv * ((a.n_splits + a.per_wave - 1) / a.per_wave);
   dim3 grid(8 * a.group * ((works + 7) / 8), groups), block(64);
   switch (per) {
     case 1: PF_TRY(launch_k(k_attn<T, 1, HD>, grid, block, s, a)); break;

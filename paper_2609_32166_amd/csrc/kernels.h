@@ -100,8 +100,9 @@ struct AttnArgs {
   int rowpad;           // row stride of q and of the partial buffers (>= rows, rows of q
                         // past M must be readable)
   const int32_t *kv_len;  // P (device)
-  int n_splits;         // key ranges (grid.x)
+  int n_splits;         // key ranges, one partial result each
   int chunk_keys;       // keys per range (multiple of the chunk, 32 bf16 / 16 fp32)
+  int per_wave;         // consecutive key ranges one wave reduces (>= 1)
   int keys_bound;       // host upper bound on P + M (loads stay below it)
   float scale_log2;     // log2(e) / sqrt(head_dim)
   int tree;

@@ -11,6 +11,11 @@
 
 namespace pf {
 
+// status helpers of the C ABI: fail() records the message returned by
+// pf_last_error() and returns st; ok() clears it
+pf_status fail(pf_status st, const char *fmt, ...);
+pf_status ok();
+
 // ---------------------------------------------------------------------------
 // element types
 // ---------------------------------------------------------------------------
@@ -169,6 +174,15 @@ struct pf_model {
         *pre_apml = nullptr;
   void *pre_xn = nullptr, *pre_qb = nullptr, *pre_attn = nullptr, *pre_act = nullptr;
   int32_t *pre_rowinfo = nullptr, *pre_status = nullptr;
+  // pinned host staging of the decode iteration (draft and result copies),
+  // allocated on its first use
+  void *stage = nullptr;
+};
+
+// proposal-length controller: parameters and estimator states
+struct pf_ctl {
+  pf_ctl_params p;
+  pf_ctl_state st;
 };
 
 struct pf_store {

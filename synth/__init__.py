@@ -432,3 +432,30 @@ def hidden_states(n: int, hidden: int, seed: int) -> np.ndarray:
 
 def bf16_bits_to_f32(a: np.ndarray) -> np.ndarray:
     return (a.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+_T_REPLAY = 904
+
+
+def replay_store(base: Store, base_keys: np.ndarray, first_token: int, outputs: np.ndarray,
+                 output_keys: np.ndarray, mutate: float, seed: int, vocab: int):
+    """A store that holds a prior execution of the same task (the paper's
+    premise: agents repeat tasks, so earlier output sequences recur): the
+    base store plus one sequence [first_token, outputs...] whose tokens past
+    the second are replaced, each with probability `mutate`, by a different
+    uniform token (a prior run that drifted). Entry p's key describes the
+    context that produced token p: output_keys[i] for outputs[i], a zero key
+    for first_token. Returns (tokens, seq_offsets, keys)."""
+    seq = np.concatenate([[first_token], outputs]).astype(np.int32)
+    k = key(seed, _T_REPLAY)
+    n = len(seq)
+    hit = uniform(k, n, first=0) < mutate
+    hit[:2] = False
+    repl = randint(k, n, 0, vocab - 1, first=n)
+    repl = np.where(repl >= seq, repl + 1, repl)   # uniform over the other tokens
+    seq = np.where(hit, repl, seq).astype(np.int32)
+    keys = np.concatenate([np.zeros((1, KEY_DIM), np.int8),
+                           np.asarray(output_keys, np.int8).reshape(-1, KEY_DIM)])
+    tokens = np.concatenate([base.tokens, seq]).astype(np.int32)
+    offs = np.concatenate([base.seq_offsets, [base.seq_offsets[-1] + n]]).astype(np.int64)
+    return tokens, offs, np.concatenate([base_keys, keys]).astype(np.int8)
