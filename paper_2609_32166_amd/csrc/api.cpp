@@ -750,11 +750,11 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   const int64_t keys_max = kv->host_bound + rows;
   const int chunk = attn_range_keys(keys_max, bf, nq, m->wave_slots);
   const int n_splits = (int)((keys_max + chunk - 1) / chunk);
-  // rows beyond two 16-row tiles take more waves per range; those waves then
+  // rows beyond one wave's tiles take more waves per range; those waves then
   // reduce several consecutive ranges each, to stay within the resident waves
-  const int row_groups = (MT + 1) / 2;
-  const int per_wave =
-      (int)(((int64_t)nq * row_groups * n_splits + m->wave_slots - 1) / m->wave_slots);
+  const int row_groups = (MT + attn_tiles_per_wave(MT) - 1) / attn_tiles_per_wave(MT);
+  const int64_t slots = (int64_t)m->wave_slots * attn_waves_per_simd(MT);
+  const int per_wave = (int)(((int64_t)nq * row_groups * n_splits + slots - 1) / slots);
 
   for (int l = 0; l < L; ++l) {
     // QKV projection (split-K partials)

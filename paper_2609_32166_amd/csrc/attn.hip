@@ -52,8 +52,24 @@ template <typename T> __device__ inline uint4 keep_first(uint4 v, int n) {
   return make_uint4(v.x & m[0], v.y & m[1], v.z & m[2], v.w & m[3]);
 }
 
-template <typename T, int RT, int HD>
-__global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
+// Max / sum over the four lanes that hold the same MFMA row (lanes l, l^16,
+// l^32, l^48) with the cross-row lane swaps (no LDS round trip): a swap of
+// x with itself leaves each lane x and its partner's x in the two results.
+__device__ __forceinline__ float row_max4(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float row_sum4(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+template <typename T, int RT, int HD, int WPE = 1, int NS = 2>
+__global__ __launch_bounds__(64, WPE) void k_attn(AttnArgs a) {
   constexpr int E = Elem<T>::E;
   constexpr int KF = 4 * E;       // d per MFMA step, keys per chunk
   constexpr int KC = 4 * E;       // keys per chunk
@@ -116,10 +132,13 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   const rsrc_t vr = make_rsrc(vplane, plane_bytes);
   const float sc = a.scale_log2;
 
-  // two chunk slots: compute one while the other's K/V loads are in flight.
-  // Chunks past the range load out of the resource (zeros, no traffic).
-  uint4 kf[2][NCG][NDS], vf[2][NDT];
-  auto load = [&](int slot, int c) {
+  // K/V chunk slots. NS >= 2: compute one chunk while the others' loads are
+  // in flight. NS == 1: one slot, the next chunk's K issued as soon as the
+  // score products have read the current one and its V after the value
+  // products (fewer live registers). Chunks past the range load out of the
+  // resource (zeros, no traffic).
+  uint4 kf[NS][NCG][NDS], vf[NS][NDT];
+  auto load_k = [&](int slot, int c) {
     const int kc = k0 + c * KC;
     const bool in = c < nchunks;
 #pragma unroll
@@ -131,16 +150,25 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
         kf[slot][cg][d] =
             bload16(kr, in ? (uint32_t)(((int64_t)key * HD + d * KF + q * E) * sizeof(T)) : kOOB);
     }
+  };
+  auto load_v = [&](int slot, int c) {
+    const int kc = k0 + c * KC;
+    const bool in = c < nchunks;
 #pragma unroll
     for (int t = 0; t < NDT; ++t)
       vf[slot][t] = bload16(
           vr, in ? (uint32_t)(((int64_t)(t * 16 + (lane & 15)) * a.cap + kc + q * E) * sizeof(T))
                  : kOOB);
   };
-  load(0, 0);
-  __builtin_amdgcn_sched_barrier(0);
-  load(1, 1);
-  __builtin_amdgcn_sched_barrier(0);
+  auto load = [&](int slot, int c) {
+    load_k(slot, c);
+    load_v(slot, c);
+  };
+#pragma unroll
+  for (int u = 0; u < NS; ++u) {
+    load(u, u);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 
   // visibility: key < lim[r] (linear drafts: draft key P + i is seen by rows
   // j >= i), and for a tree also ancestor-or-self among the draft keys
@@ -166,6 +194,18 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
     const int kc = k0 + c * KC;
     if (c >= nchunks || kc >= k1) return;  // uniform over the wave
     const int kl = kc + q * E;             // first key of this lane's chunk
+    float sv[RT][E];
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int cg = 0; cg < NCG; ++cg) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int d = 0; d < NDS; ++d) acc = mma<T>(kf[slot][cg][d], qf[r][d], acc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sv[r][4 * cg + i] = acc[i];
+      }
+    if constexpr (NS == 1) load_k(0, c + 1);
     // value columns of keys past the end of the cache are zeroed (not
     // initialised there; a zero probability must not meet a NaN)
     if (kc + KC > kend) {
@@ -176,29 +216,19 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
     const bool all_visible = kc + KC <= min(P, k1);  // cached prefix only (uniform)
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
-      float sv[E];
-#pragma unroll
-      for (int cg = 0; cg < NCG; ++cg) {
-        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int d = 0; d < NDS; ++d) acc = mma<T>(kf[slot][cg][d], qf[r][d], acc);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sv[4 * cg + i] = acc[i];
-      }
       if (!all_visible) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           const int key = kl + e;
           bool vis = key < lim[r];
           if (a.tree) vis &= (key < P) | (((anc[r] >> ((key - P) & 63)) & 1ull) != 0);
-          sv[e] = vis ? sv[e] : -INFINITY;
+          sv[r][e] = vis ? sv[r][e] : -INFINITY;
         }
       }
-      float cmax = sv[0];
+      float cmax = sv[r][0];
 #pragma unroll
-      for (int e = 1; e < E; ++e) cmax = fmaxf(cmax, sv[e]);
-      cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
-      cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
+      for (int e = 1; e < E; ++e) cmax = fmaxf(cmax, sv[r][e]);
+      cmax = row_max4(cmax);
       // move the reference of the rows that outgrew it. The branch is taken
       // by the whole wave, but every row decides for itself (the others keep
       // their reference and scale by exactly 1), so a row's arithmetic never
@@ -217,7 +247,7 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
       float p[E], psum = 0.f;
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(fmaf(sv[e], sc, -msc));  // exp2(-inf) = 0
+        p[e] = __builtin_amdgcn_exp2f(fmaf(sv[r][e], sc, -msc));  // exp2(-inf) = 0
         psum += p[e];
       }
       l_run[r] += psum;
@@ -225,6 +255,7 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int t = 0; t < NDT; ++t) o[r][t] = mma<T>(vf[slot][t], pu, o[r][t]);
     }
+    if constexpr (NS == 1) load_v(0, c + 1);
   };
   // write the partial of key range sp and restart the accumulators: lane
   // holds O^T[d = t*16 + 4q + i][row lane%16]
@@ -233,9 +264,7 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
     float *pml = a.part_ml + (((int64_t)h * a.n_splits + sp) * a.rowpad) * 2;
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
-      float l = l_run[r];
-      l += __shfl_xor(l, 16, 64);
-      l += __shfl_xor(l, 32, 64);
+      const float l = row_sum4(l_run[r]);
       const int jq = row0 + r * 16 + (lane & 15);
       if (jq < M) {
 #pragma unroll
@@ -265,23 +294,35 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   // The first kStraight chunks run as straight-line code (no loop-carried
   // accumulators to shuffle between register files); longer ranges continue
   // in a loop. Compute of a chunk past the range returns at once.
-  constexpr int kStraight = 6;
+  constexpr int kStraight = NS * ((6 + NS - 1) / NS);
+  if constexpr (NS == 1) {
 #pragma unroll
-  for (int c = 0; c < kStraight; c += 2) {
-    step(0, c);
-    load(0, c + 2);
-    __builtin_amdgcn_sched_barrier(0);
-    step(1, c + 1);
-    load(1, c + 3);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  for (int c = kStraight; c < nchunks; c += 2) {
-    step(0, c);
-    load(0, c + 2);
-    __builtin_amdgcn_sched_barrier(0);
-    step(1, c + 1);
-    load(1, c + 3);
-    __builtin_amdgcn_sched_barrier(0);
+    for (int c = 0; c < kStraight; ++c) {
+      step(0, c);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int c = kStraight; c < nchunks; ++c) {
+      step(0, c);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < kStraight; c += NS) {
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        step(u, c + u);
+        load(u, c + u + NS);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    for (int c = kStraight; c < nchunks; c += NS) {
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        step(u, c + u);
+        load(u, c + u + NS);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
   }
   // the last range ends before a whole number of chunks (key bound)
   if (nchunks % cps != 0) flush(sp);
@@ -339,17 +380,16 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
 
 template <typename T, int HD>
 static hipError_t attn_t(int rt, const AttnArgs &a, hipStream_t s) {
-  // at most two 16-row query tiles per wave (register budget); more rows
-  // are spread over blockIdx.y
-  const int per = rt <= 2 ? rt : 2;
+  const int per = attn_tiles_per_wave(rt);
   const int groups = (rt + per - 1) / per;
   if (a.chunk_keys % (4 * Elem<T>::E) != 0 || a.keys_bound < 0 || a.per_wave < 1)
     return hipErrorInvalidValue;
   const int works = a.n_kv * ((a.n_splits + a.per_wave - 1) / a.per_wave);
   dim3 grid(8 * a.group * ((works + 7) / 8), groups), block(64);
   switch (per) {
-    case 1: PF_TRY(launch_k(k_attn<T, 1, HD>, grid, block, s, a)); break;
-    case 2: PF_TRY(launch_k(k_attn<T, 2, HD>, grid, block, s, a)); break;
+    case 1: PF_TRY(launch_k(k_attn<T, 1, HD, 2, 1>, grid, block, s, a)); break;
+    case 2: PF_TRY(launch_k(k_attn<T, 2, HD, 2, 1>, grid, block, s, a)); break;
+    case 3: PF_TRY(launch_k(k_attn<T, 3, HD, 1, 1>, grid, block, s, a)); break;
     default: return hipErrorInvalidValue;
   }
   PF_TRY(launch_k(k_attn_combine<T, HD>, dim3(a.M, a.n_kv * a.group), 64, s, a));

@@ -115,6 +115,12 @@ struct AttnArgs {
 };
 
 hipError_t launch_attn(bool bf16, int rt, const AttnArgs &a, hipStream_t s);
+// Query tiles (16 rows) per attention wave for rt tiles, and the waves each
+// SIMD holds at that footprint: one or two tiles fit two waves per SIMD,
+// three tiles one; more tiles are spread over waves of three (five tiles)
+// or two.
+inline int attn_tiles_per_wave(int rt) { return rt <= 2 ? rt : (rt == 3 || rt == 5) ? 3 : 2; }
+inline int attn_waves_per_simd(int rt) { return attn_tiles_per_wave(rt) == 3 ? 1 : 2; }
 
 // step kernels (step.hip)
 struct StepArgs {
