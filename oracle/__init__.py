@@ -16,8 +16,9 @@ It computes, with plain fp64 loops in ``oracle.c``, what the paper
   proposal, greedy predictions at every row, acceptance of the longest
   matching proposal prefix plus the model's next token, which must equal
   greedy decoding ("Single-pass token verification");
-* the KV commit implied by that acceptance, and the prompt-prefix carryover
-  that resumes computation right after a reused prefix (Section 3.4);
+* the KV commit implied by that acceptance, the prompt-prefix carryover
+  that resumes computation right after a reused prefix, and the rolling-image
+  carryover that moves retained spans and re-rotates their keys (Section 3.4);
 * the paper's own retrieval keys and lookup: final-layer states projected to
   256-dimensional int8 keys by a fixed random projection (Section 4) and the
   cosine argmax over the entries whose stored token matches the query token
@@ -445,6 +446,30 @@ def greedy_decode(model: Model, kv_prefix: np.ndarray, first_token: int, steps: 
 def commit(kv_new: np.ndarray, path: Sequence[int]) -> np.ndarray:
     """KV rows kept after acceptance: node path[d] lands at depth slot d."""
     return kv_new[:, :, :, list(path), :]
+
+
+def kv_carry(kv: np.ndarray, spans: Sequence[Sequence[int]], theta: float) -> np.ndarray:
+    """Rolling-image KV-state carryover (Section 3.4): each retained span
+    (src, dst, n) of cached tokens moves from positions src..src+n-1 to
+    dst..dst+n-1; a key cached at position m becomes R(m') R(m)^-1 of it at
+    m' = m + dst - src (R: the model's rotary embedding, inverted as the
+    rotation by -m), values move unchanged. Spans apply one after another,
+    each reading the cache as the previous ones left it. kv: logical layout
+    [L][2][n_kv][T][head_dim]; returns a new fp64 array."""
+    out = np.array(kv, np.float64, copy=True)
+    for src, dst, n in spans:
+        src, dst, n = int(src), int(dst), int(n)
+        keys = out[:, 0, :, src:src + n, :].copy()
+        vals = out[:, 1, :, src:src + n, :].copy()
+        L, nkv = keys.shape[0], keys.shape[1]
+        for l in range(L):
+            for g in range(nkv):
+                for i in range(n):
+                    back = rope(keys[l, g, i], -(src + i), theta)       # R(m)^-1
+                    keys[l, g, i] = rope(back, dst + i, theta)          # R(m')
+        out[:, 0, :, dst:dst + n, :] = keys
+        out[:, 1, :, dst:dst + n, :] = vals
+    return out
 
 
 def prefill(model: Model, kv_prefix: np.ndarray, tokens: Sequence[int], chunk: int) -> dict:
