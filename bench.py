@@ -352,6 +352,49 @@ def decode_loop(torch, pf, wl, model, kv_host, store, ctx, gen=256, mutate=0.05)
     return out
 
 
+def carry_timings(torch, pf, wl, model, kv_host):
+    """Rolling-image KV-state carryover (Section 3.4) on this workload's
+    cache: the prompt's image-placeholder run (positions 64 .. 64 + 61% of P)
+    read as three screenshots; the next step evicts the first and moves the
+    other two one screenshot to the left (two spans, keys re-rotated, values
+    copied). Timed as the mean of 20 calls between events, against the
+    prefill of the same tokens that the carryover replaces."""
+    shape, P = wl.model, wl.prefix
+    n = int(0.61 * P) // 3
+    cap = ((P + 63) // 64) * 64 + 64
+    kv = pf.KVCache(model, cap)
+    pf.pf_kv_import(kv, pf.array_to_device(kv_host), P)
+    spans = [(64 + n, 64, n), (64 + 2 * n, 64 + n, n)]
+    esz = 2 if shape.dtype == "bf16" else 4
+    nbytes = 2 * (2 * n) * shape.n_layers * shape.n_kv_heads * shape.head_dim * 2 * esz
+    pf.pf_kv_carry(kv, model, spans)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(20):
+        pf.pf_kv_carry(kv, model, spans)
+    e1.record()
+    torch.cuda.synchronize()
+    us = 1e3 * e0.elapsed_time(e1) / 20
+    # the alternative: recompute the two screenshots' tokens by prefill
+    pf.pf_kv_set_len(kv, 64)
+    toks = torch.from_numpy(synth.make_prefill_tokens(wl, synth.case_seed(wl, 14), 2 * n)).cuda()
+    pf.pf_prefill(model, kv, toks, 2 * n, 512)
+    pf.pf_kv_set_len(kv, 64)
+    torch.cuda.synchronize()
+    e0.record()
+    pf.pf_prefill(model, kv, toks, 2 * n, 512)
+    e1.record()
+    torch.cuda.synchronize()
+    pre_ms = e0.elapsed_time(e1)
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"tokens_moved": 2 * n, "spans": [list(x) for x in spans], "us": round(us, 2),
+            "algorithmic_bytes": nbytes, "GBps": round(gbs, 1),
+            "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "prefill_of_same_tokens_ms": round(pre_ms, 3),
+            "speedup_vs_prefill": round(pre_ms * 1e3 / us, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -556,6 +599,8 @@ def main():
         out["prefill"] = prefill
     if not args.no_loop and not wl.tree:
         out["decode_loop"] = decode_loop(torch, pf, wl, model, kv_host, store, ctx)
+    if not args.no_sweep and wl.model.dtype == "bf16":
+        out["rolling_image_carryover"] = carry_timings(torch, pf, wl, model, kv_host)
     if not args.no_cpu_baseline:
         od = {"n_nodes": int(d["n_nodes"]), "token": np.array(d["token"][:int(d["n_nodes"])]),
               "parent": np.array(d["parent"][:int(d["n_nodes"])]),

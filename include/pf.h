@@ -370,6 +370,26 @@ pf_status pf_kv_commit(pf_kv_cache *kv, const pf_verify_result *res_dev, pf_cont
 /* ------------------------------------------------------------------------ */
 
 /*
+ * Rolling-image KV-state carryover (Section 3.4): for s = 0..n_spans-1 in
+ * order, the cached tokens at slots src[s]..src[s]+len[s]-1 move to slots
+ * dst[s]..dst[s]+len[s]-1. A key cached at position m becomes
+ * R(m') R(m)^-1 K at m' = m + dst[s] - src[s] (R: the model's rotary
+ * embedding; evaluated as the rotation by m' - m, angles in fp64, the
+ * rotation in fp32, rounded to the cache dtype); values move unchanged.
+ * Every span reads the cache as the earlier spans left it, and a span whose
+ * source and destination overlap behaves as a memmove (it runs as pieces of
+ * |dst - src| tokens, one launch each). Slots are read whether or not they
+ * lie below the cache length, which the call does not change: a step that
+ * keeps a prefix sets the length (pf_kv_set_len) to prefill the new tokens
+ * between and after the carried spans. src, dst, len: host arrays; every
+ * span must lie inside the capacity. Errors: PF_EINVAL (spans), PF_ESTATE (a
+ * verify step not committed), PF_EUNSUPPORTED (head_dim > 256). Allocates
+ * nothing, does not synchronise.
+ */
+pf_status pf_kv_carry(pf_kv_cache *kv, const pf_model *model, int32_t n_spans, const int64_t *src,
+                      const int64_t *dst, const int64_t *len, pf_stream s);
+
+/*
  * Run n new tokens (device int32) through the decoder after the cached
  * prefix P = *kv->len, in causal chunks of `chunk` rows, appending their K/V
  * at slots P..P+n-1 and setting the length to P+n. logits_last_dev: NULL or

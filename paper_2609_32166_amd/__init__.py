@@ -42,7 +42,8 @@ EXPORTED = ["pf_last_error", "pf_version", "pf_context_init", "pf_context_sync_b
             "pf_keyproj_destroy", "pf_key_encode", "pf_store_attach_keys",
             "pf_draft_lookup_cosine", "pf_verify_query_key", "pf_verify_row_keys",
             "pf_ctl_create", "pf_ctl_destroy", "pf_ctl_get_state", "pf_ctl_set_state",
-            "pf_ctl_objective", "pf_ctl_choose", "pf_ctl_observe", "pf_decode_iteration"]
+            "pf_ctl_objective", "pf_ctl_choose", "pf_ctl_observe", "pf_decode_iteration",
+            "pf_kv_carry"]
 
 PF_PROF_KINDS = 11
 PROF_NAMES = ["setup", "qkv", "qkv_post", "attn", "o_proj", "norm", "gate_up", "down",
@@ -130,6 +131,7 @@ def lib():
             "pf_ctl_choose": (i32, [vp, ctypes.c_double, i32, vp]),
             "pf_ctl_observe": (i32, [vp, i32, ctypes.c_double, i32, ctypes.c_double]),
             "pf_decode_iteration": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp]),
+            "pf_kv_carry": (i32, [vp, vp, i32, vp, vp, vp, vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -435,6 +437,14 @@ def pf_kv_export(kv: KVCache, dst, start: int, n: int, stream=None) -> None:
 
 def pf_kv_set_len(kv: KVCache, n: int, stream=None) -> None:
     _check(lib().pf_kv_set_len(ctypes.byref(kv.c), int(n), _stream(stream)))
+
+
+def pf_kv_carry(kv: KVCache, model: "Model", spans, stream=None) -> None:
+    """spans: sequence of (src, dst, len) slot spans, applied in order."""
+    sp = np.asarray(spans, np.int64).reshape(-1, 3)
+    src, dst, ln = (np.ascontiguousarray(sp[:, i]) for i in range(3))
+    _check(lib().pf_kv_carry(ctypes.byref(kv.c), model.h, len(sp), src.ctypes.data,
+                             dst.ctypes.data, ln.ctypes.data, _stream(stream)))
 
 
 def pf_kv_sync_bound(kv: KVCache, stream=None) -> None:

@@ -978,6 +978,53 @@ pf_status pf_kv_commit(pf_kv_cache *kv, const pf_verify_result *res, pf_context 
   return ok();
 }
 
+pf_status pf_kv_carry(pf_kv_cache *kv, const pf_model *m, int32_t n_spans, const int64_t *src,
+                      const int64_t *dst, const int64_t *len, pf_stream s) {
+  if (!m) return fail(PF_EINVAL, "pf_kv_carry: null model");
+  if (pf_status r = kv_check(kv, "pf_kv_carry")) return r;
+  if (pf_status r = model_kv_match(m, kv, "pf_kv_carry")) return r;
+  if (kv->pending) return fail(PF_ESTATE, "pf_kv_carry: a verify step is not committed");
+  if (n_spans < 0 || (n_spans > 0 && (!src || !dst || !len)))
+    return fail(PF_EINVAL, "pf_kv_carry: bad span arrays");
+  if (kv->head_dim / 2 > kCarryMaxHalf)
+    return fail(PF_EUNSUPPORTED, "pf_kv_carry: head_dim %d too large", kv->head_dim);
+  if (kv->capacity * kv->head_dim * (kv->dtype == PF_DTYPE_BF16 ? 2 : 4) >= ((int64_t)1 << 31))
+    return fail(PF_EUNSUPPORTED, "pf_kv_carry: one cache plane must stay below 2 GiB");
+  for (int32_t i = 0; i < n_spans; ++i) {
+    if (len[i] < 0 || src[i] < 0 || dst[i] < 0 || len[i] > kv->capacity ||
+        src[i] > kv->capacity - len[i] || dst[i] > kv->capacity - len[i])
+      return fail(PF_EINVAL, "pf_kv_carry: span %d (src %lld, dst %lld, len %lld) outside capacity %lld",
+                  i, (long long)src[i], (long long)dst[i], (long long)len[i],
+                  (long long)kv->capacity);
+  }
+  CarryArgs a{};
+  a.cache = kv->data;
+  a.L = kv->n_layers;
+  a.nkv = kv->n_kv_heads;
+  a.hd = kv->head_dim;
+  a.cap = kv->capacity;
+  a.inv_freq = m->inv_freq;
+  const bool bf = kv->dtype == PF_DTYPE_BF16;
+  for (int32_t i = 0; i < n_spans; ++i) {
+    const int64_t d = dst[i] - src[i], n = len[i];
+    if (d == 0 || n == 0) continue;  // rotation by zero: nothing moves
+    // pieces whose source and destination do not overlap, in the order that
+    // reads every source slot before it is overwritten (memmove)
+    const int64_t piece = std::min<int64_t>(n, d > 0 ? d : -d);
+    const int64_t pieces = (n + piece - 1) / piece;
+    for (int64_t k = 0; k < pieces; ++k) {
+      const int64_t j = d > 0 ? pieces - 1 - k : k;  // right shift: last piece first
+      const int64_t off = j * piece;
+      a.src = src[i] + off;
+      a.dst = dst[i] + off;
+      a.n = (int)std::min<int64_t>(piece, n - off);
+      a.delta = d;
+      HIPCHK(launch_kv_carry(bf, a, st(s)));
+    }
+  }
+  return ok();
+}
+
 constexpr int kPrefillSplits = 8;
 
 static pf_status prefill_alloc(pf_model *m, int64_t rows) {

@@ -183,6 +183,20 @@ hipError_t launch_kv_copy(bool bf16, bool import_, void *cache, const void *logi
 hipError_t launch_set_int(int32_t *p, int32_t v, hipStream_t s);
 hipError_t launch_hold(const int32_t *flag, uint64_t max_ticks, hipStream_t s);
 
+// rolling-image carryover (carry.hip): one span whose source and destination
+// slots do not overlap
+constexpr int kCarryMaxHalf = 128;  // head_dim / 2 at most
+struct CarryArgs {
+  void *cache;              // KV cache data (layout of pf_kv_cache)
+  int L, nkv, hd;
+  int64_t cap;              // slots per plane
+  int64_t src, dst;         // first source / destination slot
+  int n;                    // tokens
+  int64_t delta;            // m' - m = dst - src
+  const double *inv_freq;   // [hd/2] theta^(-2i/hd)
+};
+hipError_t launch_kv_carry(bool bf16, const CarryArgs &a, hipStream_t s);
+
 // lookup (lookup.hip)
 struct LookupArgs {
   const int32_t *tokens;
