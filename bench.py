@@ -298,14 +298,17 @@ def decode_loop(torch, pf, wl, model, kv_host, store, ctx, gen=256, mutate=0.05)
     st0 = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
     pf.pf_store_attach_keys(st0, base_keys)
 
-    def run(st, ctl, l_fixed, record=False):
+    def run(st, ctl, l_fixed, record=False, append=False):
         pf.pf_kv_import(kv, kvd, P)
         c = pf.Context(ctx, len(ctx) + gen + 70)
         q.zero_()
+        if append:
+            pf.pf_store_begin_sequence(st)
         torch.cuda.synchronize()
         its, keys, produced, wall = [], [], 0, 0.0
         while produced < gen:
-            it = pf.pf_decode_iteration(model, kv, c, st, kp, ctl, l_fixed, q, draft, res)
+            it = pf.pf_decode_iteration(model, kv, c, st, kp, ctl, l_fixed, q, draft, res,
+                                        append=append)
             wall += it["ms"]
             if record:
                 keys.append(q.cpu().numpy())
@@ -339,6 +342,31 @@ def decode_loop(torch, pf, wl, model, kv_host, store, ctx, gen=256, mutate=0.05)
             "ms_per_iteration": round(wall / len(its), 4),
             "identical_to_greedy_tokens": same}
         log(f"decode loop {name}: {out['modes'][name]}")
+    # the memory update (step 6) online: a store of the base sequences only;
+    # a greedy execution appends its own outputs and contexts, then the same
+    # task runs again with the controller and retrieves from that memory
+    st_on = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
+    base_keys = np.empty((T, pf.KEY_DIM), np.int8)
+    for a in range(0, T, 1 << 18):
+        b = min(T, a + (1 << 18))
+        base_keys[a:b] = synth.random_keys(b - a, synth.case_seed(wl, 11), first=a)
+    pf.pf_store_attach_keys(st_on, base_keys)
+    del base_keys
+    pf.pf_store_reserve(st_on, 4 * gen + 256, 8)
+    ctl_on = pf.pf_ctl_create(l_max=64, explore_every=16, lr=0.05, forget=0.98, prior_var=100.0)
+    for name, cl, lf in (("online_greedy_appending", None, 0),
+                         ("online_second_execution", ctl_on, 0)):
+        toks, its, _, wall = run(st_on, cl, lf, append=True)
+        same = int(np.argmax(toks != first)) if (toks != first).any() else gen
+        acc = [it["accepted"] for it in its]
+        out["modes"][name] = {
+            "tokens_per_s": round(sum(a + 1 for a in acc) / (wall * 1e-3), 1),
+            "iterations": len(its), "mean_l": round(float(np.mean([it["l"] for it in its])), 2),
+            "mean_accepted": round(float(np.mean(acc)), 2),
+            "ms_per_iteration": round(wall / len(its), 4),
+            "identical_to_greedy_tokens": same}
+        log(f"decode loop {name}: {out['modes'][name]}")
+    out["online_memory_appended_positions"] = pf.pf_store_appended(st_on)
     g = out["modes"]["greedy"]["tokens_per_s"]
     for v in out["modes"].values():
         v["speedup_vs_greedy"] = round(v["tokens_per_s"] / g, 3)

@@ -399,6 +399,54 @@ pf_status pf_prefill(pf_model *model, pf_kv_cache *kv, const int32_t *tokens_dev
                      int32_t chunk, float *logits_last_dev, pf_stream s);
 
 /* ------------------------------------------------------------------------ */
+/* Online memory update (Section 3.2, step 6; decoding-memory budget,       */
+/* Section 5.6)                                                             */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * After each decoding iteration the tokens it appended and the contexts that
+ * produced them join the decoding memory. The store (with keys attached)
+ * gets an append region: positions T .. T + capacity - 1 of its token and
+ * key arrays, in appended output sequences. The cosine lookup sees appended
+ * positions like built ones: eligible when the token matches and the
+ * position precedes its sequence's last position; the open sequence's last
+ * position is its newest token, so every append makes the previous one
+ * eligible. The n-gram lookup sees only built positions. A store with an
+ * append region ranks exactly like a store built from the same sequences
+ * (tests compare the two).
+ *
+ * pf_store_reserve: create the region (capacity positions, at most max_seqs
+ *   sequences); needs keys attached; once per store (pf_store_attach_keys
+ *   then fails with PF_ESTATE). Synchronises s.
+ * pf_store_begin_sequence: open a new, empty output sequence (the previous
+ *   one is closed); PF_ECAPACITY past max_seqs.
+ * pf_store_append: append *n_dev tokens (device int32, at most n_max) with
+ *   their keys (device int8 [n][256], 16-byte aligned) to the open sequence.
+ * pf_store_append_verified: append the last verify step's out_tokens[0 ..
+ *   accept_len] with the keys of the rows that produced them (rows path[j],
+ *   from the model's final-layer states; the projection as in
+ *   pf_verify_row_keys), device-side, with no host synchronisation.
+ * Both appends fail with PF_ESTATE without an open sequence and with
+ *   PF_ECAPACITY when the host's bound on appended positions (grown by n_max
+ *   or the verify rows per call, made exact by pf_store_appended) would pass
+ *   the capacity.
+ * pf_store_appended: synchronise s, return the appended positions.
+ * pf_store_compact: synchronise s and rebuild the store from its sequences
+ *   (built, then appended, in order), evicting the oldest sequences while
+ *   more than `budget` positions remain (0: no budget); the append region is
+ *   recreated empty with no open sequence. The store's size (pf_store_size)
+ *   then counts the kept positions.
+ */
+pf_status pf_store_reserve(pf_store *store, int64_t capacity, int32_t max_seqs, pf_stream s);
+pf_status pf_store_begin_sequence(pf_store *store, pf_stream s);
+pf_status pf_store_append(pf_store *store, const int32_t *tokens_dev, const int8_t *keys_dev,
+                          const int32_t *n_dev, int32_t n_max, pf_stream s);
+pf_status pf_store_append_verified(pf_store *store, const pf_model *model, const pf_keyproj *kp,
+                                   const pf_verify_result *res_dev, pf_stream s);
+pf_status pf_store_appended(pf_store *store, pf_stream s, int64_t *n_out);
+pf_status pf_store_compact(pf_store *store, int64_t budget, pf_stream s);
+
+/* ------------------------------------------------------------------------ */
 /* Proposal-length controller (Section 3.2, "Runtime-adaptive proposal-     */
 /* length controller", Eq. (1))                                             */
 /* ------------------------------------------------------------------------ */
@@ -479,7 +527,8 @@ typedef struct pf_iteration {
  * proposal, cap ctl's l_max, or l_fixed without a controller) -> the length
  * l: Eq. (1) through pf_ctl_choose, or min(l_fixed, retrieved length), or 0
  * when nothing is eligible -> pf_verify_step over l + 1 rows ->
- * pf_kv_commit (appends the accepted tokens and the bonus to ctx) ->
+ * pf_kv_commit (appends the accepted tokens and the bonus to ctx) -> with
+ * append != 0, pf_store_append_verified (the memory update of step 6) ->
  * pf_verify_query_key into q_dev (the next iteration's query) -> with a
  * controller, pf_ctl_observe(l, s, accepted, ms) (also for greedy passes,
  * which teach the latency fit T(0)). ctl: nullable. store must have keys
@@ -491,10 +540,10 @@ typedef struct pf_iteration {
  * of the calls it makes, PF_EINVAL for null pointers or l_fixed outside
  * 0..64.
  */
-pf_status pf_decode_iteration(pf_model *model, pf_kv_cache *kv, pf_context *ctx,
-                              const pf_store *store, const pf_keyproj *kp, pf_ctl *ctl,
-                              int32_t l_fixed, int8_t *q_dev, pf_draft *draft_dev,
-                              pf_verify_result *res_dev, pf_iteration *out, pf_stream s);
+pf_status pf_decode_iteration(pf_model *model, pf_kv_cache *kv, pf_context *ctx, pf_store *store,
+                              const pf_keyproj *kp, pf_ctl *ctl, int32_t l_fixed, int32_t append,
+                              int8_t *q_dev, pf_draft *draft_dev, pf_verify_result *res_dev,
+                              pf_iteration *out, pf_stream s);
 
 #ifdef __cplusplus
 }

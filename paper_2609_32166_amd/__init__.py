@@ -43,7 +43,8 @@ EXPORTED = ["pf_last_error", "pf_version", "pf_context_init", "pf_context_sync_b
             "pf_draft_lookup_cosine", "pf_verify_query_key", "pf_verify_row_keys",
             "pf_ctl_create", "pf_ctl_destroy", "pf_ctl_get_state", "pf_ctl_set_state",
             "pf_ctl_objective", "pf_ctl_choose", "pf_ctl_observe", "pf_decode_iteration",
-            "pf_kv_carry"]
+            "pf_kv_carry", "pf_store_reserve", "pf_store_begin_sequence", "pf_store_append",
+            "pf_store_append_verified", "pf_store_appended", "pf_store_compact"]
 
 PF_PROF_KINDS = 11
 PROF_NAMES = ["setup", "qkv", "qkv_post", "attn", "o_proj", "norm", "gate_up", "down",
@@ -130,7 +131,13 @@ def lib():
             "pf_ctl_objective": (i32, [vp, ctypes.c_double, i32, vp, vp]),
             "pf_ctl_choose": (i32, [vp, ctypes.c_double, i32, vp]),
             "pf_ctl_observe": (i32, [vp, i32, ctypes.c_double, i32, ctypes.c_double]),
-            "pf_decode_iteration": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp]),
+            "pf_decode_iteration": (i32, [vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]),
+            "pf_store_reserve": (i32, [vp, i64, i32, vp]),
+            "pf_store_begin_sequence": (i32, [vp, vp]),
+            "pf_store_append": (i32, [vp, vp, vp, vp, i32, vp]),
+            "pf_store_append_verified": (i32, [vp, vp, vp, vp, vp]),
+            "pf_store_appended": (i32, [vp, vp, vp]),
+            "pf_store_compact": (i32, [vp, i64, vp]),
             "pf_kv_carry": (i32, [vp, vp, i32, vp, vp, vp, vp]),
         }
         for name, (res, args) in sig.items():
@@ -218,6 +225,10 @@ def pf_store_build(tokens: np.ndarray, seq_offsets: np.ndarray, ngram: int, stre
     _check(lib().pf_store_build(tokens.ctypes.data, offs.ctypes.data, len(offs) - 1, int(ngram),
                                 _stream(stream), ctypes.byref(out)))
     return Store(out.value)
+
+
+def pf_store_size(store: "Store") -> int:
+    return int(lib().pf_store_size(store.h))
 
 
 def new_draft():
@@ -315,12 +326,12 @@ class pf_iteration(ctypes.Structure):
 
 def pf_decode_iteration(model: "Model", kv: "KVCache", ctx: "Context", store: "Store",
                         kp: "KeyProj", ctl: Optional[Controller], l_fixed: int, qkey, draft,
-                        result, stream=None) -> dict:
+                        result, append: bool = False, stream=None) -> dict:
     it = pf_iteration()
     _check(lib().pf_decode_iteration(model.h, ctypes.byref(kv.c), ctypes.byref(ctx.c), store.h,
                                      kp.h, ctl.h if ctl is not None else None, int(l_fixed),
-                                     qkey.data_ptr(), draft.data_ptr(), result.data_ptr(),
-                                     ctypes.byref(it), _stream(stream)))
+                                     int(bool(append)), qkey.data_ptr(), draft.data_ptr(),
+                                     result.data_ptr(), ctypes.byref(it), _stream(stream)))
     return {k: getattr(it, k) for k, _ in pf_iteration._fields_}
 
 
@@ -359,6 +370,35 @@ def pf_store_attach_keys(store: "Store", keys: np.ndarray, stream=None) -> None:
     keys = np.ascontiguousarray(keys, np.int8)
     assert keys.shape == (store.size, KEY_DIM)
     _check(lib().pf_store_attach_keys(store.h, keys.ctypes.data, _stream(stream)))
+
+
+def pf_store_reserve(store: "Store", capacity: int, max_seqs: int, stream=None) -> None:
+    _check(lib().pf_store_reserve(store.h, int(capacity), int(max_seqs), _stream(stream)))
+
+
+def pf_store_begin_sequence(store: "Store", stream=None) -> None:
+    _check(lib().pf_store_begin_sequence(store.h, _stream(stream)))
+
+
+def pf_store_append(store: "Store", tokens, keys, n_dev, n_max: int, stream=None) -> None:
+    _check(lib().pf_store_append(store.h, tokens.data_ptr(), keys.data_ptr(), n_dev.data_ptr(),
+                                 int(n_max), _stream(stream)))
+
+
+def pf_store_append_verified(store: "Store", model: "Model", kp: "KeyProj", result,
+                             stream=None) -> None:
+    _check(lib().pf_store_append_verified(store.h, model.h, kp.h, result.data_ptr(),
+                                          _stream(stream)))
+
+
+def pf_store_appended(store: "Store", stream=None) -> int:
+    n = ctypes.c_int64()
+    _check(lib().pf_store_appended(store.h, _stream(stream), ctypes.byref(n)))
+    return int(n.value)
+
+
+def pf_store_compact(store: "Store", budget: int = 0, stream=None) -> None:
+    _check(lib().pf_store_compact(store.h, int(budget), _stream(stream)))
 
 
 def pf_draft_lookup_cosine(store: "Store", ctx: Context, qkey, k_max: int, tree: bool, n_cand: int,

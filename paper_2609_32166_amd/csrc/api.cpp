@@ -261,8 +261,20 @@ static void store_free_keys(pf_store *S) {
   S->n_tok = 0;
 }
 
+static void store_free_log(pf_store *S) {
+  void *ptrs[] = {S->log_state, S->log_seq, S->log_nk, S->seq_end, S->row_keys};
+  for (void *p : ptrs)
+    if (p) (void)hipFree(p);
+  S->log_state = S->log_seq = S->log_nk = S->seq_end = nullptr;
+  S->row_keys = nullptr;
+  S->cap_log = S->max_log_seqs = 0;
+  S->log_host_bound = 0;
+  S->log_seqs_host = 0;
+}
+
 void pf_store_destroy(pf_store *S) {
   if (!S) return;
+  store_free_log(S);
   if (S->tokens) (void)hipFree(S->tokens);
   if (S->ent_pos) (void)hipFree(S->ent_pos);
   if (S->ent_rem) (void)hipFree(S->ent_rem);
@@ -351,6 +363,7 @@ pf_status pf_key_encode(const pf_keyproj *kp, const void *h, int32_t dtype, int6
 pf_status pf_store_attach_keys(pf_store *S, const int8_t *keys, pf_stream s) {
   if (!S) return fail(PF_EINVAL, "pf_store_attach_keys: null store");
   if (S->T > 0 && !keys) return fail(PF_EINVAL, "pf_store_attach_keys: null keys");
+  if (S->log_state) return fail(PF_ESTATE, "pf_store_attach_keys: the store has an append region");
   const int64_t T = S->T;
   // entries p < b(p), grouped by token, ascending p within a token
   int32_t n_tok = 1;
@@ -433,7 +446,215 @@ pf_status pf_draft_lookup_cosine(const pf_store *S, const pf_context *ctx, const
   a.part = S->cpart;
   a.part_elig = S->cpart_elig;
   a.draft = draft;
+  a.log_state = S->log_state;
+  a.log_seq = S->log_seq;
+  a.log_nk = S->log_nk;
+  a.seq_end = S->seq_end;
+  a.T_base = (int32_t)S->T;
   HIPCHK(launch_cos_lookup(a, st(s)));
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// online memory update: append region, appends, compaction
+// ---------------------------------------------------------------------------
+
+pf_status pf_store_reserve(pf_store *S, int64_t capacity, int32_t max_seqs, pf_stream s) {
+  if (!S) return fail(PF_EINVAL, "pf_store_reserve: null store");
+  if (!S->tok_off) return fail(PF_ESTATE, "pf_store_reserve: attach keys first");
+  if (S->log_state) return fail(PF_ESTATE, "pf_store_reserve: the store already has an append region");
+  if (capacity < 1 || max_seqs < 1 || S->T + capacity >= ((int64_t)1 << 31) ||
+      capacity > ((int64_t)1 << 28))
+    return fail(PF_EINVAL, "pf_store_reserve: capacity %lld / sequences %d out of range",
+                (long long)capacity, max_seqs);
+  const int64_t T = S->T, N = T + capacity;
+  int32_t *tokens = nullptr;
+  int8_t *keys = nullptr;
+  pf_status r = PF_OK;
+  if ((r = dev_alloc(&tokens, N * 4, nullptr))) return r;
+  if ((r = dev_alloc(&keys, N * PF_KEY_DIM, nullptr))) {
+    (void)hipFree(tokens);
+    return r;
+  }
+  hipStream_t hs = st(s);
+  hipError_t e = hipSuccess;
+  if (T) e = hipMemcpyAsync(tokens, S->tokens, T * 4, hipMemcpyDeviceToDevice, hs);
+  if (e == hipSuccess && T)
+    e = hipMemcpyAsync(keys, S->keys, T * PF_KEY_DIM, hipMemcpyDeviceToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) {
+    (void)hipFree(tokens);
+    (void)hipFree(keys);
+    return fail(PF_EHIP, "pf_store_reserve: copy failed: %s", hipGetErrorString(e));
+  }
+  (void)hipFree(S->tokens);
+  (void)hipFree(S->keys);
+  S->tokens = tokens;
+  S->keys = keys;
+  if ((r = dev_alloc(&S->log_state, 2 * 4, nullptr)) ||
+      (r = dev_alloc(&S->log_seq, capacity * 4, nullptr)) ||
+      (r = dev_alloc(&S->log_nk, capacity * 4, nullptr)) ||
+      (r = dev_alloc(&S->seq_end, (int64_t)max_seqs * 4, nullptr)) ||
+      (r = dev_alloc(&S->row_keys, (int64_t)kRowPad * PF_KEY_DIM, nullptr))) {
+    store_free_log(S);
+    return r;
+  }
+  e = hipMemsetAsync(S->log_state, 0, 2 * 4, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) {
+    store_free_log(S);
+    return fail(PF_EHIP, "pf_store_reserve: %s", hipGetErrorString(e));
+  }
+  S->cap_log = (int32_t)capacity;
+  S->max_log_seqs = max_seqs;
+  return ok();
+}
+
+pf_status pf_store_begin_sequence(pf_store *S, pf_stream s) {
+  if (!S) return fail(PF_EINVAL, "pf_store_begin_sequence: null store");
+  if (!S->log_state) return fail(PF_ESTATE, "pf_store_begin_sequence: no append region");
+  if (S->log_seqs_host >= S->max_log_seqs)
+    return fail(PF_ECAPACITY, "pf_store_begin_sequence: %d sequences already opened",
+                S->log_seqs_host);
+  HIPCHK(launch_store_begin(S->log_state, S->seq_end, (int32_t)S->T, st(s)));
+  ++S->log_seqs_host;
+  return ok();
+}
+
+static pf_status append_check(const pf_store *S, int32_t n_max, const char *fn) {
+  if (!S->log_state) return fail(PF_ESTATE, "%s: no append region", fn);
+  if (S->log_seqs_host < 1) return fail(PF_ESTATE, "%s: no open sequence", fn);
+  if (S->log_host_bound + n_max > S->cap_log)
+    return fail(PF_ECAPACITY, "%s: appended bound %lld + %d > capacity %d", fn,
+                (long long)S->log_host_bound, n_max, S->cap_log);
+  return PF_OK;
+}
+
+pf_status pf_store_append(pf_store *S, const int32_t *tokens, const int8_t *keys,
+                          const int32_t *n_dev, int32_t n_max, pf_stream s) {
+  if (!S || !tokens || !keys || !n_dev) return fail(PF_EINVAL, "pf_store_append: null pointer");
+  if (n_max < 0) return fail(PF_EINVAL, "pf_store_append: n_max < 0");
+  if (pf_status r = append_check(S, n_max, "pf_store_append")) return r;
+  if (((uintptr_t)keys & 15) != 0) return fail(PF_EINVAL, "pf_store_append: keys not 16-byte aligned");
+  AppendArgs a{};
+  a.tokens = S->tokens;
+  a.keys = S->keys;
+  a.log_state = S->log_state;
+  a.log_seq = S->log_seq;
+  a.log_nk = S->log_nk;
+  a.seq_end = S->seq_end;
+  a.T_base = (int32_t)S->T;
+  a.cap = S->cap_log;
+  a.tok_src = tokens;
+  a.key_src = keys;
+  a.n_dev = n_dev;
+  a.n_max = n_max;
+  a.res = nullptr;
+  HIPCHK(launch_store_append(a, st(s)));
+  S->log_host_bound += n_max;
+  return ok();
+}
+
+pf_status pf_store_append_verified(pf_store *S, const pf_model *m, const pf_keyproj *kp,
+                                   const pf_verify_result *res, pf_stream s) {
+  if (!S || !m || !kp || !res) return fail(PF_EINVAL, "pf_store_append_verified: null pointer");
+  const int rows = m->last_rows;
+  if (rows < 1) return fail(PF_ESTATE, "pf_store_append_verified: no verify step yet");
+  if (pf_status r = append_check(S, rows, "pf_store_append_verified")) return r;
+  if (pf_status r = pf_verify_row_keys(m, kp, rows, S->row_keys, s)) return r;
+  AppendArgs a{};
+  a.tokens = S->tokens;
+  a.keys = S->keys;
+  a.log_state = S->log_state;
+  a.log_seq = S->log_seq;
+  a.log_nk = S->log_nk;
+  a.seq_end = S->seq_end;
+  a.T_base = (int32_t)S->T;
+  a.cap = S->cap_log;
+  a.key_src = S->row_keys;
+  a.n_max = rows;
+  a.res = res;
+  HIPCHK(launch_store_append(a, st(s)));
+  S->log_host_bound += rows;
+  return ok();
+}
+
+pf_status pf_store_appended(pf_store *S, pf_stream s, int64_t *n_out) {
+  if (!S || !n_out) return fail(PF_EINVAL, "pf_store_appended: null pointer");
+  *n_out = 0;
+  if (!S->log_state) return ok();
+  int32_t st2[2];
+  HIPCHK(hipMemcpyAsync(st2, S->log_state, 8, hipMemcpyDeviceToHost, st(s)));
+  HIPCHK(hipStreamSynchronize(st(s)));
+  S->log_host_bound = st2[0];
+  *n_out = st2[0];
+  return ok();
+}
+
+pf_status pf_store_compact(pf_store *S, int64_t budget, pf_stream s) {
+  if (!S) return fail(PF_EINVAL, "pf_store_compact: null store");
+  if (!S->tok_off) return fail(PF_ESTATE, "pf_store_compact: the store has no keys");
+  if (budget < 0) return fail(PF_EINVAL, "pf_store_compact: budget < 0");
+  hipStream_t hs = st(s);
+  const int64_t T = S->T;
+  int32_t lst[2] = {0, 0};
+  std::vector<int32_t> ends;
+  if (S->log_state) {
+    HIPCHK(hipMemcpyAsync(lst, S->log_state, 8, hipMemcpyDeviceToHost, hs));
+    HIPCHK(hipStreamSynchronize(hs));
+    ends.resize((size_t)std::max(lst[1], 0));
+    if (lst[1] > 0)
+      HIPCHK(hipMemcpyAsync(ends.data(), S->seq_end, (size_t)lst[1] * 4, hipMemcpyDeviceToHost, hs));
+  }
+  const int64_t N = T + lst[0];
+  std::vector<int32_t> tok((size_t)N);
+  std::vector<int8_t> keys((size_t)N * PF_KEY_DIM);
+  if (N) {
+    HIPCHK(hipMemcpyAsync(tok.data(), S->tokens, N * 4, hipMemcpyDeviceToHost, hs));
+    HIPCHK(hipMemcpyAsync(keys.data(), S->keys, N * PF_KEY_DIM, hipMemcpyDeviceToHost, hs));
+  }
+  HIPCHK(hipStreamSynchronize(hs));
+  // sequences in store order: the built ones, then the appended ones
+  std::vector<std::pair<int64_t, int64_t>> seqs;  // [start, end)
+  for (int64_t p = 0; p < T;) {
+    const int64_t e = (int64_t)S->h_last[p] + 1;
+    seqs.push_back({p, e});
+    p = e;
+  }
+  int64_t start = T;
+  for (int32_t q = 0; q < lst[1]; ++q) {
+    const int64_t e = (int64_t)ends[q] + 1;
+    if (e > start) seqs.push_back({start, e});
+    start = std::max(start, e);
+  }
+  // evict the oldest sequences while over the budget (0: no budget)
+  int64_t total = 0;
+  for (auto &q : seqs) total += q.second - q.first;
+  size_t first = 0;
+  while (budget > 0 && total > budget && first < seqs.size()) {
+    total -= seqs[first].second - seqs[first].first;
+    ++first;
+  }
+  std::vector<int32_t> ntok;
+  std::vector<int8_t> nkeys;
+  std::vector<int64_t> offs{0};
+  for (size_t i = first; i < seqs.size(); ++i) {
+    for (int64_t p = seqs[i].first; p < seqs[i].second; ++p) ntok.push_back(tok[(size_t)p]);
+    nkeys.insert(nkeys.end(), keys.begin() + seqs[i].first * PF_KEY_DIM,
+                 keys.begin() + seqs[i].second * PF_KEY_DIM);
+    offs.push_back((int64_t)ntok.size());
+  }
+  pf_store *R = nullptr;
+  if (pf_status r = pf_store_build(ntok.data(), offs.data(), (int64_t)offs.size() - 1, S->ngram, s, &R))
+    return r;
+  pf_status r = pf_store_attach_keys(R, nkeys.data(), s);
+  if (r == PF_OK && S->log_state) r = pf_store_reserve(R, S->cap_log, S->max_log_seqs, s);
+  if (r != PF_OK) {
+    pf_store_destroy(R);
+    return r;
+  }
+  std::swap(*S, *R);
+  pf_store_destroy(R);
   return ok();
 }
 
@@ -730,6 +951,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   const float eps = (float)c.rms_eps;
   uint64_t *rowmask = (uint64_t *)(m->rowinfo + kRowPad * 4);
 
+  m->last_rows = rows;
   StepArgs sa;
   sa.draft = draft;
   sa.res = res;

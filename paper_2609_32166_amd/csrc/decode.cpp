@@ -1,7 +1,8 @@
 // One decoding iteration of Section 3.2 driven from the host: the paper's
 // retrieval, the proposal-length choice of Eq. (1), single-pass verification
-// and the commit, then the next iteration's query key and the controller's
-// update from what was observed.
+// and the commit, optionally the memory update (the iteration's tokens and
+// their contexts appended to the store), then the next iteration's query key
+// and the controller's update from what was observed.
 //
 // The host needs two facts from the device per iteration (the retrieved
 // proposal before choosing its length, the accepted length after the step),
@@ -30,10 +31,10 @@ static_assert(sizeof(pf_draft) + sizeof(pf_verify_result) <= kStageBytes, "stage
 
 extern "C" {
 
-pf_status pf_decode_iteration(pf_model *m, pf_kv_cache *kv, pf_context *ctx,
-                              const pf_store *store, const pf_keyproj *kp, pf_ctl *ctl,
-                              int32_t l_fixed, int8_t *q_dev, pf_draft *draft_dev,
-                              pf_verify_result *res_dev, pf_iteration *out, pf_stream s) {
+pf_status pf_decode_iteration(pf_model *m, pf_kv_cache *kv, pf_context *ctx, pf_store *store,
+                              const pf_keyproj *kp, pf_ctl *ctl, int32_t l_fixed, int32_t append,
+                              int8_t *q_dev, pf_draft *draft_dev, pf_verify_result *res_dev,
+                              pf_iteration *out, pf_stream s) {
   const auto t0 = std::chrono::steady_clock::now();
   if (!m || !kv || !ctx || !store || !kp || !q_dev || !draft_dev || !res_dev || !out)
     return fail(PF_EINVAL, "pf_decode_iteration: null pointer");
@@ -67,6 +68,9 @@ pf_status pf_decode_iteration(pf_model *m, pf_kv_cache *kv, pf_context *ctx,
   const int rows = l + 1;
   if (pf_status e = pf_verify_step(m, kv, draft_dev, rows, 0, nullptr, res_dev, s)) return e;
   if (pf_status e = pf_kv_commit(kv, res_dev, ctx, s)) return e;
+  if (append) {
+    if (pf_status e = pf_store_append_verified(store, m, kp, res_dev, s)) return e;
+  }
   if (pf_status e = pf_verify_query_key(m, kp, res_dev, q_dev, s)) return e;
   DCHK(hipMemcpyAsync(r, res_dev, sizeof(pf_verify_result), hipMemcpyDeviceToHost, hs));
   DCHK(hipStreamSynchronize(hs));
@@ -76,6 +80,7 @@ pf_status pf_decode_iteration(pf_model *m, pf_kv_cache *kv, pf_context *ctx,
   const int grown = r->accept_len + 1;
   kv->host_bound -= rows - grown;
   ctx->host_bound -= rows - grown;
+  if (append) store->log_host_bound -= rows - grown;
 
   const double ms =
       std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();

@@ -304,8 +304,31 @@ struct CosArgs {
   int4 *part;                          // [kCosScanBlocks][PF_MAX_CAND] (dot, nk, len, pos)
   int32_t *part_elig;                  // [kCosScanBlocks]
   pf_draft *draft;
+  // append region (null log_state: none): entries T_base + i, i < log_state[0]
+  const int32_t *log_state;            // [0] appended positions, [1] sequences opened
+  const int32_t *log_seq, *log_nk;     // per appended position: sequence, key norm^2
+  const int32_t *seq_end;              // per appended sequence: its last position
+  int32_t T_base;
 };
 hipError_t launch_cos_lookup(const CosArgs &a, hipStream_t s);
+
+// append region updates (keys.hip). Open a sequence; append n tokens with
+// their keys to the open sequence: n = *n_dev (at most n_max) from
+// tok_src / key_src rows, or, with res, the verified iteration's
+// out_tokens[0..accept_len] with key rows res->path[j] of key_src.
+struct AppendArgs {
+  int32_t *tokens;                     // store tokens [T_base + cap]
+  int8_t *keys;                        // store keys [T_base + cap][kKeyDim]
+  int32_t *log_state, *log_seq, *log_nk, *seq_end;
+  int32_t T_base, cap;
+  const int32_t *tok_src;
+  const int8_t *key_src;
+  const int32_t *n_dev;
+  int32_t n_max;
+  const pf_verify_result *res;
+};
+hipError_t launch_store_begin(int32_t *log_state, int32_t *seq_end, int32_t T_base, hipStream_t s);
+hipError_t launch_store_append(const AppendArgs &a, hipStream_t s);
 // v[r][j] (fp64) of rows of h: plain [n][ld] rows, or rows of the packed
 // verify activations (ld = padded hidden); with sel, the single row
 // sel->path[sel->accept_len]. Rc: the projection chain-major (pf_keyproj).

@@ -239,8 +239,7 @@ __global__ __launch_bounds__(256) void k_cos_scan(CosArgs a) {
 #pragma unroll
   for (int c = 0; c < PF_MAX_CAND; ++c) top[c] = no_cand();
   int cnt = 0;
-  for (int i = e0 + blockIdx.x * 256 + tid; i < e1; i += kCosScanBlocks * 256) {
-    const int p = a.ent_pos[i];
+  auto consider = [&](int p, int nk, int rem) {
     const uint4 *kp = (const uint4 *)(a.keys + (int64_t)p * kKeyDim);
     int dot = 0;
 #pragma unroll
@@ -251,7 +250,7 @@ __global__ __launch_bounds__(256) void k_cos_scan(CosArgs a) {
       dot = __builtin_amdgcn_sdot4((int)kv.z, (int)qv.z, dot, false);
       dot = __builtin_amdgcn_sdot4((int)kv.w, (int)qv.w, dot, false);
     }
-    CosCand x{dot, a.ent_nk[i], min(a.k_max, a.ent_rem[i]), p};
+    CosCand x{dot, nk, min(a.k_max, rem), p};
     ++cnt;
     // insert into the sorted thread-local list
 #pragma unroll
@@ -261,6 +260,19 @@ __global__ __launch_bounds__(256) void k_cos_scan(CosArgs a) {
         top[c] = x;
         x = t;
       }
+    }
+  };
+  for (int i = e0 + blockIdx.x * 256 + tid; i < e1; i += kCosScanBlocks * 256)
+    consider(a.ent_pos[i], a.ent_nk[i], a.ent_rem[i]);
+  // appended positions: token match and p < b(p), b(p) the last position of
+  // p's sequence (the open sequence's grows with every append)
+  if (a.log_state && y >= 0) {
+    const int n_log = a.log_state[0];
+    for (int i = blockIdx.x * 256 + tid; i < n_log; i += kCosScanBlocks * 256) {
+      const int p = a.T_base + i;
+      if (a.tokens[p] != y) continue;
+      const int b = a.seq_end[a.log_seq[i]];
+      if (p < b) consider(p, a.log_nk[i], b - p);
     }
   }
 #pragma unroll
@@ -322,6 +334,59 @@ __global__ __launch_bounds__(256) void k_cos_reduce(CosArgs a) {
   d->n_eligible = selig[0] + selig[1] + selig[2] + selig[3];
   d->tree = a.tree;
   d->n_nodes = nn;
+}
+
+// open a sequence in the append region: it starts empty at the next
+// position (last position = start - 1 until something is appended)
+__global__ void k_store_begin(int32_t *log_state, int32_t *seq_end, int32_t T_base) {
+  if (threadIdx.x != 0) return;
+  const int sq = log_state[1];
+  seq_end[sq] = T_base + log_state[0] - 1;
+  log_state[1] = sq + 1;
+}
+
+// one block: append to the open sequence (the host keeps the region and the
+// sequence table large enough)
+__global__ __launch_bounds__(256) void k_store_append(AppendArgs a) {
+  const int tid = threadIdx.x;
+  const int len0 = a.log_state[0];
+  const int sq = a.log_state[1] - 1;
+  int n = a.res ? a.res->accept_len + 1 : *a.n_dev;
+  n = max(0, min(n, min(a.n_max, a.cap - len0)));
+  if (sq < 0) n = 0;  // no open sequence
+  for (int j = tid; j < n; j += blockDim.x) {
+    const int p = a.T_base + len0 + j;
+    const int row = a.res ? a.res->path[j] : j;
+    a.tokens[p] = a.res ? a.res->out_tokens[j] : a.tok_src[j];
+    const int4 *src = (const int4 *)(a.key_src + (int64_t)row * kKeyDim);
+    int4 *dst = (int4 *)(a.keys + (int64_t)p * kKeyDim);
+    int nk = 0;
+#pragma unroll
+    for (int w = 0; w < kKeyDim / 16; ++w) {
+      const int4 v = src[w];
+      dst[w] = v;
+      nk = __builtin_amdgcn_sdot4(v.x, v.x, nk, false);
+      nk = __builtin_amdgcn_sdot4(v.y, v.y, nk, false);
+      nk = __builtin_amdgcn_sdot4(v.z, v.z, nk, false);
+      nk = __builtin_amdgcn_sdot4(v.w, v.w, nk, false);
+    }
+    a.log_seq[len0 + j] = sq;
+    a.log_nk[len0 + j] = nk;
+  }
+  __syncthreads();
+  if (tid == 0 && n > 0) {
+    a.log_state[0] = len0 + n;
+    a.seq_end[sq] = a.T_base + len0 + n - 1;
+  }
+}
+
+hipError_t launch_store_begin(int32_t *log_state, int32_t *seq_end, int32_t T_base,
+                              hipStream_t s) {
+  return launch_k(k_store_begin, 1, 64, s, log_state, seq_end, T_base);
+}
+
+hipError_t launch_store_append(const AppendArgs &a, hipStream_t s) {
+  return launch_k(k_store_append, 1, 256, s, a);
 }
 
 hipError_t launch_cos_lookup(const CosArgs &a, hipStream_t s) {

@@ -177,6 +177,7 @@ struct pf_model {
   // pinned host staging of the decode iteration (draft and result copies),
   // allocated on its first use
   void *stage = nullptr;
+  int32_t last_rows = 0;  // rows of the last verify step
 };
 
 // proposal-length controller: parameters and estimator states
@@ -206,6 +207,16 @@ struct pf_store {
   // host copies kept for attaching keys: tokens and each position's
   // sequence-last position b(p)
   std::vector<int32_t> h_tokens, h_last;
+  // append region (pf_store_reserve): positions T .. T + cap_log - 1 of the
+  // token and key arrays, filled by appends to the open sequence
+  int32_t cap_log = 0, max_log_seqs = 0;
+  int32_t *log_state = nullptr;  // device [2]: appended positions, sequences opened
+  int32_t *log_seq = nullptr;    // [cap_log] sequence of each appended position
+  int32_t *log_nk = nullptr;     // [cap_log] squared key norm
+  int32_t *seq_end = nullptr;    // [max_log_seqs] last position of each appended sequence
+  int8_t *row_keys = nullptr;    // [kRowPad][PF_KEY_DIM] keys of a verify step's rows
+  int64_t log_host_bound = 0;    // host upper bound of log_state[0]
+  int32_t log_seqs_host = 0;     // sequences opened
 };
 
 struct pf_keyproj {
