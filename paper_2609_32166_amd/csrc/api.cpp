@@ -979,21 +979,25 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   const int per_wave = (int)(((int64_t)nq * row_groups * n_splits + slots - 1) / slots);
 
   for (int l = 0; l < L; ++l) {
-    // QKV projection (split-K partials)
-    GemmArgs g{};
-    g.W = (const char *)m->wqkv + (int64_t)l * m->pqkv.bytes();
-    g.W_bytes = m->pqkv.bytes();
-    g.KFr = m->pqkv.KFr;
-    g.NTtot = m->pqkv.NT;
-    g.X = m->xn;
-    g.ldx = Hp;
-    g.M = M;
-    g.splits = splits_for(partial_blocks(m->pqkv), m->pqkv.KFr);
-    g.out = m->part;
-    g.ldo = q + 2 * kvd;
-    PROF(1, launch_gemm(bf, EPI_PARTIAL, MT, g, hs));
-    PROF(2, launch_qkv_post(bf, m->part, g.splits, kRowPad, M, nq, nkv, hd, g.ldo, m->rope, kv->len,
-                            m->qb, q, kv->data, l, kv->capacity, hs));
+    // QKV projection, RoPE and the KV append in one kernel
+    QkvArgs qa{};
+    qa.W = (const char *)m->wqkv + (int64_t)l * m->pqkv.bytes();
+    qa.W_bytes = m->pqkv.bytes();
+    qa.KFr = m->pqkv.KFr;
+    qa.X = m->xn;
+    qa.ldx = Hp;
+    qa.M = M;
+    qa.nq = nq;
+    qa.nkv = nkv;
+    qa.hd = hd;
+    qa.rope = m->rope;
+    qa.kv_len = kv->len;
+    qa.qbuf = m->qb;
+    qa.ldq = q;
+    qa.cache = kv->data;
+    qa.layer = l;
+    qa.cap = kv->capacity;
+    PROF(1, launch_gemm_qkv(bf, MT, qa, hs));
     // attention
     AttnArgs at{};
     at.q = m->qb;

@@ -89,6 +89,25 @@ struct GemmArgs {
   int64_t ldlog;
 };
 
+// QKV projection with RoPE and the KV append fused (qkv.hip): one block per
+// pair of 16-column tiles half a head apart, K split over the block's waves
+struct QkvArgs {
+  const void *W;        // packed fused QKV weights of one layer
+  int64_t W_bytes, KFr;
+  const void *X;        // fragment-packed normalised rows
+  int64_t ldx;
+  int M;                // valid rows
+  int nq, nkv, hd;
+  const float *rope;    // [kRowPad][hd/2][2] cos, sin of each row's position
+  const int32_t *kv_len;
+  void *qbuf;           // [kRowPad][ldq] queries after RoPE
+  int64_t ldq;
+  void *cache;          // KV cache: keys at slot P + row, values transposed
+  int layer;
+  int64_t cap;
+};
+hipError_t launch_gemm_qkv(bool bf16, int mt, const QkvArgs &a, hipStream_t s);
+
 struct AttnArgs {
   const void *q;        // [kRowPad][ldq] queries after RoPE
   int64_t ldq;

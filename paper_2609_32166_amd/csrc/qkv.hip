@@ -1,0 +1,152 @@
+// QKV projection of the verify step with its epilogue in the same kernel:
+// the sums for a pair of 16-column tiles half a head apart are reduced
+// inside the block (its waves split K, added in a fixed order), rotated
+// (RoPE pairs dimension d with d + head_dim/2), and written where the next
+// kernels read them: queries row-major for the attention, keys and values
+// into the cache at slot P + row. No split-K partials and no separate
+// epilogue kernel.
+#include "kernels.h"
+
+namespace pf {
+
+namespace {
+
+// Eight waves per block for every row count: the K split, and so the order
+// of the sums, must not depend on the rows (a verify row reproduces the
+// single-row step bit for bit). Sixteen measured slower (3B 9.8 vs 7.7 us).
+constexpr int kQkvWaves = 8;
+template <int MT> constexpr int qkv_slots() { return 6; }
+
+template <typename T, int MT>
+__global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
+  constexpr int NW = kQkvWaves;
+  constexpr int kU = qkv_slots<MT>();  // fragment slots in flight per wave
+  constexpr int E = Elem<T>::E;
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+  const int half_tiles = a.hd / 32;  // 16-column tiles per rotation half
+  const int hh = blockIdx.x / half_tiles, jt = blockIdx.x % half_tiles;
+  const int64_t tA = (int64_t)hh * (a.hd / 16) + jt, tB = tA + half_tiles;
+
+  // this wave's k fragments (the whole K is split over the block's waves)
+  const int64_t f0 = wid * a.KFr / NW, f1 = (wid + 1) * a.KFr / NW;
+  const int64_t n = f1 - f0;
+  const rsrc_t wr = make_rsrc(a.W, (uint32_t)a.W_bytes);
+  const rsrc_t xr = make_rsrc(a.X, (uint32_t)(kRowPad * a.ldx * sizeof(T)));
+  const uint32_t wbase[2] = {(uint32_t)(((tA * a.KFr + f0) * 64 + lane) * 16),
+                             (uint32_t)(((tB * a.KFr + f0) * 64 + lane) * 16)};
+  uint32_t xbase[MT];
+  const int64_t xkfr = a.ldx / (4 * E);
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+    xbase[m] = m * 16 + (lane & 15) < a.M ? (uint32_t)(((m * xkfr + f0) * 64 + lane) * 16) : kOOB;
+
+  f32x4 acc[MT][2];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) acc[m][0] = acc[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint4 wv[kU][2], xv[kU][MT];
+  auto load = [&](int u, int64_t i) {
+    const bool in = i < n;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+      wv[u][t] = bload16_stream(wr, in ? wbase[t] + (uint32_t)(i * 1024) : kOOB);
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+      xv[u][m] = bload16(xr, in && xbase[m] != kOOB ? xbase[m] + (uint32_t)(i * 1024) : kOOB);
+  };
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    load(u, u);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int64_t i = 0; i < n; i += kU) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) acc[m][t] = mma<T>(wv[u][t], xv[u][m], acc[m][t]);
+      load(u, i + kU + u);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // fixed-order reduction over the waves, one row tile at a time
+  __shared__ f32x4 red[NW - 1][2][64];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    if (wid > 0) {
+      red[wid - 1][0][lane] = acc[m][0];
+      red[wid - 1][1][lane] = acc[m][1];
+    }
+    __syncthreads();
+    if (wid == 0) {
+#pragma unroll
+      for (int w = 0; w < NW - 1; ++w) {
+        acc[m][0] += red[w][0][lane];
+        acc[m][1] += red[w][1][lane];
+      }
+    }
+    __syncthreads();
+  }
+  if (wid != 0) return;
+
+  // lane holds D[col = tile*16 + 4q + i][row = m*16 + lane%16]
+  const int q4 = lane >> 4, half = a.hd / 2;
+  const int P = *a.kv_len;
+  const int64_t plane = a.cap * a.hd;
+  const int kind = hh < a.nq ? 0 : (hh < a.nq + a.nkv ? 1 : 2);  // query, key, value head
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int row = m * 16 + (lane & 15);
+    if (row >= a.M) continue;
+    const int64_t slot = P + row;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int d = jt * 16 + 4 * q4 + i;  // dimension in the first half
+      const float x = acc[m][0][i], y = acc[m][1][i];
+      if (kind == 2) {
+        T *vp = (T *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.nkv + (hh - a.nq - a.nkv)) * plane;
+        Elem<T>::store(vp, (int64_t)d * a.cap + slot, x);
+        Elem<T>::store(vp, (int64_t)(d + half) * a.cap + slot, y);
+        continue;
+      }
+      const float c = a.rope[((int64_t)row * half + d) * 2 + 0];
+      const float s = a.rope[((int64_t)row * half + d) * 2 + 1];
+      const float rx = x * c - y * s, ry = x * s + y * c;
+      if (kind == 0) {
+        T *qp = (T *)a.qbuf + (int64_t)row * a.ldq + (int64_t)hh * a.hd;
+        Elem<T>::store(qp, d, rx);
+        Elem<T>::store(qp, d + half, ry);
+      } else {
+        T *kp = (T *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.nkv + (hh - a.nq)) * plane +
+                slot * a.hd;
+        Elem<T>::store(kp, d, rx);
+        Elem<T>::store(kp, d + half, ry);
+      }
+    }
+  }
+}
+
+template <typename T>
+hipError_t launch_t(int mt, const QkvArgs &a, hipStream_t s) {
+  const unsigned blocks = (unsigned)((a.nq + 2 * a.nkv) * (a.hd / 32));
+  switch (mt) {
+    case 1: return launch_k(k_gemm_qkv<T, 1>, blocks, 64 * kQkvWaves, s, a);
+    case 2: return launch_k(k_gemm_qkv<T, 2>, blocks, 64 * kQkvWaves, s, a);
+    case 3: return launch_k(k_gemm_qkv<T, 3>, blocks, 64 * kQkvWaves, s, a);
+    case 4: return launch_k(k_gemm_qkv<T, 4>, blocks, 64 * kQkvWaves, s, a);
+    case 5: return launch_k(k_gemm_qkv<T, 5>, blocks, 64 * kQkvWaves, s, a);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm_qkv(bool bf16, int mt, const QkvArgs &a, hipStream_t s) {
+  if (a.hd % 32 != 0) return hipErrorInvalidValue;
+  PF_TRY(bf16 ? launch_t<bf16_t>(mt, a, s) : launch_t<float>(mt, a, s));
+  return hipGetLastError();
+}
+
+}  // namespace pf
