@@ -162,15 +162,82 @@ __global__ __launch_bounds__(256) void k_residual_norm(const float *part, int sp
   }
 }
 
+// The same for wide rows: a thread per four columns (up to 1024 threads),
+// every thread issuing the loads of sixteen partials before adding them in
+// split order.
+template <typename T>
+__global__ __launch_bounds__(1024) void k_residual_norm_wide(const float *part, int splits, int rowpad,
+                                                        int H, int64_t ldpart, const float *gain,
+                                                        float eps, float *x, T *xn, int64_t ldxn,
+                                                        int packed) {
+  constexpr int kB = 16;  // partial loads in flight per thread
+  const int m = blockIdx.x;
+  float4 *xr = (float4 *)(x + (int64_t)m * H);
+  const int H4 = H / 4;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < H4; c += blockDim.x) {
+    float4 acc = xr[c];
+    for (int sp = 0; sp < splits; sp += kB) {
+      float4 v[kB];
+#pragma unroll
+      for (int u = 0; u < kB; ++u)
+        if (sp + u < splits) v[u] = ((const float4 *)(part + ((int64_t)(sp + u) * rowpad + m) * ldpart))[c];
+#pragma unroll
+      for (int u = 0; u < kB; ++u) {
+        if (sp + u < splits) {
+          acc.x += v[u].x;
+          acc.y += v[u].y;
+          acc.z += v[u].z;
+          acc.w += v[u].w;
+        }
+      }
+    }
+    xr[c] = acc;
+    ss += acc.x * acc.x + acc.y * acc.y + acc.z * acc.z + acc.w * acc.w;
+  }
+  __shared__ float sh[16];
+  ss = wave_sum(ss);
+  const int nw = blockDim.x >> 6;
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  ss = 0.f;
+  for (int w = 0; w < nw; ++w) ss += sh[w];
+  const float inv = 1.0f / sqrtf(ss / (float)H + eps);
+  for (int c = threadIdx.x; c < H4; c += blockDim.x) {
+    float4 v = xr[c];
+    float4 g = ((const float4 *)gain)[c];
+    // four consecutive k stay inside one E-element chunk of the packed layout
+    T *out = xn + xn_index<T>(packed, m, 4 * c, ldxn);
+    Elem<T>::store(out, 0, v.x * inv * g.x);
+    Elem<T>::store(out, 1, v.y * inv * g.y);
+    Elem<T>::store(out, 2, v.z * inv * g.z);
+    Elem<T>::store(out, 3, v.w * inv * g.w);
+  }
+}
+
 hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
                                 int64_t ldpart, const float *gain, float eps, float *x, void *xn,
                                 int64_t ldxn, bool packed, hipStream_t s) {
+  // rows up to 2048 columns: 256 threads, eight partials in flight; wider
+  // rows: a thread per four columns (up to 1024), sixteen in flight
+  // (measured: 7B-wide rows 5.6 -> 3.9 us; the wide form was slower at 2048)
+  if (H <= 2048) {
+    if (bf16)
+      PF_TRY(launch_k(k_residual_norm<bf16_t>, M, 256, s, part, splits, rowpad, H, ldpart, gain,
+                      eps, x, (bf16_t *)xn, ldxn, (int)packed));
+    else
+      PF_TRY(launch_k(k_residual_norm<float>, M, 256, s, part, splits, rowpad, H, ldpart, gain,
+                      eps, x, (float *)xn, ldxn, (int)packed));
+    return hipGetLastError();
+  }
+  int threads = ((H / 4 + 63) / 64) * 64;
+  if (threads > 1024) threads = 1024;
   if (bf16)
-    PF_TRY(launch_k(k_residual_norm<bf16_t>, M, 256, s, part, splits, rowpad, H, ldpart, gain, eps, x,
-                    (bf16_t *)xn, ldxn, (int)packed));
+    PF_TRY(launch_k(k_residual_norm_wide<bf16_t>, M, threads, s, part, splits, rowpad, H, ldpart, gain,
+                    eps, x, (bf16_t *)xn, ldxn, (int)packed));
   else
-    PF_TRY(launch_k(k_residual_norm<float>, M, 256, s, part, splits, rowpad, H, ldpart, gain, eps, x,
-                    (float *)xn, ldxn, (int)packed));
+    PF_TRY(launch_k(k_residual_norm_wide<float>, M, threads, s, part, splits, rowpad, H, ldpart, gain,
+                    eps, x, (float *)xn, ldxn, (int)packed));
   return hipGetLastError();
 }
 
