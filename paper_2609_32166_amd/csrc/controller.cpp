@@ -17,6 +17,9 @@
 
 #include "pf_internal.h"
 
+static_assert(sizeof(pf_ctl_params) == 32, "pf_ctl_params layout");
+static_assert(sizeof(pf_ctl_state) == 168, "pf_ctl_state layout");
+
 namespace {
 
 using pf::fail;

@@ -13,6 +13,8 @@
 
 #include "pf_internal.h"
 
+static_assert(sizeof(pf_iteration) == 40, "pf_iteration layout");
+
 using pf::fail;
 using pf::ok;
 

@@ -43,6 +43,9 @@ def test_record_layouts_match_header():
     assert ctypes.sizeof(pf.pf_kv_cache) == 56
     assert ctypes.sizeof(pf.pf_context) == 32
     assert ctypes.sizeof(pf.pf_model_config) == 48
+    assert ctypes.sizeof(pf.pf_ctl_params) == 32
+    assert ctypes.sizeof(pf.pf_ctl_state) == 168
+    assert ctypes.sizeof(pf.pf_iteration) == 40
 
 
 def test_error_paths_without_gpu():
@@ -58,3 +61,8 @@ def test_error_paths_without_gpu():
                                ctypes.byref(out)) == pf.PF_EUNSUPPORTED
     assert lib.pf_verify_step(None, None, None, 9, 0, None, None, None) == pf.PF_EINVAL
     assert lib.pf_kv_commit(None, None, None, None) == pf.PF_EINVAL
+    assert lib.pf_kv_carry(None, None, 0, None, None, None, None) == pf.PF_EINVAL
+    assert lib.pf_store_reserve(None, 1, 1, None) == pf.PF_EINVAL
+    assert lib.pf_store_append_verified(None, None, None, None, None) == pf.PF_EINVAL
+    assert lib.pf_decode_iteration(*([None] * 6), 0, 0, *([None] * 5)) == pf.PF_EINVAL
+    assert lib.pf_ctl_create(None, ctypes.byref(out)) == pf.PF_EINVAL
