@@ -1253,6 +1253,11 @@ pf_status pf_kv_carry(pf_kv_cache *kv, const pf_model *m, int32_t n_spans, const
 
 constexpr int kPrefillSplits = 8;
 
+// bf16 chunks take the LDS-staged 32x32 kernel; fp32 the register-fed one
+static hipError_t prefill_gemm(bool bf, int epi, const BigGemmArgs &a, hipStream_t s) {
+  return bf ? launch_gemm_pre(epi, a, s) : launch_gemm_big(false, epi, a, s);
+}
+
 static pf_status prefill_alloc(pf_model *m, int64_t rows) {
   if (m->pre_rows >= rows) return PF_OK;
   prefill_free(m);
@@ -1333,7 +1338,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       g.M = rows;
       g.y = m->pre_y;
       g.ldy = q + 2 * kvd;
-      HIPCHK(launch_gemm_big(bf, BIG_STORE, g, hs));
+      HIPCHK(prefill_gemm(bf, BIG_STORE, g, hs));
       HIPCHK(launch_qkv_post(bf, m->pre_y, 1, R, rows, nq, nkv, hd, q + 2 * kvd, m->pre_rope,
                              kv->len, m->pre_qb, q, kv->data, l, kv->capacity, hs));
       AttnArgs at{};
@@ -1372,7 +1377,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       go.M = rows;
       go.y = m->pre_x;
       go.ldy = H;
-      HIPCHK(launch_gemm_big(bf, BIG_RESID, go, hs));
+      HIPCHK(prefill_gemm(bf, BIG_RESID, go, hs));
       HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, m->ffn_norm + (int64_t)l * H, eps,
                                   m->pre_x, m->pre_xn, Hp, false, hs));
       BigGemmArgs gg{};
@@ -1387,7 +1392,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       gg.act = m->pre_act;
       gg.ldact = Fp;
       gg.up_tile_off = F / 16;
-      HIPCHK(launch_gemm_big(bf, BIG_SWIGLU, gg, hs));
+      HIPCHK(prefill_gemm(bf, BIG_SWIGLU, gg, hs));
       BigGemmArgs gd{};
       gd.W = (const char *)m->wd + (int64_t)l * m->pd.bytes();
       gd.W_bytes = m->pd.bytes();
@@ -1399,7 +1404,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       gd.M = rows;
       gd.y = m->pre_x;
       gd.ldy = H;
-      HIPCHK(launch_gemm_big(bf, BIG_RESID, gd, hs));
+      HIPCHK(prefill_gemm(bf, BIG_RESID, gd, hs));
       const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
       HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, next_gain, eps, m->pre_x,
                                   m->pre_xn, Hp, false, hs));

@@ -190,6 +190,9 @@ struct BigGemmArgs {
   int64_t up_tile_off;  // BIG_SWIGLU: up tile index offset (F/16)
 };
 hipError_t launch_gemm_big(bool bf16, int epi, const BigGemmArgs &a, hipStream_t s);
+// bf16 prefill GEMM with LDS-staged operands and 32x32 matrix instructions
+// (prefill_gemm.hip); needs x_rows % 128 == 0 and ldx % 32 == 0
+hipError_t launch_gemm_pre(int epi, const BigGemmArgs &a, hipStream_t s);
 hipError_t launch_argmax_accept(const ArgmaxPart *amax, int nparts, int rows, int tree,
                                 const pf_draft *draft, int32_t *pred, pf_verify_result *res,
                                 hipStream_t s);
