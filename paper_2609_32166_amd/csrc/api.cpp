@@ -118,10 +118,11 @@ template <typename T> pf_status dev_alloc(T **p, int64_t bytes, int64_t *total) 
 
 void prefill_free(pf_model *m) {
   void *ptrs[] = {m->pre_x, m->pre_y, m->pre_rope, m->pre_apo, m->pre_apml, m->pre_xn,
-                  m->pre_qb, m->pre_attn, m->pre_act, m->pre_rowinfo, m->pre_status};
+                  m->pre_qb, m->pre_attn, m->pre_act, m->pre_rowinfo, m->pre_status,
+                  m->pre_part};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
-  m->pre_x = m->pre_y = m->pre_rope = m->pre_apo = m->pre_apml = nullptr;
+  m->pre_x = m->pre_y = m->pre_rope = m->pre_apo = m->pre_apml = m->pre_part = nullptr;
   m->pre_xn = m->pre_qb = m->pre_attn = m->pre_act = nullptr;
   m->pre_rowinfo = m->pre_status = nullptr;
   m->pre_rows = 0;
@@ -1258,6 +1259,17 @@ static hipError_t prefill_gemm(bool bf, int epi, const BigGemmArgs &a, hipStream
   return bf ? launch_gemm_pre(epi, a, s) : launch_gemm_big(false, epi, a, s);
 }
 
+// split-K factor of a bf16 prefill GEMM with a narrow output: enough blocks
+// for two per CU (about 512), at least eight stages (16 fragments) a split
+constexpr int kPreSplitsMax = 8;
+static int prefill_splits(int64_t n_tiles16, int64_t rows_pad, int64_t KFr) {
+  const int64_t blocks = ((n_tiles16 + 7) / 8) * (rows_pad / 128);
+  int64_t sp = (512 + blocks - 1) / blocks;
+  const int64_t cap = std::min<int64_t>(kPreSplitsMax, KFr / 16);
+  if (sp > cap) sp = cap;
+  return sp < 1 ? 1 : (int)sp;
+}
+
 static pf_status prefill_alloc(pf_model *m, int64_t rows) {
   if (m->pre_rows >= rows) return PF_OK;
   prefill_free(m);
@@ -1283,6 +1295,8 @@ static pf_status prefill_alloc(pf_model *m, int64_t rows) {
   PALLOC(m->pre_act, R * Fp * m->esz);
   PALLOC(m->pre_rowinfo, R * 4 * 4);
   PALLOC(m->pre_status, 64);
+  if (m->cfg.dtype == PF_DTYPE_BF16)
+    PALLOC(m->pre_part, (int64_t)kPreSplitsMax * R * std::max<int64_t>(q + 2 * kv, H) * 4);
 #undef PALLOC
   void *zero[] = {m->pre_xn, m->pre_qb, m->pre_attn, m->pre_act, m->pre_status};
   int64_t zb[] = {R * Hp * m->esz, R * q * m->esz, R * qp * m->esz, R * Fp * m->esz, 64};
@@ -1336,10 +1350,13 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       g.ldx = Hp;
       g.x_rows = R;
       g.M = rows;
-      g.y = m->pre_y;
       g.ldy = q + 2 * kvd;
+      // bf16: split-K partials, added by the epilogue kernel in split order
+      g.splits = bf ? prefill_splits(m->pqkv.NT, R, m->pqkv.KFr) : 1;
+      g.y = bf ? m->pre_part : m->pre_y;
+      g.ystride = (int64_t)R * g.ldy;
       HIPCHK(prefill_gemm(bf, BIG_STORE, g, hs));
-      HIPCHK(launch_qkv_post(bf, m->pre_y, 1, R, rows, nq, nkv, hd, q + 2 * kvd, m->pre_rope,
+      HIPCHK(launch_qkv_post(bf, g.y, g.splits, R, rows, nq, nkv, hd, q + 2 * kvd, m->pre_rope,
                              kv->len, m->pre_qb, q, kv->data, l, kv->capacity, hs));
       AttnArgs at{};
       at.q = m->pre_qb;
@@ -1375,11 +1392,21 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       go.ldx = qp;
       go.x_rows = R;
       go.M = rows;
-      go.y = m->pre_x;
       go.ldy = H;
-      HIPCHK(prefill_gemm(bf, BIG_RESID, go, hs));
-      HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, m->ffn_norm + (int64_t)l * H, eps,
-                                  m->pre_x, m->pre_xn, Hp, false, hs));
+      if (bf) {  // split-K partials; the norm kernel adds them to the residual
+        go.splits = prefill_splits(m->po.NT, R, m->po.KFr);
+        go.y = m->pre_part;
+        go.ystride = (int64_t)R * H;
+        HIPCHK(prefill_gemm(bf, BIG_STORE, go, hs));
+        HIPCHK(launch_residual_norm(bf, m->pre_part, go.splits, R, rows, H, H,
+                                    m->ffn_norm + (int64_t)l * H, eps, m->pre_x, m->pre_xn, Hp,
+                                    false, hs));
+      } else {
+        go.y = m->pre_x;
+        HIPCHK(prefill_gemm(bf, BIG_RESID, go, hs));
+        HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, m->ffn_norm + (int64_t)l * H,
+                                    eps, m->pre_x, m->pre_xn, Hp, false, hs));
+      }
       BigGemmArgs gg{};
       gg.W = (const char *)m->wgu + (int64_t)l * m->pgu.bytes();
       gg.W_bytes = m->pgu.bytes();
@@ -1402,12 +1429,21 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       gd.ldx = Fp;
       gd.x_rows = R;
       gd.M = rows;
-      gd.y = m->pre_x;
       gd.ldy = H;
-      HIPCHK(prefill_gemm(bf, BIG_RESID, gd, hs));
       const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
-      HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, next_gain, eps, m->pre_x,
-                                  m->pre_xn, Hp, false, hs));
+      if (bf) {
+        gd.splits = prefill_splits(m->pd.NT, R, m->pd.KFr);
+        gd.y = m->pre_part;
+        gd.ystride = (int64_t)R * H;
+        HIPCHK(prefill_gemm(bf, BIG_STORE, gd, hs));
+        HIPCHK(launch_residual_norm(bf, m->pre_part, gd.splits, R, rows, H, H, next_gain, eps,
+                                    m->pre_x, m->pre_xn, Hp, false, hs));
+      } else {
+        gd.y = m->pre_x;
+        HIPCHK(prefill_gemm(bf, BIG_RESID, gd, hs));
+        HIPCHK(launch_residual_norm(bf, nullptr, 0, R, rows, H, H, next_gain, eps, m->pre_x,
+                                    m->pre_xn, Hp, false, hs));
+      }
     }
     HIPCHK(launch_add_int(kv->len, rows, hs));
     if (c0 + rows == n && logits_last) {

@@ -188,6 +188,10 @@ struct BigGemmArgs {
   void *act;            // BIG_SWIGLU: act[m*ldact + n]
   int64_t ldact;
   int64_t up_tile_off;  // BIG_SWIGLU: up tile index offset (F/16)
+  // launch_gemm_pre, BIG_STORE only: split K over grid.z; split z stores its
+  // partial sums at y + z * ystride (0 or 1: no split)
+  int splits;
+  int64_t ystride;
 };
 hipError_t launch_gemm_big(bool bf16, int epi, const BigGemmArgs &a, hipStream_t s);
 // bf16 prefill GEMM with LDS-staged operands and 32x32 matrix instructions

@@ -174,6 +174,7 @@ struct pf_model {
         *pre_apml = nullptr;
   void *pre_xn = nullptr, *pre_qb = nullptr, *pre_attn = nullptr, *pre_act = nullptr;
   int32_t *pre_rowinfo = nullptr, *pre_status = nullptr;
+  float *pre_part = nullptr;  // split-K partial sums of the bf16 prefill GEMMs
   // pinned host staging of the decode iteration (draft and result copies),
   // allocated on its first use
   void *stage = nullptr;

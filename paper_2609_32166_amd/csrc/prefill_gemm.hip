@@ -4,10 +4,11 @@
 // 2 x 2 tiles of the 32 x 32 x 16 bf16 matrix instruction. Both operands are
 // staged through LDS, two k fragments (64 k) per stage, double-buffered:
 // the next stage's global loads are in flight while the current stage is
-// multiplied. W keeps the packed fragment layout in LDS (a lane's 16-byte
-// operand chunk is one contiguous read); X rows are stored with their
-// 16-byte chunks XOR-swizzled by row, so the 32 rows a matrix instruction
-// reads hit different banks.
+// multiplied. Narrow outputs split K over grid.z into partial sums that the
+// following reduction kernel adds in split order. W keeps the packed
+// fragment layout in LDS (a lane's 16-byte operand chunk is one contiguous
+// read); X rows are stored with their 16-byte chunks XOR-swizzled by row, so
+// the 32 rows a matrix instruction reads hit different banks.
 #include "kernels.h"
 
 namespace pf {
@@ -47,23 +48,29 @@ __global__ __launch_bounds__(256) void k_gemm_pre(BigGemmArgs a) {
     }
   }
   const int64_t row0 = (int64_t)blockIdx.y * 128;
+  // k fragments of this block's split (grid.z; one split without)
+  const int64_t S = a.splits > 1 ? a.splits : 1;
+  const int64_t kf_lo = blockIdx.z * a.KFr / S, kf_hi = (blockIdx.z + 1) * a.KFr / S;
+  float *const y = a.y + (S > 1 ? blockIdx.z * a.ystride : 0);
   const rsrc_t wr = make_rsrc(a.W, (uint32_t)a.W_bytes);
   const rsrc_t xr = make_rsrc(a.X, (uint32_t)(a.x_rows * a.ldx * 2));
 
   __shared__ uint4 lw[2][8][2][64];  // stage, slot, fragment in the stage, lane chunk
   __shared__ uint4 lx[2][128][8];    // stage, row, swizzled 16-byte chunk
-  const int64_t nst = (a.KFr + 1) / 2;
+  const int64_t nst = (kf_hi - kf_lo + 1) / 2;
 
   // global loads of one stage: four W and four X chunks per thread
   uint4 gw[4], gx[4];
   auto gload = [&](int64_t st) {
-    const int64_t kf0 = st * 2;
+    const int64_t kf0 = kf_lo + st * 2;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int idx = tid + 256 * r;
       const int frag = idx >> 6, ln = idx & 63;
       const int s = frag >> 1, kk = frag & 1;
-      const bool in = wvld[s] && kf0 + kk < a.KFr;
+      // fragments past the split's range load zeros (W), so the X chunks
+      // there add nothing
+      const bool in = wvld[s] && kf0 + kk < kf_hi;
       gw[r] = bload16(wr, in ? (uint32_t)(((wt[s] * a.KFr + kf0 + kk) * 64 + ln) * 16) : kOOB);
       const int row = idx >> 3, ch = idx & 7;
       const int64_t k = kf0 * 32 + ch * 8;
@@ -138,7 +145,7 @@ __global__ __launch_bounds__(256) void k_gemm_pre(BigGemmArgs a) {
           const int s = wave_slot(EPI, wn, g, i >> 4);
           if (!wvld[s]) continue;
           const int64_t col = wt[s] * 16 + (i & 15);
-          float4 *dst = (float4 *)(a.y + row * a.ldy + col);
+          float4 *dst = (float4 *)(y + row * a.ldy + col);
           float4 v = make_float4(acc[g][t][4 * q], acc[g][t][4 * q + 1], acc[g][t][4 * q + 2],
                                  acc[g][t][4 * q + 3]);
           if (EPI == BIG_RESID) {
@@ -159,12 +166,14 @@ __global__ __launch_bounds__(256) void k_gemm_pre(BigGemmArgs a) {
 
 hipError_t launch_gemm_pre(int epi, const BigGemmArgs &a, hipStream_t s) {
   if (a.x_rows % 128 != 0 || a.ldx % 32 != 0) return hipErrorInvalidValue;
+  if (a.splits > 1 && (epi != BIG_STORE || a.splits > a.KFr)) return hipErrorInvalidValue;
   const unsigned gy = (unsigned)((a.M + 127) / 128);
+  const unsigned gz = a.splits > 1 ? (unsigned)a.splits : 1u;
   if (epi == BIG_SWIGLU) {
     dim3 grid((unsigned)((a.up_tile_off + 3) / 4), gy);
     PF_TRY(launch_k(k_gemm_pre<BIG_SWIGLU>, grid, 256, s, a));
   } else {
-    dim3 grid((unsigned)((a.NTtot + 7) / 8), gy);
+    dim3 grid((unsigned)((a.NTtot + 7) / 8), gy, gz);
     if (epi == BIG_STORE)
       PF_TRY(launch_k(k_gemm_pre<BIG_STORE>, grid, 256, s, a));
     else
