@@ -1337,8 +1337,20 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
     HIPCHK(launch_embed_norm(bf, m->embed, m->pre_rowinfo, rows, H, m->attn_norm, eps, m->pre_x,
                              m->pre_xn, Hp, false, hs));
     const int64_t keys_max = kv->host_bound + c0 + rows;
-    int ck = (int)roundup((keys_max + kPrefillSplits - 1) / kPrefillSplits, 32);
-    if (ck < 128) ck = 128;
+    // key ranges: the staged kernel takes enough of them for about one
+    // (KV head, range, 32-row tile) block per CU; the other path a fixed 8
+    const bool staged = attn_prefill_supported(bf, hd, nq / nkv);
+    int ck;
+    if (staged) {
+      const int blocks = nkv * ((rows + 31) / 32);
+      int want = (m->wave_slots / 4 + blocks - 1) / blocks;
+      if (want > kPrefillSplits) want = kPrefillSplits;
+      ck = (int)roundup((keys_max + want - 1) / want, 64);
+      if (ck < 256) ck = 256;
+    } else {
+      ck = (int)roundup((keys_max + kPrefillSplits - 1) / kPrefillSplits, 32);
+      if (ck < 128) ck = 128;
+    }
     const int nsp = (int)((keys_max + ck - 1) / ck);
     for (int l = 0; l < L; ++l) {
       BigGemmArgs g{};
@@ -1382,7 +1394,10 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       at.part_ml = m->pre_apml;
       at.out = m->pre_attn;
       at.ldout = qp;
-      HIPCHK(launch_attn(bf, (rows + 15) / 16, at, hs));
+      if (staged)
+        HIPCHK(launch_attn_prefill(at, hs));
+      else
+        HIPCHK(launch_attn(bf, (rows + 15) / 16, at, hs));
       BigGemmArgs go{};
       go.W = (const char *)m->wo + (int64_t)l * m->po.bytes();
       go.W_bytes = m->po.bytes();

@@ -378,6 +378,235 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Prefill attention (bf16, head_dim 128, 4..8 query heads per KV head): a
+// chunk's rows all attend to the long reused prefix, so the work is a dense
+// contraction and K/V tiles are worth staging. One block per (KV head, key
+// range, 32-row query tile); its waves are the KV head's query heads, all on
+// the same 32 rows, so one LDS copy of each 64-key K and V^T tile serves the
+// whole group. Per wave and tile: S^T = K Q^T as two 32-key halves of eight
+// 32x32x16 products (K rows permuted so that each lane ends up with eight
+// consecutive keys of its query row per 16-key step, the B-operand layout of
+// the value product), the online softmax in fp32 with the reference-maximum
+// rescale of the verify kernel, then O^T += V^T P^T. Loads of the next tile
+// are in flight while the current one is multiplied. Each block writes one
+// partial per (row, head) for k_attn_combine.
+// ---------------------------------------------------------------------------
+
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ inline f32x16 mma32(const uint4 &a, const uint4 &b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Key (within a 32-key half tile) carried by row i of the score product's A
+// operand. The product leaves value v of lane l at output row
+// 8*(v/4) + 4*(l/32) + v%4; with this assignment that row holds key
+// 16*(v/8) + 8*(l/32) + v%8.
+__device__ inline int score_key(int i) {
+  const int g = i >> 3, half = (i >> 2) & 1, r = i & 3;
+  return 16 * (g >> 1) + 8 * half + 4 * (g & 1) + r;
+}
+
+constexpr int kPreKeys = 64;  // keys per staged tile
+
+}  // namespace
+
+__global__ __launch_bounds__(512) void k_attn_prefill(AttnArgs a) {
+  constexpr int HD = 128;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int nthr = blockDim.x;  // 64 * group, at least 256
+  const int r32 = lane & 31, hh = lane >> 5;
+  // blocks of one (KV head, key range) pair get ids of equal residue mod 8:
+  // they run on one XCD and share its L2 copy of the range's K/V
+  const int rtiles = (a.M + 31) / 32;
+  const int npairs = a.n_kv * a.n_splits;
+  const int b = blockIdx.x, rest = b >> 3;
+  const int t = rest % rtiles, p = (rest / rtiles) * 8 + (b & 7);
+  if (p >= npairs) return;
+  const int g = p / a.n_splits, sp = p % a.n_splits;
+  const int h = g * a.group + wid;
+  const int j0 = t * 32;
+
+  // query fragments: lane holds Q[row j0 + r32][16*ds + 8*hh .. +8]
+  uint4 qf[HD / 16];
+  {
+    const int jr = min(j0 + r32, a.rowpad - 1);
+    const bf16_t *qrow = (const bf16_t *)a.q + (int64_t)jr * a.ldq + h * HD + 8 * hh;
+#pragma unroll
+    for (int ds = 0; ds < HD / 16; ++ds) qf[ds] = *(const uint4 *)(qrow + 16 * ds);
+  }
+  const bf16_t *kplane = (const bf16_t *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.n_kv + g) * a.plane;
+  const bf16_t *vplane = (const bf16_t *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.n_kv + g) * a.plane;
+  const rsrc_t kr = make_rsrc(kplane, (uint32_t)(a.plane * 2));
+  const rsrc_t vr = make_rsrc(vplane, (uint32_t)(a.plane * 2));
+  const float sc = a.scale_log2;
+
+  // keys of this block: its range, cut at the last row's causal bound
+  const int P = *a.kv_len;
+  const int kend = P + a.M;
+  const int k_lo = sp * a.chunk_keys;
+  const int k_hi = min(min(k_lo + a.chunk_keys, P + min(j0 + 32, a.M)), kend);
+  const int ntiles = k_hi > k_lo ? (k_hi - k_lo + kPreKeys - 1) / kPreKeys : 0;
+
+  // staged tiles: keys [key][16-byte chunk ^ (key & 15)], values transposed
+  // [dim][chunk of 8 keys ^ ((dim / 2) & 7)]; both swizzles keep the 16
+  // lanes of an operand read on distinct banks
+  __shared__ uint4 lk[2][kPreKeys][HD / 8];
+  __shared__ uint4 lv[2][HD][kPreKeys / 8];
+  uint4 gk[4], gv[4];
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int idx = tid + r * nthr;
+      const bool in = idx < kPreKeys * HD / 8;
+      const int key = kt + (idx >> 4), c = idx & 15;
+      gk[r] = bload16(kr, in && key < kend ? (uint32_t)(((int64_t)key * HD + c * 8) * 2) : kOOB);
+      const int d = idx >> 3, k8 = kt + (idx & 7) * 8;
+      gv[r] = bload16(vr, in && k8 < kend ? (uint32_t)(((int64_t)d * a.cap + k8) * 2) : kOOB);
+    }
+  };
+  auto lstore = [&](int buf, int kt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int idx = tid + r * nthr;
+      if (idx < kPreKeys * HD / 8) {
+        const int key = idx >> 4, c = idx & 15;
+        lk[buf][key][c ^ (key & 15)] = gk[r];
+        const int d = idx >> 3, c8 = idx & 7, k8 = kt + c8 * 8;
+        // value columns past the cache end are zeroed (a zero probability
+        // must not meet an uninitialised NaN)
+        const uint4 v = k8 + 8 > kend ? keep_first<bf16_t>(gv[r], max(kend - k8, 0)) : gv[r];
+        lv[buf][d][c8 ^ ((d >> 1) & 7)] = v;
+      }
+    }
+  };
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 o[HD / 32];
+#pragma unroll
+  for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o[dt][v] = 0.f;
+  const int row = j0 + r32;
+  const int lim = min(P + row + 1, kend);  // keys visible to this lane's row
+  constexpr float kSlack = 8.f;
+
+  if (ntiles > 0) {
+    gload(k_lo);
+    lstore(0, k_lo);
+  }
+  __syncthreads();
+  for (int it = 0; it < ntiles; ++it) {
+    const int buf = it & 1, kt = k_lo + it * kPreKeys;
+    if (it + 1 < ntiles) gload(kt + kPreKeys);
+    f32x16 s[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[st][v] = 0.f;
+      const int kl = st * 32 + score_key(r32);
+#pragma unroll
+      for (int ds = 0; ds < HD / 16; ++ds)
+        s[st] = mma32(lk[buf][kl][(2 * ds + hh) ^ (kl & 15)], qf[ds], s[st]);
+    }
+    // lane value v of half st is key kt + 32*st + 16*(v/8) + 8*hh + v%8
+    if (kt + kPreKeys > P + j0 + 1) {  // some key past the first row's bound (uniform)
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kt + 32 * st + 16 * (v >> 3) + 8 * hh + (v & 7);
+          s[st][v] = key < lim ? s[st][v] : -INFINITY;
+        }
+    }
+    float cmax = s[0][0];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) cmax = fmaxf(cmax, s[st][v]);
+    {  // the row's other 32 keys sit in lane l ^ 32
+      auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(cmax), __float_as_uint(cmax), false,
+                                                false);
+      cmax = fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1]));
+    }
+    const bool grow = m_run == -INFINITY ? cmax > -INFINITY : (cmax - m_run) * sc > kSlack;
+    if (__any(grow)) {
+      const float m_new = grow ? fmaxf(m_run, cmax) : m_run;
+      const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * sc) : 1.f;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < HD / 32; ++dt) o[dt] *= alpha;
+      m_run = m_new;
+    }
+    const float msc = m_run == -INFINITY ? 0.f : m_run * sc;
+    uint4 pb[2][2];  // P^T operand of each 16-key step
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        float pv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          pv[e] = __builtin_amdgcn_exp2f(fmaf(s[st][8 * s2 + e], sc, -msc));
+          l_run += pv[e];
+        }
+        pb[st][s2] = pack_probs<bf16_t>(pv);
+      }
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int dt = 0; dt < HD / 32; ++dt) {
+          const int d = 32 * dt + r32, c = 4 * st + 2 * s2 + hh;
+          o[dt] = mma32(lv[buf][d][c ^ ((d >> 1) & 7)], pb[st][s2], o[dt]);
+        }
+    if (it + 1 < ntiles) lstore(buf ^ 1, kt + kPreKeys);
+    __syncthreads();
+  }
+
+  // partial of this key range: lane holds O^T[d = 32*dt + 8*(v/4) + 4*hh + v%4][row]
+  {
+    auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run), false,
+                                              false);
+    l_run = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+  }
+  if (row < a.M) {
+    const int64_t slot = ((int64_t)h * a.n_splits + sp) * a.rowpad + row;
+    float *po = a.part_o + slot * HD;
+#pragma unroll
+    for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        *(float4 *)(po + 32 * dt + 8 * q4 + 4 * hh) =
+            make_float4(o[dt][4 * q4], o[dt][4 * q4 + 1], o[dt][4 * q4 + 2], o[dt][4 * q4 + 3]);
+    if (hh == 0) {
+      a.part_ml[slot * 2 + 0] = m_run == -INFINITY ? -INFINITY : m_run * sc;
+      a.part_ml[slot * 2 + 1] = l_run;
+    }
+  }
+}
+
+bool attn_prefill_supported(bool bf16, int head_dim, int group) {
+  return bf16 && head_dim == 128 && group >= 4 && group <= 8;
+}
+
+hipError_t launch_attn_prefill(const AttnArgs &a, hipStream_t s) {
+  if (!attn_prefill_supported(true, a.head_dim, a.group) || a.chunk_keys % kPreKeys != 0 ||
+      a.M < 1 || a.plane * 2 >= (int64_t)1 << 31)
+    return hipErrorInvalidValue;
+  const int rtiles = (a.M + 31) / 32;
+  const int npairs = a.n_kv * a.n_splits;
+  dim3 grid(8 * ((npairs + 7) / 8) * rtiles);
+  PF_TRY(launch_k(k_attn_prefill, grid, dim3(64 * a.group), s, a));
+  PF_TRY(launch_k(k_attn_combine<bf16_t, 128>, dim3(a.M, a.n_kv * a.group), 64, s, a));
+  return hipGetLastError();
+}
+
 template <typename T, int HD>
 static hipError_t attn_t(int rt, const AttnArgs &a, hipStream_t s) {
   const int per = attn_tiles_per_wave(rt);

@@ -134,6 +134,11 @@ struct AttnArgs {
 };
 
 hipError_t launch_attn(bool bf16, int rt, const AttnArgs &a, hipStream_t s);
+// Prefill attention with LDS-staged K/V tiles shared by a KV head's query
+// heads (bf16, head_dim 128, 4..8 query heads per KV head; chunk_keys a
+// multiple of 64), followed by the partial combine.
+bool attn_prefill_supported(bool bf16, int head_dim, int group);
+hipError_t launch_attn_prefill(const AttnArgs &a, hipStream_t s);
 // Query tiles (16 rows) per attention wave for rt tiles, and the waves each
 // SIMD holds at that footprint: one or two tiles fit two waves per SIMD,
 // three tiles one; more tiles are spread over waves of three (five tiles)
