@@ -1259,12 +1259,13 @@ static hipError_t prefill_gemm(bool bf, int epi, const BigGemmArgs &a, hipStream
   return bf ? launch_gemm_pre(epi, a, s) : launch_gemm_big(false, epi, a, s);
 }
 
-// split-K factor of a bf16 prefill GEMM with a narrow output: enough blocks
-// for two per CU (about 512), at least eight stages (16 fragments) a split
+// split-K factor of a bf16 prefill GEMM with a narrow output: about one
+// block (256 W rows x 128 X rows) per CU, at least eight stages (16
+// fragments) a split
 constexpr int kPreSplitsMax = 8;
-static int prefill_splits(int64_t n_tiles16, int64_t rows_pad, int64_t KFr) {
-  const int64_t blocks = ((n_tiles16 + 7) / 8) * (rows_pad / 128);
-  int64_t sp = (512 + blocks - 1) / blocks;
+static int prefill_splits(int64_t n_tiles16, int64_t rows_pad, int64_t KFr, int cus) {
+  const int64_t blocks = ((n_tiles16 + 15) / 16) * (rows_pad / 128);
+  int64_t sp = cus / blocks;
   const int64_t cap = std::min<int64_t>(kPreSplitsMax, KFr / 16);
   if (sp > cap) sp = cap;
   return sp < 1 ? 1 : (int)sp;
@@ -1364,7 +1365,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       g.M = rows;
       g.ldy = q + 2 * kvd;
       // bf16: split-K partials, added by the epilogue kernel in split order
-      g.splits = bf ? prefill_splits(m->pqkv.NT, R, m->pqkv.KFr) : 1;
+      g.splits = bf ? prefill_splits(m->pqkv.NT, R, m->pqkv.KFr, m->wave_slots / 4) : 1;
       g.y = bf ? m->pre_part : m->pre_y;
       g.ystride = (int64_t)R * g.ldy;
       HIPCHK(prefill_gemm(bf, BIG_STORE, g, hs));
@@ -1409,7 +1410,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       go.M = rows;
       go.ldy = H;
       if (bf) {  // split-K partials; the norm kernel adds them to the residual
-        go.splits = prefill_splits(m->po.NT, R, m->po.KFr);
+        go.splits = prefill_splits(m->po.NT, R, m->po.KFr, m->wave_slots / 4);
         go.y = m->pre_part;
         go.ystride = (int64_t)R * H;
         HIPCHK(prefill_gemm(bf, BIG_STORE, go, hs));
@@ -1447,7 +1448,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       gd.ldy = H;
       const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
       if (bf) {
-        gd.splits = prefill_splits(m->pd.NT, R, m->pd.KFr);
+        gd.splits = prefill_splits(m->pd.NT, R, m->pd.KFr, m->wave_slots / 4);
         gd.y = m->pre_part;
         gd.ystride = (int64_t)R * H;
         HIPCHK(prefill_gemm(bf, BIG_STORE, gd, hs));

@@ -199,7 +199,8 @@ struct BigGemmArgs {
   int64_t ystride;
 };
 hipError_t launch_gemm_big(bool bf16, int epi, const BigGemmArgs &a, hipStream_t s);
-// bf16 prefill GEMM with LDS-staged operands and 32x32 matrix instructions
+// bf16 prefill GEMM: W streamed into the matrix operands, X staged in LDS,
+// 32x32 matrix instructions
 // (prefill_gemm.hip); needs x_rows % 128 == 0 and ldx % 32 == 0
 hipError_t launch_gemm_pre(int epi, const BigGemmArgs &a, hipStream_t s);
 hipError_t launch_argmax_accept(const ArgmaxPart *amax, int nparts, int rows, int tree,
