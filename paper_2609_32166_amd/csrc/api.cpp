@@ -67,8 +67,11 @@ int splits_for(int64_t nblocks, int64_t KFr) {
   return (int)s;
 }
 
+// blocks of a partial-sum GEMM counted at two n tiles per block whatever the
+// row count, so the split factor (and with it every row's summation order)
+// does not depend on how many rows a step verifies
 int64_t partial_blocks(const Packed &p) {
-  int nt = gemm_tiles_per_block(EPI_PARTIAL);
+  const int nt = gemm_tiles_per_block(EPI_PARTIAL, 1);
   return (p.NT + nt - 1) / nt;
 }
 
@@ -1086,8 +1089,8 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   gl.logits = logits;
   gl.ldlog = V;
   PROF(8, launch_gemm(bf, EPI_ARGMAX, MT, gl, hs));
-  const int nparts = (int)((m->plm.NT + gemm_tiles_per_block(EPI_ARGMAX) - 1) /
-                           gemm_tiles_per_block(EPI_ARGMAX));
+  const int nparts = (int)((m->plm.NT + gemm_tiles_per_block(EPI_ARGMAX, MT) - 1) /
+                           gemm_tiles_per_block(EPI_ARGMAX, MT));
   PROF(9, launch_argmax_accept(m->amax, nparts, rows, tree, draft, m->pred, res, hs));
   kv->pending = rows;
   kv->pending_tree = tree;

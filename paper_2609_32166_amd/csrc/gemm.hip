@@ -68,16 +68,20 @@ hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers,
 // ---------------------------------------------------------------------------
 
 
-template <int EPI> struct EpiTiles;
-template <> struct EpiTiles<EPI_PARTIAL> { static constexpr int NT = 2; };
-template <> struct EpiTiles<EPI_SWIGLU> { static constexpr int NT = 2; };  // 1 gate + 1 up
-template <> struct EpiTiles<EPI_ARGMAX> { static constexpr int NT = 4; };
+// n tiles per block. With three 16-row X tiles the X fragments outweigh the
+// W fragments they meet, so a wave takes four W tiles (two gate/up pairs) to
+// reuse each X fragment twice as often (more tiles would cost occupancy).
+// Per tile the sums are the same: a tile's k range and its split of the
+// range over the waves do not depend on how many tiles share the block.
+template <int EPI, int MT> struct EpiTiles {
+  static constexpr int NT = EPI == EPI_ARGMAX ? 4 : MT == 3 ? 4 : 2;  // SwiGLU: gate, up pairs
+};
 
 __device__ inline float silu(float g) { return g / (1.0f + expf(-g)); }
 
 template <typename T, int MT, int EPI>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
-  constexpr int NT = EpiTiles<EPI>::NT;
+  constexpr int NT = EpiTiles<EPI, MT>::NT;
   constexpr int kU = NT >= 4 ? 4 : 6;  // fragment slots in flight per wave
   constexpr int E = Elem<T>::E;
   const int lane = threadIdx.x & 63;
@@ -88,9 +92,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   bool tv[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
-    if (EPI == EPI_SWIGLU) {
-      int64_t t = blockIdx.x;
-      tile[j] = j == 0 ? t : t + a.up_tile_off;
+    if (EPI == EPI_SWIGLU) {  // gate tiles first, then their up tiles
+      constexpr int NP = NT / 2;
+      const int64_t t = (int64_t)blockIdx.x * NP + j % NP;
+      tile[j] = j < NP ? t : t + a.up_tile_off;
       tv[j] = t < a.up_tile_off;
     } else {
       tile[j] = (int64_t)blockIdx.x * NT + j;
@@ -190,17 +195,21 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
       }
     }
   } else if (EPI == EPI_SWIGLU) {
-    if (!tv[0]) return;
+    constexpr int NP = NT / 2;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       int row = m * 16 + (lane & 15);
       if (row >= a.M) continue;
-      // act is the next GEMM's X: fragment-packed; the four columns stay in
-      // one E-element chunk
-      int64_t col = tile[0] * 16 + 4 * q;
-      T *dst = (T *)a.act + act_off<T>(row, col, a.ldact);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) Elem<T>::store(dst, i, silu(acc[m][0][i]) * acc[m][1][i]);
+      for (int p = 0; p < NP; ++p) {
+        if (!tv[p]) continue;
+        // act is the next GEMM's X: fragment-packed; the four columns stay in
+        // one E-element chunk
+        int64_t col = tile[p] * 16 + 4 * q;
+        T *dst = (T *)a.act + act_off<T>(row, col, a.ldact);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) Elem<T>::store(dst, i, silu(acc[m][p][i]) * acc[m][p + NP][i]);
+      }
     }
   } else {  // EPI_ARGMAX
 #pragma unroll
@@ -258,12 +267,11 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
 }
 
-int gemm_tiles_per_block(int epi) {
-  switch (epi) {
-    case EPI_PARTIAL: return EpiTiles<EPI_PARTIAL>::NT;
-    case EPI_SWIGLU: return 1;
-    default: return EpiTiles<EPI_ARGMAX>::NT;
-  }
+int gemm_tiles_per_block(int epi, int mt) {
+  // SwiGLU blocks are counted in gate tiles (each with its up tile)
+  if (epi == EPI_ARGMAX) return 4;
+  const int nt = mt == 3 ? 4 : 2;
+  return epi == EPI_SWIGLU ? nt / 2 : nt;
 }
 
 template <typename T, int EPI>
@@ -280,11 +288,8 @@ static hipError_t launch_t(int mt, const GemmArgs &a, dim3 grid, hipStream_t s) 
 }
 
 hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, hipStream_t s) {
-  int64_t nb;
-  if (epi == EPI_SWIGLU)
-    nb = a.up_tile_off;
-  else
-    nb = (a.NTtot + gemm_tiles_per_block(epi) - 1) / gemm_tiles_per_block(epi);
+  const int tpb = gemm_tiles_per_block(epi, mt);
+  const int64_t nb = ((epi == EPI_SWIGLU ? a.up_tile_off : a.NTtot) + tpb - 1) / tpb;
   dim3 grid((unsigned)nb, (unsigned)a.splits);
   if (bf16) {
     if (epi == EPI_PARTIAL) return launch_t<bf16_t, EPI_PARTIAL>(mt, a, grid, s);

@@ -373,7 +373,7 @@ hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers, in
                        bool bf16, const Packed &geom, void *dst, hipStream_t s);
 
 // Tiles per block along N for each epilogue.
-int gemm_tiles_per_block(int epi);
+int gemm_tiles_per_block(int epi, int mt);
 hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, hipStream_t s);
 
 }  // namespace pf

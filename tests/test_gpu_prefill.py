@@ -108,6 +108,24 @@ def test_verify_after_prefill(pf):
     assert out["kv_len"] == P + n + int(out["res"]["accept_len"]) + 1
 
 
+def test_prefill_3b_widths_two_layers(pf):
+    """3B-class widths (8 query heads per KV head, the widest group of the
+    staged prefill attention) at 2 layers: a 1000-token prefix, 300 new
+    tokens in 128-row chunks (the last one 44 rows)."""
+    wl = synth.WORKLOADS["3b"]
+    shape = wl.model.with_layers(2)
+    w, kv_host, toks, gpu, kv_new, logits = _prefill_case(pf, shape, synth.case_seed(wl, 5), 1000,
+                                                          300, 128)
+    om = oracle.Model(shape, w)
+    ref = oracle.prefill(om, kv_host, toks, 128)
+    r = ref["kv_new"]
+    e = np.abs(kv_new - r).max(axis=(2, 3, 4)) / np.abs(r).max(axis=(2, 3, 4))
+    assert e.max() <= tol_of(shape), e
+    assert rel_err_rows(logits[None], ref["logits_last"][None]).max() <= tol_of(shape)
+    del gpu
+    gc.collect()
+
+
 @pytest.mark.slow
 def test_prefill_7b_widths_two_layers(pf):
     """7B-class widths and the carry-forward lengths (6144 reused + 2048 new in
