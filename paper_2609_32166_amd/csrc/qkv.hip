@@ -41,6 +41,28 @@ __global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
   for (int m = 0; m < MT; ++m)
     xbase[m] = m * 16 + (lane & 15) < a.M ? (uint32_t)(((m * xkfr + f0) * 64 + lane) * 16) : kOOB;
 
+  // the epilogue's inputs (cache length, RoPE factors of wave 0's outputs)
+  // are read before the products, so their latency hides behind the loop
+  // (up to four row tiles; more would spill)
+  constexpr bool kEarly = MT <= 4;
+  const int q4 = lane >> 4, half = a.hd / 2;
+  const int kind = hh < a.nq ? 0 : (hh < a.nq + a.nkv ? 1 : 2);  // query, key, value head
+  int P = 0;
+  float rc[MT][4], rs[MT][4];
+  if (wid == 0) {
+    P = *a.kv_len;
+#pragma unroll
+    for (int m = 0; m < (kEarly ? MT : 0); ++m) {
+      const int row = min(m * 16 + (lane & 15), a.M - 1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = jt * 16 + 4 * q4 + i;
+        rc[m][i] = kind == 2 ? 1.f : a.rope[((int64_t)row * half + d) * 2 + 0];
+        rs[m][i] = kind == 2 ? 0.f : a.rope[((int64_t)row * half + d) * 2 + 1];
+      }
+    }
+  }
+
   f32x4 acc[MT][2];
 #pragma unroll
   for (int m = 0; m < MT; ++m) acc[m][0] = acc[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -92,10 +114,7 @@ __global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
   if (wid != 0) return;
 
   // lane holds D[col = tile*16 + 4q + i][row = m*16 + lane%16]
-  const int q4 = lane >> 4, half = a.hd / 2;
-  const int P = *a.kv_len;
   const int64_t plane = a.cap * a.hd;
-  const int kind = hh < a.nq ? 0 : (hh < a.nq + a.nkv ? 1 : 2);  // query, key, value head
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     const int row = m * 16 + (lane & 15);
@@ -111,9 +130,11 @@ __global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
         Elem<T>::store(vp, (int64_t)(d + half) * a.cap + slot, y);
         continue;
       }
-      const float c = a.rope[((int64_t)row * half + d) * 2 + 0];
-      const float s = a.rope[((int64_t)row * half + d) * 2 + 1];
-      const float rx = x * c - y * s, ry = x * s + y * c;
+      const float c = kEarly ? rc[m][i] : a.rope[((int64_t)row * half + d) * 2 + 0];
+      const float s = kEarly ? rs[m][i] : a.rope[((int64_t)row * half + d) * 2 + 1];
+      // explicit FMAs: every row-count instantiation rounds the rotation the
+      // same way (left to contraction, two instantiations may differ)
+      const float rx = fmaf(x, c, -(y * s)), ry = fmaf(x, s, y * c);
       if (kind == 0) {
         T *qp = (T *)a.qbuf + (int64_t)row * a.ldq + (int64_t)hh * a.hd;
         Elem<T>::store(qp, d, rx);

@@ -119,9 +119,20 @@ __global__ __launch_bounds__(256) void k_residual_norm(const float *part, int sp
                                                        int packed) {
   const int m = blockIdx.x;
   float4 *xr = (float4 *)(x + (int64_t)m * H);
-  const int H4 = H / 4;
+  const int H4 = H / 4;  // at most 512: two four-column chunks per thread
+  // the gains are read first and the summed row stays in registers, so no
+  // memory round trip follows the block-wide sum of squares
+  float4 keep[2], gk[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int c = threadIdx.x + 256 * r;
+    if (c < H4) gk[r] = ((const float4 *)gain)[c];
+  }
   float ss = 0.f;
-  for (int c = threadIdx.x; c < H4; c += 256) {
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int c = threadIdx.x + 256 * r;
+    if (c >= H4) continue;
     float4 acc = xr[c];
     int sp = 0;
     for (; sp + 8 <= splits; sp += 8) {
@@ -145,14 +156,17 @@ __global__ __launch_bounds__(256) void k_residual_norm(const float *part, int sp
       acc.w += v.w;
     }
     xr[c] = acc;
+    keep[r] = acc;
     ss += acc.x * acc.x + acc.y * acc.y + acc.z * acc.z + acc.w * acc.w;
   }
   __shared__ float sh[4];
   ss = block_sum256(ss, sh);
   const float inv = 1.0f / sqrtf(ss / (float)H + eps);
-  for (int c = threadIdx.x; c < H4; c += 256) {
-    float4 v = xr[c];
-    float4 g = ((const float4 *)gain)[c];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int c = threadIdx.x + 256 * r;
+    if (c >= H4) continue;
+    const float4 v = keep[r], g = gk[r];
     // four consecutive k stay inside one E-element chunk of the packed layout
     T *out = xn + xn_index<T>(packed, m, 4 * c, ldxn);
     Elem<T>::store(out, 0, v.x * inv * g.x);
@@ -171,11 +185,12 @@ __global__ __launch_bounds__(1024) void k_residual_norm_wide(const float *part, 
                                                         float eps, float *x, T *xn, int64_t ldxn,
                                                         int packed) {
   constexpr int kB = 16;  // partial loads in flight per thread
+  constexpr int kR = 2;   // four-column chunks per thread kept in registers
   const int m = blockIdx.x;
   float4 *xr = (float4 *)(x + (int64_t)m * H);
   const int H4 = H / 4;
-  float ss = 0.f;
-  for (int c = threadIdx.x; c < H4; c += blockDim.x) {
+  const int nt = blockDim.x;
+  auto reduce = [&](int c) {
     float4 acc = xr[c];
     for (int sp = 0; sp < splits; sp += kB) {
       float4 v[kB];
@@ -193,26 +208,50 @@ __global__ __launch_bounds__(1024) void k_residual_norm_wide(const float *part, 
       }
     }
     xr[c] = acc;
+    return acc;
+  };
+  // gains first, the summed row in registers (chunks past kR per thread,
+  // rows wider than 8192 columns, are read back)
+  float4 keep[kR], gk[kR];
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    const int c = threadIdx.x + nt * r;
+    if (c < H4) gk[r] = ((const float4 *)gain)[c];
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    const int c = threadIdx.x + nt * r;
+    if (c >= H4) continue;
+    keep[r] = reduce(c);
+    ss += keep[r].x * keep[r].x + keep[r].y * keep[r].y + keep[r].z * keep[r].z + keep[r].w * keep[r].w;
+  }
+  for (int c = threadIdx.x + nt * kR; c < H4; c += nt) {
+    const float4 acc = reduce(c);
     ss += acc.x * acc.x + acc.y * acc.y + acc.z * acc.z + acc.w * acc.w;
   }
   __shared__ float sh[16];
   ss = wave_sum(ss);
-  const int nw = blockDim.x >> 6;
+  const int nw = nt >> 6;
   if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = ss;
   __syncthreads();
   ss = 0.f;
   for (int w = 0; w < nw; ++w) ss += sh[w];
   const float inv = 1.0f / sqrtf(ss / (float)H + eps);
-  for (int c = threadIdx.x; c < H4; c += blockDim.x) {
-    float4 v = xr[c];
-    float4 g = ((const float4 *)gain)[c];
+  auto emit = [&](int c, float4 v, float4 g) {
     // four consecutive k stay inside one E-element chunk of the packed layout
     T *out = xn + xn_index<T>(packed, m, 4 * c, ldxn);
     Elem<T>::store(out, 0, v.x * inv * g.x);
     Elem<T>::store(out, 1, v.y * inv * g.y);
     Elem<T>::store(out, 2, v.z * inv * g.z);
     Elem<T>::store(out, 3, v.w * inv * g.w);
+  };
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    const int c = threadIdx.x + nt * r;
+    if (c < H4) emit(c, keep[r], gk[r]);
   }
+  for (int c = threadIdx.x + nt * kR; c < H4; c += nt) emit(c, xr[c], ((const float4 *)gain)[c]);
 }
 
 hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
