@@ -329,49 +329,65 @@ __global__ __launch_bounds__(64, WPE) void k_attn(AttnArgs a) {
 }
 
 // Merge the key-range partials of one (row, head) and round the result:
-// lane s reads split s's (max, sum); the output sum over splits keeps eight
-// loads in flight per lane.
+// lane s reads split s's (max, sum). The (max, sum) pairs and the first 16
+// splits' outputs are loaded before anything waits (they do not depend on
+// the cache length, which only decides how many splits count), so the
+// kernel pays one memory round trip for up to 16 splits; further splits
+// follow eight at a time. Splits are added in index order.
 template <typename T, int HD>
 __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
+  constexpr int NB = 16, NC = HD / 64;
   const int j = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const float *pml = a.part_ml + ((int64_t)h * a.n_splits * a.rowpad) * 2;
   const float *po = a.part_o + ((int64_t)h * a.n_splits * a.rowpad) * HD;
-  const int P = *a.kv_len;
-  const int used = min(a.n_splits, (P + a.M + a.chunk_keys - 1) / a.chunk_keys);
-  float m = -INFINITY, l = 0.f;
-  if (lane < used) {
-    m = pml[((int64_t)lane * a.rowpad + j) * 2];
-    l = pml[((int64_t)lane * a.rowpad + j) * 2 + 1];
+  const int ns = a.n_splits;
+  float mv = -INFINITY, lv = 0.f;
+  if (lane < ns) {
+    mv = pml[((int64_t)lane * a.rowpad + j) * 2];
+    lv = pml[((int64_t)lane * a.rowpad + j) * 2 + 1];
   }
+  float v0[NB][NC];
+#pragma unroll
+  for (int u = 0; u < NB; ++u)
+#pragma unroll
+    for (int i = 0; i < NC; ++i)
+      v0[u][i] = u < ns ? po[((int64_t)u * a.rowpad + j) * HD + lane + 64 * i] : 0.f;
+  const int P = *a.kv_len;
+  const int used = min(ns, (P + a.M + a.chunk_keys - 1) / a.chunk_keys);
+  // splits past the used ones hold stale data: weight zero, and their
+  // outputs are skipped, not multiplied
+  const float m = lane < used ? mv : -INFINITY, l = lane < used ? lv : 0.f;
   const float mx = wave_max(m);
   const float w = m == -INFINITY ? 0.f : exp2f(m - mx);
   const float den = wave_sum(w * l);
   __shared__ float ws[64];
   ws[lane] = w;
   __syncthreads();
-  float acc[HD / 64];
+  float acc[NC];
 #pragma unroll
-  for (int i = 0; i < HD / 64; ++i) acc[i] = 0.f;
-  int s = 0;
+  for (int i = 0; i < NC; ++i) acc[i] = 0.f;
+#pragma unroll
+  for (int u = 0; u < NB; ++u)
+#pragma unroll
+    for (int i = 0; i < NC; ++i) acc[i] += u < used ? ws[u] * v0[u][i] : 0.f;
+  int s = NB;
   for (; s + 8 <= used; s += 8) {
-    float v[8][HD / 64];
+    float v[8][NC];
 #pragma unroll
     for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int i = 0; i < HD / 64; ++i)
-        v[u][i] = po[((int64_t)(s + u) * a.rowpad + j) * HD + lane + 64 * i];
+      for (int i = 0; i < NC; ++i) v[u][i] = po[((int64_t)(s + u) * a.rowpad + j) * HD + lane + 64 * i];
 #pragma unroll
     for (int u = 0; u < 8; ++u)
 #pragma unroll
-      for (int i = 0; i < HD / 64; ++i) acc[i] += ws[s + u] * v[u][i];
+      for (int i = 0; i < NC; ++i) acc[i] += ws[s + u] * v[u][i];
   }
   for (; s < used; ++s)
 #pragma unroll
-    for (int i = 0; i < HD / 64; ++i)
-      acc[i] += ws[s] * po[((int64_t)s * a.rowpad + j) * HD + lane + 64 * i];
+    for (int i = 0; i < NC; ++i) acc[i] += ws[s] * po[((int64_t)s * a.rowpad + j) * HD + lane + 64 * i];
   T *out = (T *)a.out;
 #pragma unroll
-  for (int i = 0; i < HD / 64; ++i) {
+  for (int i = 0; i < NC; ++i) {
     const int64_t k = h * HD + lane + 64 * i;
     Elem<T>::store(out, a.out_packed ? act_off<T>(j, k, a.ldout) : (int64_t)j * a.ldout + k,
                    acc[i] / den);
