@@ -14,8 +14,11 @@ namespace {
 // Eight waves per block for every row count: the K split, and so the order
 // of the sums, must not depend on the rows (a verify row reproduces the
 // single-row step bit for bit). Sixteen measured slower (3B 9.8 vs 7.7 us).
+// Fragment loads in flight per wave: eight up to two row tiles (a 3B wave's
+// whole range at once: 6.85 -> 6.33 us), six beyond (registers). The slot
+// count does not change the order in which a wave adds its fragments.
 constexpr int kQkvWaves = 8;
-template <int MT> constexpr int qkv_slots() { return 6; }
+template <int MT> constexpr int qkv_slots() { return MT <= 2 ? 8 : 6; }
 
 template <typename T, int MT>
 __global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
