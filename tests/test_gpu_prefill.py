@@ -14,6 +14,10 @@ from pfharness import Gpu, rel_err_rows, tol_of
 pytestmark = pytest.mark.gpu
 
 RAGGED = synth.ModelShape(2, 512, 8, 2, 128, 1360, 4000, 1e6, 1e-6, "bf16")
+# bf16 shapes outside the staged prefill attention (head_dim 128 with 4..8
+# query heads per KV head): two heads per KV head, and head_dim 64
+GROUP2 = synth.ModelShape(2, 512, 4, 2, 128, 1360, 4000, 1e6, 1e-6, "bf16")
+HD64 = synth.ModelShape(2, 512, 8, 2, 64, 1360, 4000, 1e4, 1e-6, "bf16")
 
 
 @pytest.fixture(scope="module")
@@ -55,7 +59,9 @@ def _prefill_case(pf, shape, seed, P, n, chunk, cap_extra=128):
     (RAGGED, 300, 200, 64),
     (RAGGED, 130, 77, 77),
     (synth.WORKLOADS["tiny"].model, 512, 100, 32),
-], ids=["bf16_chunks", "bf16_one_chunk", "f32_chunks"])
+    (GROUP2, 200, 150, 64),
+    (HD64, 200, 150, 64),
+], ids=["bf16_chunks", "bf16_one_chunk", "f32_chunks", "bf16_group2", "bf16_hd64"])
 def test_prefill_matches_oracle(pf, shape, P, n, chunk):
     seed = 4242 + n
     w, kv_host, toks, gpu, kv_new, logits = _prefill_case(pf, shape, seed, P, n, chunk)
