@@ -1343,13 +1343,15 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
     HIPCHK(launch_embed_norm(bf, m->embed, m->pre_rowinfo, rows, H, m->attn_norm, eps, m->pre_x,
                              m->pre_xn, Hp, false, hs));
     const int64_t keys_max = kv->host_bound + c0 + rows;
-    // key ranges: the staged kernel takes enough of them for about one
-    // (KV head, range, 32-row tile) block per CU; the other path a fixed 8
+    // key ranges: the staged kernel takes enough of them for about two of
+    // its blocks per CU; the other path a fixed 8
     const bool staged = attn_prefill_supported(bf, hd, nq / nkv);
     int ck;
     if (staged) {
-      const int blocks = nkv * ((rows + 31) / 32);
-      int want = (m->wave_slots / 4 + blocks - 1) / blocks;
+      // two four-wave blocks per CU; a KV head's query heads take one block
+      // per four
+      const int blocks = nkv * ((rows + 31) / 32) * ((nq / nkv + 3) / 4);
+      int want = (2 * (m->wave_slots / 4) + blocks - 1) / blocks;
       if (want > kPrefillSplits) want = kPrefillSplits;
       ck = (int)roundup((keys_max + want - 1) / want, 64);
       if (ck < 256) ck = 256;

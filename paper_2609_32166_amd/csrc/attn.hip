@@ -397,10 +397,11 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
 // ---------------------------------------------------------------------------
 // Prefill attention (bf16, head_dim 128, 4..8 query heads per KV head): a
 // chunk's rows all attend to the long reused prefix, so the work is a dense
-// contraction and K/V tiles are worth staging. One block per (KV head, key
-// range, 32-row query tile); its waves are the KV head's query heads, all on
-// the same 32 rows, so one LDS copy of each 64-key K and V^T tile serves the
-// whole group. Per wave and tile: S^T = K Q^T as two 32-key halves of eight
+// contraction and K/V tiles are worth staging. One block of four waves per
+// (KV head, key range, 32-row query tile, four of the KV head's query
+// heads); its waves are those query heads, all on the same 32 rows, so one
+// LDS copy of each 64-key K and V^T tile serves them. Two such blocks fit a
+// CU, one computing while the other waits for its tiles. Per wave and tile: S^T = K Q^T as two 32-key halves of eight
 // 32x32x16 products (K rows permuted so that each lane ends up with eight
 // consecutive keys of its query row per 16-key step, the B-operand layout of
 // the value product), the online softmax in fp32 with the reference-maximum
@@ -431,20 +432,26 @@ constexpr int kPreKeys = 64;  // keys per staged tile
 
 }  // namespace
 
-__global__ __launch_bounds__(512) void k_attn_prefill(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
   constexpr int HD = 128;
+  constexpr int nthr = 256;  // four waves: up to four of the KV head's query heads
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int nthr = blockDim.x;  // 64 * group, at least 256
   const int r32 = lane & 31, hh = lane >> 5;
   // blocks of one (KV head, key range) pair get ids of equal residue mod 8:
-  // they run on one XCD and share its L2 copy of the range's K/V
+  // they run on one XCD and share its L2 copy of the range's K/V. A KV head
+  // with more than four query heads takes two blocks per row tile, so two
+  // independent blocks share every CU.
   const int rtiles = (a.M + 31) / 32;
+  const int nsub = (a.group + 3) / 4;
   const int npairs = a.n_kv * a.n_splits;
   const int b = blockIdx.x, rest = b >> 3;
-  const int t = rest % rtiles, p = (rest / rtiles) * 8 + (b & 7);
+  const int t = rest % rtiles, sub = (rest / rtiles) % nsub;
+  const int p = (rest / rtiles / nsub) * 8 + (b & 7);
   if (p >= npairs) return;
   const int g = p / a.n_splits, sp = p % a.n_splits;
-  const int h = g * a.group + wid;
+  const int hl = sub * 4 + wid;        // query head within the group
+  const bool head = hl < a.group;      // a wave past the group only helps load
+  const int h = g * a.group + min(hl, a.group - 1);
   const int j0 = t * 32;
 
   // query fragments: lane holds Q[row j0 + r32][16*ds + 8*hh .. +8]
@@ -519,6 +526,7 @@ __global__ __launch_bounds__(512) void k_attn_prefill(AttnArgs a) {
   for (int it = 0; it < ntiles; ++it) {
     const int buf = it & 1, kt = k_lo + it * kPreKeys;
     if (it + 1 < ntiles) gload(kt + kPreKeys);
+    if (head) {
     f32x16 s[2];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
@@ -581,6 +589,7 @@ __global__ __launch_bounds__(512) void k_attn_prefill(AttnArgs a) {
           const int d = 32 * dt + r32, c = 4 * st + 2 * s2 + hh;
           o[dt] = mma32(lv[buf][d][c ^ ((d >> 1) & 7)], pb[st][s2], o[dt]);
         }
+    }
     if (it + 1 < ntiles) lstore(buf ^ 1, kt + kPreKeys);
     __syncthreads();
   }
@@ -591,7 +600,7 @@ __global__ __launch_bounds__(512) void k_attn_prefill(AttnArgs a) {
                                               false);
     l_run = __uint_as_float(x[0]) + __uint_as_float(x[1]);
   }
-  if (row < a.M) {
+  if (head && row < a.M) {
     const int64_t slot = ((int64_t)h * a.n_splits + sp) * a.rowpad + row;
     float *po = a.part_o + slot * HD;
 #pragma unroll
@@ -617,8 +626,9 @@ hipError_t launch_attn_prefill(const AttnArgs &a, hipStream_t s) {
     return hipErrorInvalidValue;
   const int rtiles = (a.M + 31) / 32;
   const int npairs = a.n_kv * a.n_splits;
-  dim3 grid(8 * ((npairs + 7) / 8) * rtiles);
-  PF_TRY(launch_k(k_attn_prefill, grid, dim3(64 * a.group), s, a));
+  const int nsub = (a.group + 3) / 4;
+  dim3 grid(8 * ((npairs + 7) / 8) * rtiles * nsub);
+  PF_TRY(launch_k(k_attn_prefill, grid, dim3(256), s, a));
   PF_TRY(launch_k(k_attn_combine<bf16_t, 128>, dim3(a.M, a.n_kv * a.group), 64, s, a));
   return hipGetLastError();
 }
