@@ -286,50 +286,72 @@ hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int ro
 // ---------------------------------------------------------------------------
 
 template <typename T>
-__global__ __launch_bounds__(64) void k_qkv_post(const float *part, int splits, int rowpad, int nq,
-                                                 int nkv,
-                                                 int hd, int64_t ldpart, const float *rope,
-                                                 const int32_t *kv_len, T *qbuf, int64_t ldq,
-                                                 T *cache, int layer, int64_t cap) {
-  const int m = blockIdx.x, hh = blockIdx.y;
-  const int half = hd / 2;
+__global__ __launch_bounds__(256) void k_qkv_post(const float *part, int splits, int rowpad, int M,
+                                                  int nq, int nkv, int hd, int64_t ldpart,
+                                                  const float *rope, const int32_t *kv_len,
+                                                  T *qbuf, int64_t ldq, T *cache, int layer,
+                                                  int64_t cap) {
+  // one block per (32-row tile, head): query and key heads are rotated and
+  // stored row-major, value heads go through LDS so that the transposed
+  // cache rows (32 consecutive slots per dimension) are written contiguously
+  const int j0 = blockIdx.x * 32, hh = blockIdx.y;
+  const int half = hd / 2, h4 = half / 4;
   const int P = *kv_len;
-  const int64_t slot = P + m;
   const int64_t plane = cap * hd;
-  auto col_sum = [&](int64_t c) {
-    float acc = 0.f;
-    int sp = 0;
-    for (; sp + 8 <= splits; sp += 8) {
-      float v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = part[((int64_t)(sp + u) * rowpad + m) * ldpart + c];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) acc += v[u];
+  // sum over the splits of four consecutive columns of one row
+  auto col_sum4 = [&](int row, int64_t c) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int sp = 0; sp < splits; ++sp) {
+      const float4 v = *(const float4 *)(part + ((int64_t)sp * rowpad + row) * ldpart + c);
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
     }
-    for (; sp < splits; ++sp) acc += part[((int64_t)sp * rowpad + m) * ldpart + c];
     return acc;
   };
-  const bool isq = hh < nq;
-  const int64_t c0 = isq ? (int64_t)hh * hd : (int64_t)nq * hd + (int64_t)(hh - nq) * hd;
-  for (int i = threadIdx.x; i < half; i += 64) {
-    float a = col_sum(c0 + i), b = col_sum(c0 + i + half);
-    float c = rope[((int64_t)m * half + i) * 2 + 0], s = rope[((int64_t)m * half + i) * 2 + 1];
-    float ra = a * c - b * s, rb = a * s + b * c;
-    if (isq) {
-      Elem<T>::store(qbuf, (int64_t)m * ldq + c0 + i, ra);
-      Elem<T>::store(qbuf, (int64_t)m * ldq + c0 + i + half, rb);
-    } else {
-      const int g = hh - nq;
-      T *kp = cache + ((int64_t)(layer * 2 + 0) * nkv + g) * plane + slot * hd;
-      Elem<T>::store(kp, i, ra);
-      Elem<T>::store(kp, i + half, rb);
+  if (hh < nq + nkv) {
+    const bool isq = hh < nq;
+    const int64_t c0 = (int64_t)hh * hd;  // keys follow the queries in the fused output
+    T *kp = isq ? nullptr : cache + ((int64_t)(layer * 2 + 0) * nkv + (hh - nq)) * plane;
+    for (int idx = threadIdx.x; idx < 32 * h4; idx += 256) {
+      const int r = idx / h4, i = 4 * (idx % h4);
+      const int row = j0 + r;
+      if (row >= M) continue;
+      const float4 a4 = col_sum4(row, c0 + i), b4 = col_sum4(row, c0 + i + half);
+      const float4 cs0 = *(const float4 *)(rope + ((int64_t)row * half + i) * 2);
+      const float4 cs1 = *(const float4 *)(rope + ((int64_t)row * half + i) * 2 + 4);
+      const float av[4] = {a4.x, a4.y, a4.z, a4.w}, bv[4] = {b4.x, b4.y, b4.z, b4.w};
+      const float cv[4] = {cs0.x, cs0.z, cs1.x, cs1.z}, sv[4] = {cs0.y, cs0.w, cs1.y, cs1.w};
+      T *dst = isq ? qbuf + (int64_t)row * ldq + c0 : kp + (int64_t)(P + row) * hd;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        Elem<T>::store(dst, i + u, fmaf(av[u], cv[u], -(bv[u] * sv[u])));
+        Elem<T>::store(dst, i + u + half, fmaf(av[u], sv[u], bv[u] * cv[u]));
+      }
     }
+    return;
   }
-  if (!isq) {
-    const int g = hh - nq;
-    const int64_t cv = (int64_t)nq * hd + (int64_t)nkv * hd + (int64_t)g * hd;
-    T *vp = cache + ((int64_t)(layer * 2 + 1) * nkv + g) * plane;
-    for (int i = threadIdx.x; i < hd; i += 64) Elem<T>::store(vp, (int64_t)i * cap + slot, col_sum(cv + i));
+  // value head: [32 rows][hd] summed into LDS, then written transposed
+  const int g = hh - nq - nkv;
+  const int64_t cv0 = (int64_t)(nq + nkv) * hd + (int64_t)g * hd;
+  __shared__ float tile[32][128 + 1];
+  const int d4 = hd / 4;
+  for (int idx = threadIdx.x; idx < 32 * d4; idx += 256) {
+    const int r = idx / d4, d = 4 * (idx % d4);
+    const int row = j0 + r;
+    const float4 v = row < M ? col_sum4(row, cv0 + d) : make_float4(0.f, 0.f, 0.f, 0.f);
+    tile[r][d] = v.x;
+    tile[r][d + 1] = v.y;
+    tile[r][d + 2] = v.z;
+    tile[r][d + 3] = v.w;
+  }
+  __syncthreads();
+  T *vp = cache + ((int64_t)(layer * 2 + 1) * nkv + g) * plane;
+  const int rows = min(32, M - j0);
+  for (int idx = threadIdx.x; idx < hd * 32; idx += 256) {
+    const int d = idx / 32, r = idx % 32;
+    if (r < rows) Elem<T>::store(vp, (int64_t)d * cap + P + j0 + r, tile[r][d]);
   }
 }
 
@@ -337,13 +359,14 @@ hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int rowpad,
                            int nkv, int hd, int64_t ldpart, const float *rope, const int32_t *kv_len,
                            void *qbuf, int64_t ldq, void *cache, int layer, int64_t cap,
                            hipStream_t s) {
-  dim3 grid(M, nq + nkv);
+  if (hd > 128 || hd % 8 != 0) return hipErrorInvalidValue;
+  dim3 grid((M + 31) / 32, nq + 2 * nkv);
   if (bf16)
-    PF_TRY(launch_k(k_qkv_post<bf16_t>, grid, 64, s, part, splits, rowpad, nq, nkv, hd, ldpart, rope, kv_len,
-                                           (bf16_t *)qbuf, ldq, (bf16_t *)cache, layer, cap));
+    PF_TRY(launch_k(k_qkv_post<bf16_t>, grid, 256, s, part, splits, rowpad, M, nq, nkv, hd, ldpart,
+                    rope, kv_len, (bf16_t *)qbuf, ldq, (bf16_t *)cache, layer, cap));
   else
-    PF_TRY(launch_k(k_qkv_post<float>, grid, 64, s, part, splits, rowpad, nq, nkv, hd, ldpart, rope, kv_len,
-                                          (float *)qbuf, ldq, (float *)cache, layer, cap));
+    PF_TRY(launch_k(k_qkv_post<float>, grid, 256, s, part, splits, rowpad, M, nq, nkv, hd, ldpart,
+                    rope, kv_len, (float *)qbuf, ldq, (float *)cache, layer, cap));
   return hipGetLastError();
 }
 
