@@ -275,6 +275,71 @@ def test_chained_steps_equal_greedy_decoding(pf, case):
     assert list(c.tokens()[len(ctx):]) == emitted
 
 
+def _poison_past_len(gpu, torch):
+    """Fill every cache slot at or past the committed length with NaN: keys
+    are [slot][head_dim] rows, values [head_dim][slot] columns."""
+    s = gpu.shape
+    n = int(gpu.kv.len.item())
+    cap = gpu.kv.data.numel() // (s.n_layers * 2 * s.n_kv_heads * s.head_dim *
+                                  (2 if s.dtype == "bf16" else 4))
+    dt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
+    planes = gpu.kv.data.view(dt).view(s.n_layers, 2, s.n_kv_heads, cap * s.head_dim)
+    planes[:, 0].view(s.n_layers, s.n_kv_heads, cap, s.head_dim)[:, :, n:, :] = float("nan")
+    planes[:, 1].view(s.n_layers, s.n_kv_heads, s.head_dim, cap)[:, :, :, n:] = float("nan")
+
+
+@pytest.mark.parametrize("shape_name,tree", [("tiny", False), ("tiny", True), ("ragged", False),
+                                             ("ragged", True)])
+def test_rejected_slots_poisoned_with_nan_do_not_leak(pf, shape_name, tree):
+    """Rollback correctness: after every commit, one of two identical caches
+    gets NaN in every slot past the committed length (the rejected drafts'
+    K/V and everything beyond). Chained steps on both give bit-identical
+    logits, accept decisions and committed K/V: no kernel reads a slot past
+    the length it was given, not even as a zero-weighted value."""
+    import torch
+    wl = TINY if shape_name == "tiny" else RAGGED_WL
+    shape = wl.model
+    seed = synth.case_seed(wl, 300 + int(tree))
+    w = synth.make_weights(shape, seed)
+    kv_host = synth.make_kv_prefix(shape, seed, wl.prefix)
+    om = oracle.Model(shape, w)
+    store = synth.make_store(wl, seed)
+    ctx, _ = synth.make_context(wl, seed, store, hit=True)
+    greedy = oracle.greedy_decode(om, kv_host, int(ctx[-1]), 24)["tokens"]
+    # the store holds pieces of the continuation (with a wrong token) so
+    # drafts are partly accepted and partly rolled back
+    g2 = greedy.copy()
+    g2[9] = (g2[9] + 1) % shape.vocab
+    store = store.append(np.concatenate([ctx[-3:], g2[:14]]))
+    store = store.append(np.concatenate([g2[5:7], (g2[7:15] + 3) % shape.vocab]))
+    cap = ((wl.prefix + 12 * 70 + 63) // 64) * 64 + 64
+    a = Gpu(shape, w, kv_host, wl.prefix, cap)
+    b = Gpu(shape, w, kv_host, wl.prefix, cap)
+    st = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
+    ca, cb = pf.Context(ctx, len(ctx) + 1200), pf.Context(ctx, len(ctx) + 1200)
+    rows = 49 if tree else wl.k_max + 1
+    la = torch.zeros(rows, shape.vocab, device="cuda")
+    lb = torch.zeros(rows, shape.vocab, device="cuda")
+    rejected = 0
+    for it in range(8):
+        for g, c, lg in ((a, ca, la), (b, cb, lb)):
+            pf.pf_draft_lookup(st, c, wl.k_max, tree, 4 if tree else 1, 48 if tree else 64, g.draft)
+            pf.pf_verify_step(g.model, g.kv, g.draft, rows, tree, lg, g.res)
+            pf.pf_kv_commit(g.kv, g.res, c)
+        torch.cuda.synchronize()
+        assert torch.equal(la, lb), it
+        ra, rb = pf.read_result(a.res), pf.read_result(b.res)
+        assert (ra["accept_len"], ra["bonus"]) == (rb["accept_len"], rb["bonus"])
+        d = pf.read_draft(a.draft)
+        rejected += int(d["n_nodes"]) - 1 - int(ra["accept_len"])
+        _poison_past_len(b, torch)
+    n = int(a.kv.len.item())
+    assert n == int(b.kv.len.item())
+    assert torch.equal(a.export(0, n), b.export(0, n))
+    assert not torch.isnan(lb).any()
+    assert rejected > 0, "no draft token was rolled back"
+
+
 # ----------------------------------------------------------------------------
 # bf16, several tiles and ragged tails
 # ----------------------------------------------------------------------------
