@@ -61,7 +61,9 @@ def _prefill_case(pf, shape, seed, P, n, chunk, cap_extra=128):
     (synth.WORKLOADS["tiny"].model, 512, 100, 32),
     (GROUP2, 200, 150, 64),
     (HD64, 200, 150, 64),
-], ids=["bf16_chunks", "bf16_one_chunk", "f32_chunks", "bf16_group2", "bf16_hd64"])
+    (RAGGED, 100, 5, 1),
+], ids=["bf16_chunks", "bf16_one_chunk", "f32_chunks", "bf16_group2", "bf16_hd64",
+        "bf16_single_rows"])
 def test_prefill_matches_oracle(pf, shape, P, n, chunk):
     seed = 4242 + n
     w, kv_host, toks, gpu, kv_new, logits = _prefill_case(pf, shape, seed, P, n, chunk)
