@@ -383,8 +383,9 @@ pf_status pf_kv_commit(pf_kv_cache *kv, const pf_verify_result *res_dev, pf_cont
  * keeps a prefix sets the length (pf_kv_set_len) to prefill the new tokens
  * between and after the carried spans. src, dst, len: host arrays; every
  * span must lie inside the capacity. Errors: PF_EINVAL (spans), PF_ESTATE (a
- * verify step not committed), PF_EUNSUPPORTED (head_dim > 256). Allocates
- * nothing, does not synchronise.
+ * verify step not committed), PF_EUNSUPPORTED (head_dim > 256, or one cache
+ * plane, capacity * head_dim elements, of 2 GiB or more). Allocates nothing,
+ * does not synchronise.
  */
 pf_status pf_kv_carry(pf_kv_cache *kv, const pf_model *model, int32_t n_spans, const int64_t *src,
                       const int64_t *dst, const int64_t *len, pf_stream s);
