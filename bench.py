@@ -75,38 +75,96 @@ def prefill_flops(wl) -> float:
     return linear + attn
 
 
-def cpu_baseline(wl, w, kv_host, draft, layers: int):
-    """The oracle's batched verify, timed on this host's cores, on a sample:
-    the first `layers` layers at full widths plus the full lm_head, same
-    prefix and rows. Scaled to GB/s with the sample's own algorithmic bytes."""
-    import oracle
-
-    shape = wl.model.with_layers(layers)
+def _first_layers(w, shape, layers: int):
     ws = dict(w)
     for k in ("wqkv", "wo", "wgu", "wd", "attn_norm", "ffn_norm"):
         ws[k] = w[k][:layers]
+    return shape.with_layers(layers), ws
+
+
+def _repeat(fn, seconds: float, max_runs: int):
+    """Runs fn until `seconds` of host time have been spent; mean seconds per run."""
+    runs, t0 = 0, time.perf_counter()
+    while True:
+        fn()
+        runs += 1
+        total = time.perf_counter() - t0
+        if total >= seconds or runs >= max_runs:
+            return total / runs, runs, total
+
+
+def cpu_baseline(wl, w, kv_host, draft, layers: int):
+    """The oracle's batched verify, timed on this host's cores, on a sample:
+    the first `layers` layers at full widths plus the full lm_head, same
+    prefix and rows. Scaled to GB/s with the sample's own algorithmic bytes.
+    Beside it, on the same sample: the K single-row greedy decodes that the
+    batched pass replaces (timed as a few decodes, times K), for the tiny
+    fp32 workload the batched verify on one thread, and for the carry-forward
+    workload the chunked prefill, timed on one layer and scaled."""
+    import oracle
+
+    shape, ws = _first_layers(w, wl.model, layers)
     kvs = kv_host[:layers]
     om = oracle.Model(shape, ws)
     # repeated until about ten seconds of host work have been timed
-    runs, t0 = 0, time.perf_counter()
-    while True:
-        oracle.verify_batched(om, kvs, draft, wl.rows, wl.tree, want_logits=False)
-        runs += 1
-        total = time.perf_counter() - t0
-        if total >= 10.0 or runs >= 50:
-            break
-    dt = total / runs
+    dt, runs, total = _repeat(
+        lambda: oracle.verify_batched(om, kvs, draft, wl.rows, wl.tree, want_logits=False), 10.0, 50)
     sample_wl = synth.Workload(wl.name, wl.index, shape, wl.prefix, wl.k_max, wl.ngram, wl.tree,
                                wl.n_cand, wl.max_nodes, wl.store_seqs, wl.store_len,
                                wl.store_tokens, wl.planted)
     nbytes = sample_wl.verify_bytes()
-    return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": f"{runs} batched verifies of {wl.rows} rows over P={wl.prefix} with the first "
-                      f"{layers} of {wl.model.n_layers} layers at full width plus the full "
-                      f"lm_head ({nbytes / 1e9:.2f} GB algorithmic each), {total:.1f} s in all, "
-                      f"{dt:.2f} s per verify",
-            "seconds": round(total, 2)}
+    out = {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.threads(),
+           "kind": "oracle",
+           "sample": f"{runs} batched verifies of {wl.rows} rows over P={wl.prefix} with the first "
+                     f"{layers} of {wl.model.n_layers} layers at full width plus the full "
+                     f"lm_head ({nbytes / 1e9:.2f} GB algorithmic each), {total:.1f} s in all, "
+                     f"{dt:.2f} s per verify",
+           "seconds": round(total, 2)}
+    # sequential definition: single-row greedy decodes at positions P, P+1, ...
+    first = int(draft["token"][0])
+    t1, n1, _ = _repeat(lambda: oracle.greedy_decode(om, kvs, first, 1), 3.0, 20)
+    out["sequential_decodes"] = {
+        "k": wl.k_max, "s_per_decode": round(t1, 4), "decodes_timed": n1,
+        "k_decodes_s": round(wl.k_max * t1, 3), "batched_verify_s": round(dt, 4),
+        "k_decodes_over_batched": round(wl.k_max * t1 / dt, 2),
+        "note": "same layer sample; K decodes timed as single decodes at position P, times K"}
+    if wl.model.dtype == "f32":
+        n = oracle.threads()
+        oracle.set_threads(1)
+        try:
+            d1, r1, _ = _repeat(
+                lambda: oracle.verify_batched(om, kvs, draft, wl.rows, wl.tree, want_logits=False),
+                3.0, 50)
+        finally:
+            oracle.set_threads(n)
+        out["one_thread"] = {"value": round(nbytes / d1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                             "s_per_verify": round(d1, 5), "runs": r1}
+    if wl.prefill_new:
+        out["prefill_scaled"] = cpu_prefill(wl, w, kv_host)
+    return out
+
+
+def cpu_prefill(wl, w, kv_host):
+    """The oracle's chunked prefill on the first layer, a short and a longer
+    run of new tokens after the reused prefix: the difference gives the host
+    time per new token and layer, scaled to every new token and layer."""
+    import oracle
+
+    shape, ws = _first_layers(w, wl.model, 1)
+    om = oracle.Model(shape, ws)
+    kvs = np.ascontiguousarray(kv_host[:1, :, :, :wl.prefill_reuse])
+    toks = synth.make_prefill_tokens(wl, synth.case_seed(wl, 0), 64)
+    ts = {}
+    for n in (16, 64):
+        t0 = time.perf_counter()
+        oracle.prefill(om, kvs, toks[:n], wl.prefill_chunk)
+        ts[n] = time.perf_counter() - t0
+    per = (ts[64] - ts[16]) / 48.0
+    full = per * wl.prefill_new * wl.model.n_layers
+    return {"s_per_token_layer": round(per, 5), "scaled_s": round(full, 1),
+            "sample": f"one layer at full width, 16 and 64 new tokens after {wl.prefill_reuse} "
+                      f"reused ({ts[16]:.2f} s, {ts[64]:.2f} s); the difference per token, scaled "
+                      f"to {wl.prefill_new} tokens x {wl.model.n_layers} layers (scaled, not run)"}
 
 
 def _capture(torch, fn):
