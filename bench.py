@@ -238,17 +238,31 @@ def phase_timings(torch, pf, wl, model, kv, st, c, ctx, draft, res, args, ms_ste
         pf.pf_kv_set_len(kv, wl.prefix)
         pf.pf_verify_step(model, kv, draft, wl.rows, wl.tree, None, res)
 
+    def verify_commit():
+        verify()
+        pf.pf_kv_commit(kv, res, None)
+
     lookup()
     t_lookup = _time_inner(torch, lookup)
     gv = _capture(torch, verify)
-    t_verify = _time_graph(torch, gv, 50)
     # the capture left a verify pending on the host side; commit it once
     pf.pf_kv_commit(kv, res, None)
+    gvc = _capture(torch, verify_commit)
+    # the commit (one kernel of a few us) is the difference of the two graphs;
+    # they alternate and each keeps its best round, since the difference is
+    # close to the spread of single rounds
+    tv, tvc = [], []
+    for _ in range(4):
+        tv.append(_time_graph(torch, gv, 50))
+        tvc.append(_time_graph(torch, gvc, 50))
+    t_verify = min(tv)
     out["phases_ms"] = {"lookup (context reset + lookup; 20 per graph)": round(t_lookup, 4),
                         "verify (length reset + verify)": round(t_verify, 4),
-                        "commit (+ launch overhead, step minus the two)":
-                            round(ms_step - t_lookup - t_verify, 4),
+                        "commit (verify + commit graph minus verify graph)":
+                            round(min(tvc) - t_verify, 4),
+                        "verify_round_spread": round(max(tv) - min(tv), 4),
                         "step": round(ms_step, 4)}
+    del gv, gvc
 
     def step_k(k):
         rows = k + 1
