@@ -80,6 +80,35 @@ def test_lookup_random_small_stores(pf, seed):
                 assert_same_draft(d, od, tree)
 
 
+@pytest.mark.parametrize("case", ["no_sequences", "only_empty", "shorter_than_n", "empty_between"])
+def test_lookup_degenerate_stores(pf, case):
+    """Stores with nothing to retrieve, or with empty sequences among real
+    ones: drafts bit-exact vs the oracle; a store without an eligible entry
+    gives the greedy step's draft (the current token alone)."""
+    rng = np.random.default_rng(900)
+    if case == "no_sequences":
+        lens = np.zeros(0, np.int64)
+    elif case == "only_empty":
+        lens = np.zeros(5, np.int64)
+    elif case == "shorter_than_n":
+        lens = np.array([1, 2, 0, 2, 1], np.int64)
+    else:
+        lens = np.array([0, 9, 0, 0, 12, 0, 7, 0], np.int64)
+    toks = rng.integers(0, 3, int(lens.sum())).astype(np.int32)
+    store = synth.Store(toks, np.concatenate([[0], np.cumsum(lens)]).astype(np.int64))
+    store_ngram[0] = 3
+    for k_max in (0, 4, 64):
+        for tree, n_cand, max_nodes in ((False, 1, 64), (True, 4, 48)):
+            for ctx in (np.array([1], np.int32), np.array([0, 1, 2, 0, 1], np.int32),
+                        toks[:5] if len(toks) >= 5 else np.array([2, 2, 2], np.int32)):
+                d = _gpu_lookup(pf, store, ctx, k_max, tree, n_cand, max_nodes)
+                od = oracle.lookup(store.tokens, store.seq_offsets, 3, ctx, k_max, n_cand=n_cand,
+                                   tree=tree, max_nodes=max_nodes)
+                assert_same_draft(d, od, tree)
+                if case != "empty_between":
+                    assert od["n_found"] == 0 and int(d["n_nodes"]) == 1
+
+
 @pytest.mark.parametrize("name", ["tiny", "3b", "3b_tree", "7b"])
 def test_lookup_workload_stores(pf, name):
     wl = synth.WORKLOADS[name]
