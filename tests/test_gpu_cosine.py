@@ -135,6 +135,27 @@ def test_cosine_lookup_ties_zero_query_and_misses(pf):
     _cos_case(pf, st2, tokens, offs, k2, np.array([5], np.int32), keys[0], 8, True, 4)
 
 
+@pytest.mark.parametrize("lens", [[], [0, 0, 0], [1, 1, 0, 1], [0, 3, 0, 0, 4, 0]],
+                         ids=["no_sequences", "only_empty", "single_tokens", "empty_between"])
+def test_cosine_lookup_degenerate_stores(pf, lens):
+    """Stores with no sequence, only empty ones, only one-token sequences
+    (no position has a successor) and empty sequences between real ones:
+    drafts bit-exact vs the oracle; nothing eligible gives the greedy draft."""
+    lens = np.array(lens, np.int64)
+    T = int(lens.sum())
+    tokens = (np.arange(T) % 3).astype(np.int32)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    keys = synth.random_keys(T, 62) if T else np.zeros((0, 256), np.int8)
+    st = pf.pf_store_build(tokens, offs, 1)
+    pf.pf_store_attach_keys(st, keys)
+    q = synth.random_keys(1, 63)[0]
+    for y in (0, 1, 2, 5):
+        for tree, n_cand in ((False, 1), (True, 4)):
+            d, od = _cos_case(pf, st, tokens, offs, keys, np.array([y], np.int32), q, 8, tree, n_cand)
+            if (lens < 2).all() or y == 5:
+                assert int(d["n_nodes"]) == 1 and od["n_found"] == 0
+
+
 def test_paper_boundary_example_gpu(pf):
     A, B, C, D, E = 10, 11, 12, 13, 14
     tokens = np.array([A, B, C, D, E], np.int32)
