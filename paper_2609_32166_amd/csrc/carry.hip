@@ -18,6 +18,38 @@ namespace pf {
 
 namespace {
 
+// Element e of a 16-byte chunk held in registers, read and written with
+// shifts and selects (indexing the chunk through a pointer would put it in
+// scratch memory). e is a compile-time constant after unrolling.
+__device__ inline uint32_t chunk_word(const uint4 &v, int w) {
+  return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+}
+__device__ inline void chunk_put_word(uint4 &v, int w, uint32_t x) {
+  if (w == 0) v.x = x;
+  else if (w == 1) v.y = x;
+  else if (w == 2) v.z = x;
+  else v.w = x;
+}
+template <typename T> struct Chunk;
+template <> struct Chunk<float> {
+  __device__ static float get(const uint4 &v, int e) { return __uint_as_float(chunk_word(v, e)); }
+  __device__ static void set(uint4 &v, int e, float f) { chunk_put_word(v, e, __float_as_uint(f)); }
+  __device__ static void put_raw(float *p, const uint32_t (&o)[4], int e) { p[0] = __uint_as_float(o[e]); }
+};
+template <> struct Chunk<bf16_t> {
+  __device__ static float get(const uint4 &v, int e) {
+    return bf16_to_f32((uint16_t)(chunk_word(v, e >> 1) >> (16 * (e & 1))));
+  }
+  __device__ static void set(uint4 &v, int e, float f) {
+    const int sh = 16 * (e & 1);
+    const uint32_t w = chunk_word(v, e >> 1);
+    chunk_put_word(v, e >> 1, (w & ~(0xFFFFu << sh)) | ((uint32_t)f32_to_bf16(f) << sh));
+  }
+  __device__ static void put_raw(bf16_t *p, const uint32_t (&o)[4], int e) {
+    p[0].bits = (uint16_t)(o[e >> 1] >> (16 * (e & 1)));
+  }
+};
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_kv_carry(CarryArgs a) {
   constexpr int VE = 16 / (int)sizeof(T);  // elements per 16-byte access
@@ -44,15 +76,13 @@ __global__ __launch_bounds__(256) void k_kv_carry(CarryArgs a) {
       const T *s = kp + (a.src + tok) * a.hd + grp * VE;
       T *d = kp + (a.dst + tok) * a.hd + grp * VE;
       const uint4 lo = *(const uint4 *)s, hi = *(const uint4 *)(s + h);
-      const T *x = (const T *)&lo, *y = (const T *)&hi;
-      uint4 olo, ohi;
-      T *ox = (T *)&olo, *oy = (T *)&ohi;
+      uint4 olo = lo, ohi = hi;
 #pragma unroll
       for (int e = 0; e < VE; ++e) {
         const int i = grp * VE + e;
-        const float xv = Elem<T>::load(x, e), yv = Elem<T>::load(y, e);
-        Elem<T>::store(ox, e, xv * cs[i] - yv * sn[i]);
-        Elem<T>::store(oy, e, xv * sn[i] + yv * cs[i]);
+        const float xv = Chunk<T>::get(lo, e), yv = Chunk<T>::get(hi, e);
+        Chunk<T>::set(olo, e, xv * cs[i] - yv * sn[i]);
+        Chunk<T>::set(ohi, e, xv * sn[i] + yv * cs[i]);
       }
       *(uint4 *)d = olo;
       *(uint4 *)(d + h) = ohi;
@@ -76,27 +106,27 @@ __global__ __launch_bounds__(256) void k_kv_carry(CarryArgs a) {
     const int64_t off = (int64_t)i * a.cap + a0;
     const uint4 A = bload16(vr, off >= 0 ? (uint32_t)(off * ESZ) : kOOB);
     const uint4 B = bload16(vr, off + VE >= 0 ? (uint32_t)((off + VE) * ESZ) : kOOB);
-    const uint32_t wv[8] = {A.x, A.y, A.z, A.w, B.x, B.y, B.z, B.w};
-    uint32_t o[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      uint32_t lo = 0, hi = 0;
-      switch (q) {  // uniform over the launch
-        case 0: lo = wv[k]; hi = wv[k + 1]; break;
-        case 1: lo = wv[k + 1]; hi = wv[k + 2]; break;
-        case 2: lo = wv[k + 2]; hi = wv[k + 3]; break;
-        default: lo = wv[k + 3]; hi = wv[k + 4]; break;
-      }
-      o[k] = bsh ? __builtin_amdgcn_alignbyte(hi, lo, bsh) : lo;
+    // source words q .. q + 4 of the two chunks, as named registers (an
+    // array indexed by q would be placed in scratch memory)
+    uint32_t w0, w1, w2, w3, w4;
+    switch (q) {  // uniform over the launch
+      case 0: w0 = A.x; w1 = A.y; w2 = A.z; w3 = A.w; w4 = B.x; break;
+      case 1: w0 = A.y; w1 = A.z; w2 = A.w; w3 = B.x; w4 = B.y; break;
+      case 2: w0 = A.z; w1 = A.w; w2 = B.x; w3 = B.y; w4 = B.z; break;
+      default: w0 = A.w; w1 = B.x; w2 = B.y; w3 = B.z; w4 = B.w; break;
     }
+    uint32_t o[4];
+    o[0] = bsh ? __builtin_amdgcn_alignbyte(w1, w0, bsh) : w0;
+    o[1] = bsh ? __builtin_amdgcn_alignbyte(w2, w1, bsh) : w1;
+    o[2] = bsh ? __builtin_amdgcn_alignbyte(w3, w2, bsh) : w2;
+    o[3] = bsh ? __builtin_amdgcn_alignbyte(w4, w3, bsh) : w3;
     T *drow = vp + (int64_t)i * a.cap;
     if (d0 >= a.dst && d0 + VE <= a.dst + a.n) {
       *(uint4 *)(drow + d0) = make_uint4(o[0], o[1], o[2], o[3]);
     } else {
-      const T *ov = (const T *)o;
 #pragma unroll
       for (int e = 0; e < VE; ++e)
-        if (d0 + e >= a.dst && d0 + e < a.dst + a.n) drow[d0 + e] = ov[e];
+        if (d0 + e >= a.dst && d0 + e < a.dst + a.n) Chunk<T>::put_raw(drow + d0 + e, o, e);
     }
   }
 }

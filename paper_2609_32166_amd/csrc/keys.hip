@@ -180,11 +180,15 @@ __device__ inline CosCand unpack_cand(int4 v) { return CosCand{v.x, v.y, v.z, v.
 // Block-wide selection of the best n_cand of the items[256 * NI] in LDS
 // (each a candidate or none), in rank order, into out[]. Tree reduction per
 // round over (item index) with the exact order; the winner is removed.
+// The rounds are unrolled to the largest candidate count so that out[] is
+// indexed by constants and stays in registers.
 template <int NI>
-__device__ int select_top(int4 *items, int n_cand, CosCand *out, int *wins) {
+__device__ int select_top(int4 *items, int n_cand, CosCand (&out)[PF_MAX_CAND], int *wins) {
   const int tid = threadIdx.x;
   int found = 0;
-  for (int r = 0; r < n_cand; ++r) {
+#pragma unroll
+  for (int r = 0; r < PF_MAX_CAND; ++r) {
+    if (r >= n_cand) break;  // uniform over the block
     // each thread's best of its NI items
     int bi = tid * NI;
     CosCand b = unpack_cand(items[bi]);
@@ -210,7 +214,8 @@ __device__ int select_top(int4 *items, int n_cand, CosCand *out, int *wins) {
     const CosCand best = unpack_cand(items[w]);
     __syncthreads();
     if (best.pos < 0) break;
-    out[found++] = best;
+    out[r] = best;  // r == found: every earlier round found one
+    found = r + 1;
     if (tid == 0) items[w] = pack_cand(no_cand());
     __syncthreads();
   }
