@@ -44,25 +44,26 @@ __global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
   for (int m = 0; m < MT; ++m)
     xbase[m] = m * 16 + (lane & 15) < a.M ? (uint32_t)(((m * xkfr + f0) * 64 + lane) * 16) : kOOB;
 
-  // the epilogue's inputs (cache length, RoPE factors of wave 0's outputs)
-  // are read before the products, so their latency hides behind the loop
-  // (up to four row tiles; more would spill)
-  constexpr bool kEarly = MT <= 4;
-  const int q4 = lane >> 4, half = a.hd / 2;
+  // Epilogue: thread t < 256 owns one (row, RoPE pair) of each row tile:
+  // queries and keys run along the dimension (row-major stores), values
+  // along the row (their cache rows are transposed). Its cache length and
+  // RoPE factors are read before the products, so their latency hides
+  // behind the loop.
+  const int half = a.hd / 2;
   const int kind = hh < a.nq ? 0 : (hh < a.nq + a.nkv ? 1 : 2);  // query, key, value head
+  const int et = threadIdx.x;
+  const int er = kind == 2 ? (et & 15) : (et >> 4) & 15;  // row within the tile
+  const int ec = kind == 2 ? (et >> 4) & 15 : (et & 15);  // column within the tile
+  const int ed = jt * 16 + ec;                             // dimension in the first half
   int P = 0;
-  float rc[MT][4], rs[MT][4];
-  if (wid == 0) {
+  float rc[MT], rs[MT];
+  if (et < 256) {
     P = *a.kv_len;
 #pragma unroll
-    for (int m = 0; m < (kEarly ? MT : 0); ++m) {
-      const int row = min(m * 16 + (lane & 15), a.M - 1);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = jt * 16 + 4 * q4 + i;
-        rc[m][i] = kind == 2 ? 1.f : a.rope[((int64_t)row * half + d) * 2 + 0];
-        rs[m][i] = kind == 2 ? 0.f : a.rope[((int64_t)row * half + d) * 2 + 1];
-      }
+    for (int m = 0; m < MT; ++m) {
+      const int row = min(m * 16 + er, a.M - 1);
+      rc[m] = kind == 2 ? 1.f : a.rope[((int64_t)row * half + ed) * 2 + 0];
+      rs[m] = kind == 2 ? 0.f : a.rope[((int64_t)row * half + ed) * 2 + 1];
     }
   }
 
@@ -96,59 +97,44 @@ __global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
     }
   }
 
-  // fixed-order reduction over the waves, one row tile at a time
-  __shared__ f32x4 red[NW - 1][2][64];
-#pragma unroll
-  for (int m = 0; m < MT; ++m) {
-    if (wid > 0) {
-      red[wid - 1][0][lane] = acc[m][0];
-      red[wid - 1][1][lane] = acc[m][1];
-    }
-    __syncthreads();
-    if (wid == 0) {
-#pragma unroll
-      for (int w = 0; w < NW - 1; ++w) {
-        acc[m][0] += red[w][0][lane];
-        acc[m][1] += red[w][1][lane];
-      }
-    }
-    __syncthreads();
-  }
-  if (wid != 0) return;
-
-  // lane holds D[col = tile*16 + 4q + i][row = m*16 + lane%16]
+  // fixed-order reduction over the waves, one row tile at a time: every wave
+  // writes its sums, then each epilogue thread adds its output's eight wave
+  // sums in wave order, rotates the pair and stores it
+  __shared__ f32x4 red[NW][2][64];
   const int64_t plane = a.cap * a.hd;
+  // lane of the MFMA output holding (row er, column ec), and its element
+  const int src_lane = er + 16 * (ec >> 2), src_i = ec & 3;
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
-    const int row = m * 16 + (lane & 15);
-    if (row >= a.M) continue;
-    const int64_t slot = P + row;
+    red[wid][0][lane] = acc[m][0];
+    red[wid][1][lane] = acc[m][1];
+    __syncthreads();
+    const int row = m * 16 + er;
+    if (et < 256 && row < a.M) {
+      float x = red[0][0][src_lane][src_i], y = red[0][1][src_lane][src_i];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int d = jt * 16 + 4 * q4 + i;  // dimension in the first half
-      const float x = acc[m][0][i], y = acc[m][1][i];
+      for (int w = 1; w < NW; ++w) {
+        x += red[w][0][src_lane][src_i];
+        y += red[w][1][src_lane][src_i];
+      }
+      const int64_t slot = P + row;
       if (kind == 2) {
         T *vp = (T *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.nkv + (hh - a.nq - a.nkv)) * plane;
-        Elem<T>::store(vp, (int64_t)d * a.cap + slot, x);
-        Elem<T>::store(vp, (int64_t)(d + half) * a.cap + slot, y);
-        continue;
-      }
-      const float c = kEarly ? rc[m][i] : a.rope[((int64_t)row * half + d) * 2 + 0];
-      const float s = kEarly ? rs[m][i] : a.rope[((int64_t)row * half + d) * 2 + 1];
-      // explicit FMAs: every row-count instantiation rounds the rotation the
-      // same way (left to contraction, two instantiations may differ)
-      const float rx = fmaf(x, c, -(y * s)), ry = fmaf(x, s, y * c);
-      if (kind == 0) {
-        T *qp = (T *)a.qbuf + (int64_t)row * a.ldq + (int64_t)hh * a.hd;
-        Elem<T>::store(qp, d, rx);
-        Elem<T>::store(qp, d + half, ry);
+        Elem<T>::store(vp, (int64_t)ed * a.cap + slot, x);
+        Elem<T>::store(vp, (int64_t)(ed + half) * a.cap + slot, y);
       } else {
-        T *kp = (T *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.nkv + (hh - a.nq)) * plane +
-                slot * a.hd;
-        Elem<T>::store(kp, d, rx);
-        Elem<T>::store(kp, d + half, ry);
+        const float c = rc[m], sn = rs[m];
+        // explicit FMAs: every row-count instantiation rounds the rotation the
+        // same way (left to contraction, two instantiations may differ)
+        const float rx = fmaf(x, c, -(y * sn)), ry = fmaf(x, sn, y * c);
+        T *dst = kind == 0 ? (T *)a.qbuf + (int64_t)row * a.ldq + (int64_t)hh * a.hd
+                           : (T *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.nkv + (hh - a.nq)) * plane +
+                                 slot * a.hd;
+        Elem<T>::store(dst, ed, rx);
+        Elem<T>::store(dst, ed + half, ry);
       }
     }
+    __syncthreads();
   }
 }
 
