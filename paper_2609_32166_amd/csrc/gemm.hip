@@ -162,7 +162,53 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     }
   }
 
-  // reduce the four waves' partial sums in LDS (fixed order: wave 0..3)
+  // lane holds D[n = tile*16 + 4*q + i][row = m*16 + lane%16], q = lane/16
+  const int q = lane >> 4;
+  if (EPI != EPI_ARGMAX) {
+    // every wave stores its partial sums; wave w then finishes the outputs
+    // w, w + 4, ... of the block, adding the four waves' sums in wave order
+    __shared__ f32x4 red[4][MT][NT][64];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) red[wid][m][j][lane] = acc[m][j];
+    __syncthreads();
+    auto sum4 = [&](int m, int j) {
+      f32x4 v = red[0][m][j][lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) v += red[w][m][j][lane];
+      return v;
+    };
+    if (EPI == EPI_PARTIAL) {
+#pragma unroll
+      for (int k = 0; k < MT * NT; ++k) {
+        const int m = k / NT, j = k % NT;
+        const int row = m * 16 + (lane & 15);
+        if (k % 4 != wid || row >= a.M || !tv[j]) continue;
+        const f32x4 v = sum4(m, j);
+        const int64_t col = tile[j] * 16 + 4 * q;
+        *(float4 *)(a.out + (s * kRowPad + row) * a.ldo + col) = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    } else {  // EPI_SWIGLU
+      constexpr int NP = NT / 2;
+#pragma unroll
+      for (int k = 0; k < MT * NP; ++k) {
+        const int m = k / NP, p = k % NP;
+        const int row = m * 16 + (lane & 15);
+        if (k % 4 != wid || row >= a.M || !tv[p]) continue;
+        const f32x4 g = sum4(m, p), u = sum4(m, p + NP);
+        // act is the next GEMM's X: fragment-packed; the four columns stay in
+        // one E-element chunk
+        const int64_t col = tile[p] * 16 + 4 * q;
+        T *dst = (T *)a.act + act_off<T>(row, col, a.ldact);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) Elem<T>::store(dst, i, silu(g[i]) * u[i]);
+      }
+    }
+    return;
+  }
+
+  // argmax: reduce the four waves' partial sums in LDS (fixed order: wave 0..3)
   __shared__ f32x4 red[3][MT][NT][64];
   if (wid > 0) {
 #pragma unroll
@@ -179,39 +225,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < NT; ++j) acc[m][j] += red[w][m][j][lane];
 
-  // lane holds D[n = tile*16 + 4*q + i][row = m*16 + lane%16], q = lane/16
-  const int q = lane >> 4;
-  if (EPI == EPI_PARTIAL) {
-#pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      int row = m * 16 + (lane & 15);
-      if (row >= a.M) continue;
-#pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        if (!tv[j]) continue;
-        int64_t col = tile[j] * 16 + 4 * q;
-        float4 v = make_float4(acc[m][j][0], acc[m][j][1], acc[m][j][2], acc[m][j][3]);
-        *(float4 *)(a.out + (s * kRowPad + row) * a.ldo + col) = v;
-      }
-    }
-  } else if (EPI == EPI_SWIGLU) {
-    constexpr int NP = NT / 2;
-#pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      int row = m * 16 + (lane & 15);
-      if (row >= a.M) continue;
-#pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        if (!tv[p]) continue;
-        // act is the next GEMM's X: fragment-packed; the four columns stay in
-        // one E-element chunk
-        int64_t col = tile[p] * 16 + 4 * q;
-        T *dst = (T *)a.act + act_off<T>(row, col, a.ldact);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) Elem<T>::store(dst, i, silu(acc[m][p][i]) * acc[m][p + NP][i]);
-      }
-    }
-  } else {  // EPI_ARGMAX
+  {
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       int row = m * 16 + (lane & 15);
