@@ -120,35 +120,38 @@ __global__ __launch_bounds__(256) void k_residual_norm(const float *part, int sp
   const int m = blockIdx.x;
   float4 *xr = (float4 *)(x + (int64_t)m * H);
   const int H4 = H / 4;  // at most 512: two four-column chunks per thread
-  // the gains are read first and the summed row stays in registers, so no
-  // memory round trip follows the block-wide sum of squares
-  float4 keep[2], gk[2];
+  // the gains, the residual and the first kB split partials of both chunks
+  // are loaded together before anything waits (one memory round trip, not
+  // one per split), then added in split order; the summed row stays in
+  // registers, so no memory round trip follows the block-wide sum of squares
+  constexpr int kB = 8;
+  float4 keep[2], gk[2], xv[2], pv[2][kB];
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
     const int c = threadIdx.x + 256 * r;
-    if (c < H4) gk[r] = ((const float4 *)gain)[c];
+    if (c >= H4) continue;
+    gk[r] = ((const float4 *)gain)[c];
+    xv[r] = xr[c];
+#pragma unroll
+    for (int u = 0; u < kB; ++u)
+      if (u < splits) pv[r][u] = ((const float4 *)(part + ((int64_t)u * rowpad + m) * ldpart))[c];
   }
   float ss = 0.f;
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
     const int c = threadIdx.x + 256 * r;
     if (c >= H4) continue;
-    float4 acc = xr[c];
-    int sp = 0;
-    for (; sp + 8 <= splits; sp += 8) {
-      float4 v[8];
+    float4 acc = xv[r];
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        v[u] = ((const float4 *)(part + ((int64_t)(sp + u) * rowpad + m) * ldpart))[c];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        acc.x += v[u].x;
-        acc.y += v[u].y;
-        acc.z += v[u].z;
-        acc.w += v[u].w;
+    for (int u = 0; u < kB; ++u) {
+      if (u < splits) {
+        acc.x += pv[r][u].x;
+        acc.y += pv[r][u].y;
+        acc.z += pv[r][u].z;
+        acc.w += pv[r][u].w;
       }
     }
-    for (; sp < splits; ++sp) {
+    for (int sp = kB; sp < splits; ++sp) {  // more splits than kB: one at a time
       float4 v = ((const float4 *)(part + ((int64_t)sp * rowpad + m) * ldpart))[c];
       acc.x += v.x;
       acc.y += v.y;
