@@ -71,7 +71,11 @@ def lib():
         vp, i32, i64, f64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
         L.or_forward.restype = i32
         L.or_forward.argtypes = [ctypes.POINTER(_Model), vp, i64, vp, i64, i32, vp, vp, vp, i32,
-                                 vp, vp, vp]
+                                 vp, vp, vp, vp]
+        L.or_layer.restype = None
+        L.or_layer.argtypes = [ctypes.POINTER(_Model), i32, vp, i64, vp, i64, i32, vp, vp, vp, vp]
+        L.or_head.restype = None
+        L.or_head.argtypes = [ctypes.POINTER(_Model), vp, i32, vp, vp]
         L.or_lookup_candidates.restype = i32
         L.or_lookup_candidates.argtypes = [vp, vp, i64, i32, vp, i64, i32, i32, vp, vp]
         L.or_build_draft.restype = i32
@@ -94,6 +98,8 @@ def lib():
         L.or_attend.argtypes = [vp, vp, vp, i64, i32, f64, vp]
         L.or_argmax.restype = ctypes.c_int32
         L.or_argmax.argtypes = [vp, i64]
+        L.or_key_project.restype = None
+        L.or_key_project.argtypes = [vp, i32, i32, vp, i64, vp]
         L.or_key_encode.restype = None
         L.or_key_encode.argtypes = [vp, i32, i32, vp, i64, vp]
         L.or_cos_candidates.restype = i32
@@ -202,11 +208,14 @@ class Model:
 
     def forward(self, kv_prefix: np.ndarray, tok: Sequence[int], pos: Sequence[int],
                 vis: np.ndarray, kv_extra: Optional[np.ndarray] = None, logits_from: int = 0,
-                want_logits: bool = True, want_kv: bool = True, hidden: Optional[np.ndarray] = None):
+                want_logits: bool = True, want_kv: bool = True, hidden: Optional[np.ndarray] = None,
+                resid: Optional[np.ndarray] = None):
         """Forward of M new rows. Returns (logits [M][V] fp32 or None, kv_new
         [L][2][nkv][M][hd] fp64 or None). kv_prefix: [L][2][nkv][P][hd].
         hidden, if given ([M][H] fp64), receives the final-layer states of
-        rows >= logits_from (the lm_head input)."""
+        rows >= logits_from (the lm_head input); resid, if given
+        ([L+1][M][H] fp64), the embeddings and the residual stream after
+        every layer."""
         s = self.shape
         kv_prefix = np.ascontiguousarray(kv_prefix)
         P = kv_prefix.shape[3]
@@ -225,10 +234,44 @@ class Model:
         if hidden is not None:
             assert hidden.dtype == np.float64 and hidden.shape == (M, s.hidden)
             assert hidden.flags.c_contiguous
+        if resid is not None:
+            assert resid.dtype == np.float64 and resid.shape == (s.n_layers + 1, M, s.hidden)
+            assert resid.flags.c_contiguous
         lib().or_forward(ctypes.byref(self._c), _ptr(kv_prefix), P, _ptr(kv_extra), E, M,
                          _ptr(tok), _ptr(pos), _ptr(vis), int(logits_from), _ptr(logits),
-                         _ptr(kv_new), _ptr(hidden))
+                         _ptr(kv_new), _ptr(hidden), _ptr(resid))
         return logits, kv_new
+
+    def layer(self, l: int, kv_prefix: np.ndarray, x: np.ndarray, pos: Sequence[int],
+              vis: np.ndarray, kv_extra: Optional[np.ndarray] = None) -> np.ndarray:
+        """Decoder layer l applied to the residual stream x [M][H]; returns
+        the stream after the layer (x itself is not modified)."""
+        s = self.shape
+        kv_prefix = np.ascontiguousarray(kv_prefix)
+        P = kv_prefix.shape[3]
+        x = np.array(x, np.float64, copy=True, order="C")
+        M = x.shape[0]
+        assert x.shape == (M, s.hidden)
+        pos = np.ascontiguousarray(pos, np.int64)
+        vis = np.ascontiguousarray(vis, np.uint8).reshape(M, M)
+        E = 0
+        if kv_extra is not None:
+            kv_extra = np.ascontiguousarray(kv_extra, np.float64)
+            E = kv_extra.shape[3]
+        lib().or_layer(ctypes.byref(self._c), int(l), _ptr(kv_prefix), P, _ptr(kv_extra), E, M,
+                       _ptr(pos), _ptr(vis), _ptr(x), None)
+        return x
+
+    def head(self, x: np.ndarray, want_hidden: bool = False):
+        """Final norm and lm_head of the residual stream x [M][H]: logits
+        [M][V] fp32 (and the lm_head input with want_hidden)."""
+        s = self.shape
+        x = np.ascontiguousarray(x, np.float64)
+        M = x.shape[0]
+        logits = np.zeros((M, s.vocab), np.float32)
+        hidden = np.zeros((M, s.hidden), np.float64) if want_hidden else None
+        lib().or_head(ctypes.byref(self._c), _ptr(x), M, _ptr(logits), _ptr(hidden))
+        return (logits, hidden) if want_hidden else logits
 
 
 # ----------------------------------------------------------------------------
@@ -263,6 +306,18 @@ def lookup(tokens: np.ndarray, seq_offsets: np.ndarray, ngram: int, ctx: np.ndar
 
 
 KEY_DIM = 256  # Section 4: 256-dimensional int8 retrieval keys
+
+
+def key_project(R: np.ndarray, h: np.ndarray) -> np.ndarray:
+    """The fp64 projection v = R h of hidden states h [n][H] (plain index-order
+    sums, see or_key_project): [n][KEY_DIM]."""
+    R = np.ascontiguousarray(R, np.float64)
+    h = np.ascontiguousarray(np.atleast_2d(h), np.float64)
+    kd, H = R.shape
+    assert h.shape[1] == H
+    v = np.zeros((h.shape[0], kd), np.float64)
+    lib().or_key_project(_ptr(R), kd, H, _ptr(h), h.shape[0], _ptr(v))
+    return v
 
 
 def key_encode(R: np.ndarray, h: np.ndarray) -> np.ndarray:

@@ -164,31 +164,26 @@ void or_attend(const double *q, const double *const *keys, const double *const *
 /* ------------------------------------------------------------------------ */
 
 /*
- * Forward pass of M new rows over a cached context.
+ * One decoder layer l over M new rows, in place on the residual stream x
+ * [M][H] (fp64).
  *
  *   kv_prefix  cached K/V of positions 0..P-1, logical layout
  *              [L][2][nkv][P][hd] in the model's storage format
  *   kv_extra   further cached K/V rows that every new row sees, fp64 values
  *              (already rounded to the storage format), [L][2][nkv][E][hd]
- *   tok[M]     token ids of the new rows
  *   pos[M]     absolute RoPE positions of the new rows
  *   vis[M*M]   vis[j*M+i] != 0 iff new row j attends to new row i (j sees
  *              itself; causal for a linear draft, ancestors for a tree)
- *   logits     [M][V] fp32 for rows >= logits_from (others untouched); NULL ok
- *   kv_new     [L][2][nkv][M][hd] fp64 K/V of the new rows; NULL ok
- *   hidden     [M][H] final-layer states (the final RMSNorm output, rounded
- *              as it enters the lm_head) for rows >= logits_from; NULL ok
- * Returns 0.
+ *   kv_new     [L][2][nkv][M][hd] fp64 K/V of the new rows (layer l's part
+ *              is written); NULL ok
  */
-int or_forward(const or_model *m, const void *kv_prefix, int64_t P, const double *kv_extra,
-               int64_t E, int M, const int32_t *tok, const int64_t *pos, const uint8_t *vis,
-               int logits_from, float *logits, double *kv_new, double *hidden) {
-  const int L = m->L, H = m->H, nq = m->nq, nkv = m->nkv, hd = m->hd, F = m->F;
-  const int64_t V = m->V;
+void or_layer(const or_model *m, int l, const void *kv_prefix, int64_t P, const double *kv_extra,
+              int64_t E, int M, const int64_t *pos, const uint8_t *vis, double *x,
+              double *kv_new) {
+  const int H = m->H, nq = m->nq, nkv = m->nkv, hd = m->hd, F = m->F;
   const int qd = nq * hd, kvd = nkv * hd, nqkv = qd + 2 * kvd, grp = nq / nkv;
   const double scale = 1.0 / sqrt((double)hd);
 
-  double *x = (double *)calloc((size_t)M * H, sizeof(double));
   double *xn = (double *)malloc(sizeof(double) * (size_t)M * H);
   double *qkv = (double *)malloc(sizeof(double) * (size_t)M * nqkv);
   double *att = (double *)malloc(sizeof(double) * (size_t)M * qd);
@@ -198,112 +193,150 @@ int or_forward(const or_model *m, const void *kv_prefix, int64_t P, const double
   double *pk = (double *)malloc(sizeof(double) * (size_t)nkv * (P > 0 ? P : 1) * hd);
   double *pv = (double *)malloc(sizeof(double) * (size_t)nkv * (P > 0 ? P : 1) * hd);
 
+  /* attention sub-layer input: RMSNorm, rounded */
+  for (int r = 0; r < M; ++r) {
+    or_rmsnorm(x + (int64_t)r * H, m->attn_norm + (int64_t)l * H, H, m->eps, xn + (int64_t)r * H);
+    for (int k = 0; k < H; ++k) xn[(int64_t)r * H + k] = rnd(m, xn[(int64_t)r * H + k]);
+  }
+  linear(m, (const char *)m->wqkv + (size_t)l * nqkv * H * (m->bf16 ? 2 : 4), nqkv, H, M, xn,
+         qkv);
+  /* RoPE on every query and key head, then round Q, K, V */
+  for (int r = 0; r < M; ++r) {
+    double *row = qkv + (int64_t)r * nqkv;
+    for (int h = 0; h < nq + nkv; ++h) or_rope(row + h * hd, hd, (double)pos[r], m->theta);
+    for (int i = 0; i < nqkv; ++i) row[i] = rnd(m, row[i]);
+  }
+  if (kv_new) {
+    for (int r = 0; r < M; ++r)
+      for (int g = 0; g < nkv; ++g)
+        for (int i = 0; i < hd; ++i) {
+          const double *row = qkv + (int64_t)r * nqkv;
+          kv_new[((((int64_t)l * 2 + 0) * nkv + g) * M + r) * hd + i] = row[qd + g * hd + i];
+          kv_new[((((int64_t)l * 2 + 1) * nkv + g) * M + r) * hd + i] = row[qd + kvd + g * hd + i];
+        }
+  }
+  /* cached prefix of this layer as fp64 */
+  for (int g = 0; g < nkv; ++g)
+    for (int64_t t = 0; t < P; ++t)
+      for (int i = 0; i < hd; ++i) {
+        int64_t src_k = ((((int64_t)l * 2 + 0) * nkv + g) * P + t) * hd + i;
+        int64_t src_v = ((((int64_t)l * 2 + 1) * nkv + g) * P + t) * hd + i;
+        pk[((int64_t)g * P + t) * hd + i] = wget(m, kv_prefix, src_k);
+        pv[((int64_t)g * P + t) * hd + i] = wget(m, kv_prefix, src_v);
+      }
+  /* grouped-query attention: query head h reads KV head h / grp; keys in
+     position order: prefix, extra rows, visible new rows */
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int r = 0; r < M; ++r)
+    for (int h = 0; h < nq; ++h) {
+      int g = h / grp;
+      int64_t cap = P + E + M;
+      const double **ks = (const double **)malloc(sizeof(double *) * (size_t)cap);
+      const double **vs = (const double **)malloc(sizeof(double *) * (size_t)cap);
+      int64_t nk = 0;
+      for (int64_t t = 0; t < P; ++t, ++nk) {
+        ks[nk] = pk + ((int64_t)g * P + t) * hd;
+        vs[nk] = pv + ((int64_t)g * P + t) * hd;
+      }
+      for (int64_t e = 0; e < E; ++e, ++nk) {
+        ks[nk] = kv_extra + ((((int64_t)l * 2 + 0) * nkv + g) * E + e) * hd;
+        vs[nk] = kv_extra + ((((int64_t)l * 2 + 1) * nkv + g) * E + e) * hd;
+      }
+      for (int i = 0; i < M; ++i) {
+        if (!vis[(int64_t)r * M + i]) continue;
+        ks[nk] = qkv + (int64_t)i * nqkv + qd + g * hd;
+        vs[nk] = qkv + (int64_t)i * nqkv + qd + kvd + g * hd;
+        ++nk;
+      }
+      double *o = att + (int64_t)r * qd + h * hd;
+      or_attend(qkv + (int64_t)r * nqkv + h * hd, ks, vs, nk, hd, scale, o);
+      for (int i = 0; i < hd; ++i) o[i] = rnd(m, o[i]);
+      free(ks);
+      free(vs);
+    }
+  /* output projection + residual */
+  linear(m, (const char *)m->wo + (size_t)l * H * qd * (m->bf16 ? 2 : 4), H, qd, M, att, tmp);
+  for (int64_t i = 0; i < (int64_t)M * H; ++i) x[i] += tmp[i];
+  /* feed-forward sub-layer */
+  for (int r = 0; r < M; ++r) {
+    or_rmsnorm(x + (int64_t)r * H, m->ffn_norm + (int64_t)l * H, H, m->eps, xn + (int64_t)r * H);
+    for (int k = 0; k < H; ++k) xn[(int64_t)r * H + k] = rnd(m, xn[(int64_t)r * H + k]);
+  }
+  linear(m, (const char *)m->wgu + (size_t)l * 2 * F * H * (m->bf16 ? 2 : 4), 2 * (int64_t)F, H,
+         M, xn, gu);
+  for (int r = 0; r < M; ++r)
+    for (int j = 0; j < F; ++j) {
+      double g = gu[(int64_t)r * 2 * F + j], u = gu[(int64_t)r * 2 * F + F + j];
+      act[(int64_t)r * F + j] = rnd(m, or_swiglu(g, u));
+    }
+  linear(m, (const char *)m->wd + (size_t)l * H * F * (m->bf16 ? 2 : 4), H, F, M, act, tmp);
+  for (int64_t i = 0; i < (int64_t)M * H; ++i) x[i] += tmp[i];
+
+  free(xn); free(qkv); free(att); free(tmp); free(gu); free(act); free(pk); free(pv);
+}
+
+/*
+ * Final RMSNorm (rounded as it enters the lm_head) and the lm_head of M rows
+ * of the last layer's residual stream x [M][H]. hidden [M][H] (NULL ok)
+ * receives the lm_head input; logits [M][V] fp32 (NULL ok).
+ */
+void or_head(const or_model *m, const double *x, int M, float *logits, double *hidden) {
+  const int H = m->H;
+  const int64_t V = m->V;
+  double *xn = (double *)malloc(sizeof(double) * (size_t)(M > 0 ? M : 1) * H);
+  for (int r = 0; r < M; ++r) {
+    or_rmsnorm(x + (int64_t)r * H, m->final_norm, H, m->eps, xn + (int64_t)r * H);
+    for (int k = 0; k < H; ++k) xn[(int64_t)r * H + k] = rnd(m, xn[(int64_t)r * H + k]);
+  }
+  if (hidden)
+    for (int64_t i = 0; i < (int64_t)M * H; ++i) hidden[i] = xn[i];
+  if (logits) {
+    double *lg = (double *)malloc(sizeof(double) * (size_t)(M > 0 ? M : 1) * V);
+    linear(m, m->lm_head, V, H, M, xn, lg);
+    for (int64_t i = 0; i < (int64_t)M * V; ++i) logits[i] = (float)lg[i];
+    free(lg);
+  }
+  free(xn);
+}
+
+/*
+ * Forward pass of M new rows over a cached context: token embedding, the L
+ * decoder layers (or_layer), then the final norm and lm_head (or_head).
+ *
+ *   kv_prefix, P, kv_extra, E, pos, vis: as for or_layer
+ *   tok[M]     token ids of the new rows
+ *   logits     [M][V] fp32 for rows >= logits_from (others untouched); NULL ok
+ *   kv_new     [L][2][nkv][M][hd] fp64 K/V of the new rows; NULL ok
+ *   hidden     [M][H] final-layer states (the final RMSNorm output, rounded
+ *              as it enters the lm_head) for rows >= logits_from; NULL ok
+ *   resid      [L+1][M][H] residual stream: the embeddings, then the stream
+ *              after each layer; NULL ok
+ * Returns 0.
+ */
+int or_forward(const or_model *m, const void *kv_prefix, int64_t P, const double *kv_extra,
+               int64_t E, int M, const int32_t *tok, const int64_t *pos, const uint8_t *vis,
+               int logits_from, float *logits, double *kv_new, double *hidden, double *resid) {
+  const int L = m->L, H = m->H;
+  const int64_t V = m->V;
+  double *x = (double *)calloc((size_t)M * H, sizeof(double));
+
   /* token embedding */
   for (int r = 0; r < M; ++r)
     for (int k = 0; k < H; ++k) x[(int64_t)r * H + k] = wget(m, m->embed, (int64_t)tok[r] * H + k);
+  if (resid) memcpy(resid, x, sizeof(double) * (size_t)M * H);
 
   for (int l = 0; l < L; ++l) {
-    /* attention sub-layer input: RMSNorm, rounded */
-    for (int r = 0; r < M; ++r) {
-      or_rmsnorm(x + (int64_t)r * H, m->attn_norm + (int64_t)l * H, H, m->eps, xn + (int64_t)r * H);
-      for (int k = 0; k < H; ++k) xn[(int64_t)r * H + k] = rnd(m, xn[(int64_t)r * H + k]);
-    }
-    linear(m, (const char *)m->wqkv + (size_t)l * nqkv * H * (m->bf16 ? 2 : 4), nqkv, H, M, xn,
-           qkv);
-    /* RoPE on every query and key head, then round Q, K, V */
-    for (int r = 0; r < M; ++r) {
-      double *row = qkv + (int64_t)r * nqkv;
-      for (int h = 0; h < nq + nkv; ++h) or_rope(row + h * hd, hd, (double)pos[r], m->theta);
-      for (int i = 0; i < nqkv; ++i) row[i] = rnd(m, row[i]);
-    }
-    if (kv_new) {
-      for (int r = 0; r < M; ++r)
-        for (int g = 0; g < nkv; ++g)
-          for (int i = 0; i < hd; ++i) {
-            const double *row = qkv + (int64_t)r * nqkv;
-            kv_new[((((int64_t)l * 2 + 0) * nkv + g) * M + r) * hd + i] = row[qd + g * hd + i];
-            kv_new[((((int64_t)l * 2 + 1) * nkv + g) * M + r) * hd + i] = row[qd + kvd + g * hd + i];
-          }
-    }
-    /* cached prefix of this layer as fp64 */
-    for (int g = 0; g < nkv; ++g)
-      for (int64_t t = 0; t < P; ++t)
-        for (int i = 0; i < hd; ++i) {
-          int64_t src_k = ((((int64_t)l * 2 + 0) * nkv + g) * P + t) * hd + i;
-          int64_t src_v = ((((int64_t)l * 2 + 1) * nkv + g) * P + t) * hd + i;
-          pk[((int64_t)g * P + t) * hd + i] = wget(m, kv_prefix, src_k);
-          pv[((int64_t)g * P + t) * hd + i] = wget(m, kv_prefix, src_v);
-        }
-    /* grouped-query attention: query head h reads KV head h / grp; keys in
-       position order: prefix, extra rows, visible new rows */
-#pragma omp parallel for collapse(2) schedule(dynamic)
-    for (int r = 0; r < M; ++r)
-      for (int h = 0; h < nq; ++h) {
-        int g = h / grp;
-        int64_t cap = P + E + M;
-        const double **ks = (const double **)malloc(sizeof(double *) * (size_t)cap);
-        const double **vs = (const double **)malloc(sizeof(double *) * (size_t)cap);
-        int64_t nk = 0;
-        for (int64_t t = 0; t < P; ++t, ++nk) {
-          ks[nk] = pk + ((int64_t)g * P + t) * hd;
-          vs[nk] = pv + ((int64_t)g * P + t) * hd;
-        }
-        for (int64_t e = 0; e < E; ++e, ++nk) {
-          ks[nk] = kv_extra + ((((int64_t)l * 2 + 0) * nkv + g) * E + e) * hd;
-          vs[nk] = kv_extra + ((((int64_t)l * 2 + 1) * nkv + g) * E + e) * hd;
-        }
-        for (int i = 0; i < M; ++i) {
-          if (!vis[(int64_t)r * M + i]) continue;
-          ks[nk] = qkv + (int64_t)i * nqkv + qd + g * hd;
-          vs[nk] = qkv + (int64_t)i * nqkv + qd + kvd + g * hd;
-          ++nk;
-        }
-        double *o = att + (int64_t)r * qd + h * hd;
-        or_attend(qkv + (int64_t)r * nqkv + h * hd, ks, vs, nk, hd, scale, o);
-        for (int i = 0; i < hd; ++i) o[i] = rnd(m, o[i]);
-        free(ks);
-        free(vs);
-      }
-    /* output projection + residual */
-    linear(m, (const char *)m->wo + (size_t)l * H * qd * (m->bf16 ? 2 : 4), H, qd, M, att, tmp);
-    for (int64_t i = 0; i < (int64_t)M * H; ++i) x[i] += tmp[i];
-    /* feed-forward sub-layer */
-    for (int r = 0; r < M; ++r) {
-      or_rmsnorm(x + (int64_t)r * H, m->ffn_norm + (int64_t)l * H, H, m->eps, xn + (int64_t)r * H);
-      for (int k = 0; k < H; ++k) xn[(int64_t)r * H + k] = rnd(m, xn[(int64_t)r * H + k]);
-    }
-    linear(m, (const char *)m->wgu + (size_t)l * 2 * F * H * (m->bf16 ? 2 : 4), 2 * (int64_t)F, H,
-           M, xn, gu);
-    for (int r = 0; r < M; ++r)
-      for (int j = 0; j < F; ++j) {
-        double g = gu[(int64_t)r * 2 * F + j], u = gu[(int64_t)r * 2 * F + F + j];
-        act[(int64_t)r * F + j] = rnd(m, or_swiglu(g, u));
-      }
-    linear(m, (const char *)m->wd + (size_t)l * H * F * (m->bf16 ? 2 : 4), H, F, M, act, tmp);
-    for (int64_t i = 0; i < (int64_t)M * H; ++i) x[i] += tmp[i];
+    or_layer(m, l, kv_prefix, P, kv_extra, E, M, pos, vis, x, kv_new);
+    if (resid) memcpy(resid + (int64_t)(l + 1) * M * H, x, sizeof(double) * (size_t)M * H);
   }
 
   if ((logits || hidden) && logits_from < M) {
     int nr = M - logits_from;
-    for (int r = 0; r < nr; ++r) {
-      int rr = logits_from + r;
-      or_rmsnorm(x + (int64_t)rr * H, m->final_norm, H, m->eps, xn + (int64_t)r * H);
-      for (int k = 0; k < H; ++k) xn[(int64_t)r * H + k] = rnd(m, xn[(int64_t)r * H + k]);
-    }
-    if (hidden)
-      for (int64_t i = 0; i < (int64_t)nr * H; ++i) hidden[(int64_t)logits_from * H + i] = xn[i];
+    or_head(m, x + (int64_t)logits_from * H, nr,
+            logits ? logits + (int64_t)logits_from * V : NULL,
+            hidden ? hidden + (int64_t)logits_from * H : NULL);
   }
-  if (logits && logits_from < M) {
-    int nr = M - logits_from;
-    double *lg = (double *)malloc(sizeof(double) * (size_t)nr * V);
-    linear(m, m->lm_head, V, H, nr, xn, lg);
-    for (int r = 0; r < nr; ++r)
-      for (int64_t v = 0; v < V; ++v)
-        logits[(int64_t)(logits_from + r) * V + v] = (float)lg[(int64_t)r * V + v];
-    free(lg);
-  }
-
-  free(x); free(xn); free(qkv); free(att); free(tmp); free(gu); free(act); free(pk); free(pv);
+  free(x);
   return 0;
 }
 
@@ -416,35 +449,42 @@ int or_build_draft(const int32_t *tokens, const int64_t *cand_pos, const int32_t
 }
 
 /*
- * Retrieval keys (Section 4, "Memory and retrieval": normalized final-layer
- * states are mapped to 256-dimensional int8 keys through a fixed random
- * projection). h is the final-layer state as it enters the lm_head (the
- * final RMSNorm output). v = R h with R [kd][H] row-major, in fp64: each
- * component is summed as 16 interleaved chains (chain c takes k = c, c+16,
- * c+32, ... in increasing order, each step a fused multiply-add starting from
- * 0), then the chains are added in order c = 0..15.
+ * Retrieval keys (Section 4, "Memory and retrieval": the final-layer states
+ * are normalized and reduced to 256-dimensional int8 keys by one fixed random
+ * projection). h is the final-layer state as it enters the lm_head (the final
+ * RMSNorm output). The projection is v = R h with R [kd][H] row-major: each
+ * component is one plain fp64 sum over k = 0 .. H-1 in index order, every
+ * product and every partial sum rounded separately (no fused operations).
  * The key is the symmetric int8 quantisation of v with a per-vector scale:
  * code_j = round-half-even(v_j * 127 / max_i |v_i|); an all-zero v gives the
  * zero key. (A positive rescaling of h changes neither the direction nor,
  * up to rounding, the codes, so no further normalisation is applied.)
+ * Another summation order of the same projection can move a code by one only
+ * where v_j * 127 / max_i |v_i| lies within that order's rounding error of a
+ * half-integer.
  */
-void or_key_encode(const double *R, int kd, int H, const double *h, int64_t n, int8_t *out) {
+__attribute__((optimize("fp-contract=off")))
+void or_key_project(const double *R, int kd, int H, const double *h, int64_t n, double *v) {
   for (int64_t r = 0; r < n; ++r) {
     const double *hr = h + r * H;
-    double v[1024];
-    double mx = 0.0;
     for (int j = 0; j < kd; ++j) {
-      double chain[16];
-      for (int c = 0; c < 16; ++c) {
-        double acc = 0.0;
-        for (int k = c; k < H; k += 16) acc = fma(R[(int64_t)j * H + k], hr[k], acc);
-        chain[c] = acc;
+      volatile double acc = 0.0;
+      for (int k = 0; k < H; ++k) {
+        volatile double p = R[(int64_t)j * H + k] * hr[k];
+        acc = acc + p;
       }
-      double sum = chain[0];
-      for (int c = 1; c < 16; ++c) sum += chain[c];
-      v[j] = sum;
-      if (fabs(sum) > mx) mx = fabs(sum);
+      v[r * kd + j] = acc;
     }
+  }
+}
+
+void or_key_encode(const double *R, int kd, int H, const double *h, int64_t n, int8_t *out) {
+  double *v = (double *)malloc(sizeof(double) * (size_t)kd);
+  for (int64_t r = 0; r < n; ++r) {
+    or_key_project(R, kd, H, h + r * H, 1, v);
+    double mx = 0.0;
+    for (int j = 0; j < kd; ++j)
+      if (fabs(v[j]) > mx) mx = fabs(v[j]);
     for (int j = 0; j < kd; ++j) {
       double c = mx > 0.0 ? rint((v[j] * 127.0) / mx) : 0.0;
       if (c > 127.0) c = 127.0;
@@ -452,6 +492,7 @@ void or_key_encode(const double *R, int kd, int H, const double *h, int64_t n, i
       out[r * kd + j] = (int8_t)c;
     }
   }
+  free(v);
 }
 
 /*

@@ -1,16 +1,20 @@
 """GPU parity of the paper's retrieval (Section 3.2, "Context-compatible
 retrieval"; Section 4, "Memory and retrieval"): int8 keys from a fixed random
 projection of final-layer states, and the exact cosine lookup over the
-entries whose stored token matches the query token. Keys and drafts are
-integer work and must match the oracle bit for bit; keys of the verify
-step's own states are compared with keys of the oracle's states (the states
-themselves agree only to rounding)."""
+entries whose stored token matches the query token. Drafts are integer work
+and must match the oracle bit for bit. Keys are integers decided by an fp64
+projection that the device sums in another order than the oracle: they must
+equal the oracle's codes except where the scaled value lies within the two
+orders' rounding bound of a half-integer, where either neighbour is valid
+(keycheck). Keys of the verify step's own states are compared with keys of
+the oracle's states (the states themselves agree only to rounding)."""
 import numpy as np
 import pytest
 
 import oracle
 import synth
 from pfharness import Gpu, assert_same_draft
+import keycheck
 
 pytestmark = pytest.mark.gpu
 
@@ -37,13 +41,17 @@ def _encode_gpu(pf, kp, h, dtype):
 
 @pytest.mark.parametrize("H,n,dtype", [(64, 3, "f32"), (256, 70, "f32"), (2048, 17, "bf16"),
                                        (3584, 33, "bf16"), (272, 5, "bf16"), (16, 1, "f32")])
-def test_key_encode_bit_exact(pf, H, n, dtype):
+def test_key_encode_valid(pf, H, n, dtype):
     R = synth.key_projection(H, 21)
     h = synth.hidden_states(n, H, 22 + n)
     kp = pf.pf_keyproj_create(R)
     got, hv = _encode_gpu(pf, kp, h, dtype)
-    ref = oracle.key_encode(R.astype(np.float64), hv)
-    assert (got == ref).all(), np.argwhere(got != ref)[:8]
+    R64 = R.astype(np.float64)
+    ref = oracle.key_encode(R64, hv)
+    band = keycheck.check_codes(got, R64, hv, oracle.key_project(R64, hv))
+    exact = (got == ref).mean()
+    print(f"H={H} n={n} {dtype}: {exact:.6f} of the codes equal the oracle's, {band} in the half band")
+    assert band > 0 or (got == ref).all()
 
 
 def test_key_encode_zero_and_scaled_rows(pf):
@@ -56,7 +64,8 @@ def test_key_encode_zero_and_scaled_rows(pf):
     got, hv = _encode_gpu(pf, kp, h, "f32")
     assert (got[1] == 0).all()
     assert (got[2] == got[0]).all()
-    assert (got == oracle.key_encode(R.astype(np.float64), hv)).all()
+    R64 = R.astype(np.float64)
+    keycheck.check_codes(got, R64, hv, oracle.key_project(R64, hv))
 
 
 def _store(T, n_seqs, vocab, seed, keys=None):

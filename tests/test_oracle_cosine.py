@@ -14,6 +14,7 @@ import pytest
 
 import oracle
 import synth
+import keycheck
 
 
 def _eye(n):
@@ -66,32 +67,80 @@ def test_encode_matches_float_projection():
 
 
 def _exact_codes(R, h):
-    """The encode definition evaluated with exact rationals: 16 interleaved
-    fused multiply-add chains (each step rounded once to double), the chains
-    added in order, then the per-vector quantisation."""
+    """The encode definition in exact rationals: v_j = sum_k R_jk h_k with no
+    rounding at all (so no summation order enters), then code_j =
+    round-half-even(v_j * 127 / max |v|), also exact. Returns the codes and
+    the exact scaled values."""
     kd, H = R.shape
-    v = []
-    for j in range(kd):
-        chains = []
-        for c in range(16):
-            acc = 0.0
-            for kk in range(c, H, 16):
-                acc = float(Fraction(R[j, kk]) * Fraction(h[kk]) + Fraction(acc))
-            chains.append(acc)
-        s = chains[0]
-        for c in range(1, 16):
-            s = s + chains[c]
-        v.append(s)
+    hf = [Fraction(float(t)) for t in h]
+    v = [sum((Fraction(float(R[j, k])) * hf[k] for k in range(H)), Fraction(0)) for j in range(kd)]
     m = max(abs(t) for t in v)
-    return [int(np.rint((t * 127.0) / m)) for t in v]
+    if m == 0:
+        return [0] * kd, [Fraction(0)] * kd
+    x = [t * 127 / m for t in v]
+    codes = []
+    for t in x:
+        f = t.numerator // t.denominator            # floor
+        r = t - f
+        c = f + 1 if (r > Fraction(1, 2) or (r == Fraction(1, 2) and f % 2 == 1)) else f
+        codes.append(int(c))
+    return codes, x
 
 
-def test_encode_exact_rational_reference():
-    R = synth.key_projection(40, 9)[:5].astype(np.float64)
-    h = synth.hidden_states(3, 40, 10).astype(np.float64)
+@pytest.mark.parametrize("kd,H,n,seed", [(5, 40, 3, 9), (24, 512, 2, 11), (256, 64, 2, 13)])
+def test_encode_exact_rational_reference(kd, H, n, seed):
+    """The oracle's fp64 codes equal the exact rational codes, except where the
+    exact scaled value lies within the fp64 summation bound of a half-integer
+    (then either neighbour is a correct rounding of an fp64 evaluation)."""
+    R = synth.key_projection(H, seed)[:kd].astype(np.float64)
+    h = synth.hidden_states(n, H, seed + 1).astype(np.float64)
     k = oracle.key_encode(R, h)
-    for r in range(3):
-        assert k[r].tolist() == _exact_codes(R, h[r])
+    v = oracle.key_project(R, h)
+    _, d = keycheck.scaled_bounds(R, h, v)
+    band = 0
+    for r in range(n):
+        want, x = _exact_codes(R, h[r])
+        for j in range(kd):
+            if int(k[r, j]) == want[j]:
+                continue
+            frac = abs(float(x[j] - (x[j].numerator // x[j].denominator)) - 0.5)
+            assert frac <= d[r, j] and abs(int(k[r, j]) - want[j]) == 1, (r, j, int(k[r, j]), want[j])
+            band += 1
+    assert band == 0  # with these seeds no exact value sits that close to a half
+
+
+def test_encode_projection_is_the_exact_sum_to_fp64_accuracy():
+    """or_key_project against the exact rational sum: within the summation
+    bound of every component (a dropped term, a transposed R or a wrong
+    stride misses it by orders of magnitude)."""
+    R = synth.key_projection(96, 17)[:12].astype(np.float64)
+    h = synth.hidden_states(2, 96, 18).astype(np.float64)
+    v = oracle.key_project(R, h)
+    for r in range(2):
+        for j in range(12):
+            exact = sum(Fraction(float(R[j, k])) * Fraction(float(h[r, k])) for k in range(96))
+            s = float(np.abs(R[j]) @ np.abs(h[r]))
+            assert abs(v[r, j] - float(exact)) <= 96 * 2.0 ** -53 * s * 1.01
+
+
+def test_a_different_summation_order_is_valid_under_the_band_check():
+    """keycheck accepts codes from another fp64 order (16 interleaved chains,
+    as a blocked kernel would sum) and rejects a planted wrong code."""
+    H = 2048
+    R = synth.key_projection(H, 31).astype(np.float64)
+    h = synth.hidden_states(8, H, 32).astype(np.float64)
+    v = oracle.key_project(R, h)
+    chains = np.zeros((8, 256))
+    for c in range(16):
+        chains += h[:, c::16] @ R[:, c::16].T
+    m = np.abs(chains).max(axis=1, keepdims=True)
+    other = np.clip(np.rint(chains * 127.0 / m), -127, 127).astype(np.int8)
+    keycheck.check_codes(other, R, h, v)
+    keycheck.check_codes(oracle.key_encode(R, h), R, h, v)
+    bad = other.astype(np.int64).copy()
+    bad[3, 7] += 1 if bad[3, 7] < 127 else -1
+    with pytest.raises(AssertionError):
+        keycheck.check_codes(bad, R, h, v)
 
 
 # ---------------------------------------------------------- cosine retrieval

@@ -485,3 +485,123 @@ def test_ffn_gate_is_the_silu_argument():
     wgu[0, :shape.ffn, :] *= -1
     c, _ = oracle.Model(shape, w).forward(kv, [t], [5], np.ones((1, 1)))
     assert np.abs(c - b).max() > 1e-2
+
+
+# ----------------------------------------------------------------------------
+# the attention sub-layer inside the decoder forward, in closed form
+# ----------------------------------------------------------------------------
+# One layer, FFN output zeroed (down projection 0) and the output projection a
+# cyclic permutation of the q = H features, so the layer's change of the
+# residual stream is exactly the permuted (rounded) attention output. The
+# expected values below come from the definitions (RMSNorm of a row, a dense
+# product, a rotation of a basis pair, softmax over the visible keys) written
+# with numpy and torch's bf16 rounding, not from the oracle's code.
+
+def _fmt(x, shape):
+    """fp64 values -> the model's storage format (fp32, or bf16 bits RNE)."""
+    t = torch.from_numpy(np.ascontiguousarray(x, np.float64)).to(torch.float32)
+    if shape.dtype == "f32":
+        return t.numpy()
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def _val(a, shape):
+    """storage format -> fp64 values."""
+    if shape.dtype == "f32":
+        return np.asarray(a, np.float64)
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(
+        torch.float64).numpy()
+
+
+def _rnd(x, shape):
+    if shape.dtype == "f32":
+        return np.asarray(x, np.float64)
+    return torch.from_numpy(np.asarray(x, np.float64)).to(torch.bfloat16).to(torch.float64).numpy()
+
+
+def _one_layer(shape, seed):
+    s1 = shape.with_layers(1)
+    w = dict(synth.make_weights(s1, seed))
+    H, q = s1.hidden, s1.q_dim
+    assert q == H
+    shift = np.roll(np.eye(H), 1, axis=1)          # (P x)[n] = x[n + 1]
+    w["wo"] = _fmt(shift[None], s1).reshape(1, H, q)
+    w["wd"] = np.zeros_like(w["wd"])
+    return s1, w, shift
+
+
+@pytest.mark.parametrize("shape", [SMALL, SMALL_BF16], ids=["f32", "bf16"])
+def test_zero_queries_attend_uniformly_to_unrotated_values(shape):
+    """Query projection 0: every visible key scores 0, so each head's output
+    is the mean of the visible value rows of its KV group (prefix values as
+    cached, new rows' values as projected, no rotation), rounded to the
+    model's format, and the output projection maps it into the stream."""
+    s1, w, shift = _one_layer(shape, 41)
+    H, hd, nq, nkv = s1.hidden, s1.head_dim, s1.n_heads, s1.n_kv_heads
+    q, kvd, grp = s1.q_dim, s1.kv_dim, nq // nkv
+    wqkv = w["wqkv"].copy()
+    wqkv[0, :q] = 0
+    w["wqkv"] = wqkv
+    m = oracle.Model(s1, w)
+    P, M = 5, 3
+    kv = synth.make_kv_prefix(s1, 41, P)
+    tok = [7, 19, 88]
+    pos = P + np.arange(M)
+    resid = np.zeros((2, M, H))
+    m.forward(kv, tok, pos, np.tril(np.ones((M, M))), resid=resid)
+    emb = _val(w["embed"], s1)
+    g = np.asarray(w["attn_norm"][0], np.float64)
+    Wv = _val(w["wqkv"][0, q + kvd:], s1)                   # [kvd][H]
+    vpre = _val(kv[0, 1], s1)                              # [nkv][P][hd]
+    vnew = []
+    for t in tok:
+        x = emb[t]
+        xn = _rnd(x / np.sqrt(np.mean(x * x) + s1.rms_eps) * g, s1)
+        vnew.append(_rnd(Wv @ xn, s1).reshape(nkv, hd))
+    for r in range(M):
+        att = np.zeros(q)
+        for h in range(nq):
+            gk = h // grp
+            rows = list(vpre[gk]) + [vnew[i][gk] for i in range(r + 1)]
+            att[h * hd:(h + 1) * hd] = _rnd(np.mean(rows, axis=0), s1)
+        got = resid[1, r] - resid[0, r]
+        assert np.allclose(got, shift @ att, rtol=0, atol=1e-14), np.abs(got - shift @ att).max()
+
+
+@pytest.mark.parametrize("shape", [SMALL, SMALL_BF16], ids=["f32", "bf16"])
+def test_two_prefix_keys_weight_is_logistic_at_inverse_sqrt_head_dim(shape):
+    """One new row at position P = 2 whose query is a * e_0 in head 0 (a
+    one-hot embedding row, one nonzero projection weight); its own key and
+    value are 0. Prefix key 1 is 0 with value 0; prefix key 2 is k * R(P) e_0
+    (the query's direction after the rotation) with value e_0. Head 0's first
+    output is then e^s / (2 + e^s) with s = (q_rot . k_2) / sqrt(head_dim);
+    head 1 (zero query, same group) averages the three values: 1/3."""
+    s1, w, shift = _one_layer(shape, 43)
+    H, hd, nq, nkv = s1.hidden, s1.head_dim, s1.n_heads, s1.n_kv_heads
+    q, kvd = s1.q_dim, s1.kv_dim
+    P, tok, i0, c, a, kk = 2, 5, 9, 1.0, 0.75, 1.5
+    emb = np.zeros((s1.vocab, H)); emb[tok, i0] = c
+    w["embed"] = _fmt(emb, s1)
+    wqkv = np.zeros((1, q + 2 * kvd, H)); wqkv[0, 0, i0] = a
+    w["wqkv"] = _fmt(wqkv, s1)
+    kv = np.zeros((1, 2, nkv, P, hd))
+    half = hd // 2
+    kv[0, 0, 0, 1, 0] = kk * np.cos(P)        # angle P * theta^0 on the pair (0, half)
+    kv[0, 0, 0, 1, half] = kk * np.sin(P)
+    kv[0, 1, 0, 1, 0] = 1.0
+    kv = _fmt(kv, s1).reshape(kv.shape)
+    m = oracle.Model(s1, w)
+    resid = np.zeros((2, 1, H))
+    m.forward(kv, [tok], [P], np.ones((1, 1)), resid=resid)
+    g = float(w["attn_norm"][0, i0])
+    xn = _rnd(c / np.sqrt(c * c / H + s1.rms_eps) * g, s1)
+    qa = a * xn
+    q_rot = np.array([_rnd(qa * np.cos(P), s1), _rnd(qa * np.sin(P), s1)])
+    k2 = _val(kv[0, 0, 0, 1], s1)[[0, half]]
+    s = float(q_rot @ k2) / np.sqrt(hd)
+    att = np.zeros(q)
+    att[0] = _rnd(np.exp(s) / (2.0 + np.exp(s)), s1)
+    att[hd] = _rnd(1.0 / 3.0, s1)
+    got = resid[1, 0] - resid[0, 0]
+    assert abs(s - 1.5 * 0.75 * 8 / 4) < 0.2       # the construction gives s near 2.25
+    assert np.allclose(got, shift @ att, rtol=0, atol=1e-14), (got[H - 1], att[0])
