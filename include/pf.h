@@ -340,6 +340,43 @@ pf_status pf_verify_step_profiled(pf_model *model, pf_kv_cache *kv, const pf_dra
                                   int32_t *count_out);
 
 /*
+ * Benchmark hook: enqueues only the launches of one profiling kind (one of
+ * PF_PROF_SETUP .. PF_PROF_ACCEPT) that pf_verify_step would make for these
+ * arguments, every layer's, on the step's own buffers, so that one kernel's
+ * duration can be timed in isolation (e.g. captured in a graph). The outputs
+ * are meaningless, nothing becomes pending for pf_kv_commit, and the cache
+ * slots P.. may be overwritten. Argument checks and errors as for
+ * pf_verify_step; kind out of range: PF_EINVAL.
+ */
+pf_status pf_verify_kernel_repeat(pf_model *model, pf_kv_cache *kv, const pf_draft *draft_dev,
+                                  int32_t rows, int32_t tree, int32_t kind,
+                                  pf_verify_result *res_dev, pf_stream s);
+
+/*
+ * Calibration for the benchmark's roofline: reads `bytes` of device memory at
+ * buf_dev (16-byte aligned, a multiple of 16 KiB) once with a plain streaming
+ * kernel (one 256-thread block per compute unit, every wave keeping eight
+ * 16-byte loads per lane in flight) and writes a checksum word to sink_dev,
+ * so that the time of the call is the device's achievable HBM read rate.
+ */
+pf_status pf_read_stream(const void *buf_dev, int64_t bytes, uint32_t *sink_dev, pf_stream s);
+
+/*
+ * Test-mode variant of pf_verify_step: the same step, plus a copy of the
+ * residual stream (the fp32 state every decoder layer adds its attention and
+ * feed-forward outputs to, Section 3.2's verification forward) into resid_dev,
+ * device fp32 [n_layers + 1][rows][hidden]: entry 0 holds the token
+ * embeddings, entry l + 1 the stream after layer l (the input of the final
+ * norm for l = n_layers - 1). It lets a test drive a reference from the
+ * device's own input of each layer. resid_dev must not be NULL; the other
+ * arguments and errors are those of pf_verify_step. The copies are extra
+ * launches on s (allocates nothing).
+ */
+pf_status pf_verify_step_trace(pf_model *model, pf_kv_cache *kv, const pf_draft *draft_dev,
+                               int32_t rows, int32_t tree, float *logits_dev,
+                               pf_verify_result *res_dev, float *resid_dev, pf_stream s);
+
+/*
  * Retrieval keys from the last verify step's final-layer states (they stay
  * in the model's work buffers until its next verify step or prefill).
  * pf_verify_query_key: the key of the row whose prediction is the bonus token

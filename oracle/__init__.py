@@ -243,9 +243,10 @@ class Model:
         return logits, kv_new
 
     def layer(self, l: int, kv_prefix: np.ndarray, x: np.ndarray, pos: Sequence[int],
-              vis: np.ndarray, kv_extra: Optional[np.ndarray] = None) -> np.ndarray:
+              vis: np.ndarray, kv_extra: Optional[np.ndarray] = None, want_kv: bool = False):
         """Decoder layer l applied to the residual stream x [M][H]; returns
-        the stream after the layer (x itself is not modified)."""
+        the stream after the layer (x itself is not modified), and with
+        want_kv also the layer's K/V of the new rows ([2][nkv][M][hd])."""
         s = self.shape
         kv_prefix = np.ascontiguousarray(kv_prefix)
         P = kv_prefix.shape[3]
@@ -258,9 +259,11 @@ class Model:
         if kv_extra is not None:
             kv_extra = np.ascontiguousarray(kv_extra, np.float64)
             E = kv_extra.shape[3]
+        kv_new = (np.zeros((s.n_layers, 2, s.n_kv_heads, M, s.head_dim), np.float64)
+                  if want_kv else None)
         lib().or_layer(ctypes.byref(self._c), int(l), _ptr(kv_prefix), P, _ptr(kv_extra), E, M,
-                       _ptr(pos), _ptr(vis), _ptr(x), None)
-        return x
+                       _ptr(pos), _ptr(vis), _ptr(x), _ptr(kv_new))
+        return (x, kv_new[l]) if want_kv else x
 
     def head(self, x: np.ndarray, want_hidden: bool = False):
         """Final norm and lm_head of the residual stream x [M][H]: logits

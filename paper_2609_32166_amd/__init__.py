@@ -38,7 +38,9 @@ EXPORTED = ["pf_last_error", "pf_version", "pf_context_init", "pf_context_sync_b
             "pf_store_build", "pf_store_destroy", "pf_store_size", "pf_draft_lookup",
             "pf_model_create", "pf_model_destroy", "pf_model_bytes", "pf_kv_bytes", "pf_kv_init",
             "pf_kv_import", "pf_kv_export", "pf_kv_set_len", "pf_kv_sync_bound", "pf_verify_step",
-            "pf_kv_commit", "pf_prefill", "pf_verify_step_profiled", "pf_keyproj_create",
+            "pf_kv_commit", "pf_prefill", "pf_verify_step_profiled", "pf_verify_step_trace",
+            "pf_verify_kernel_repeat", "pf_read_stream",
+            "pf_keyproj_create",
             "pf_keyproj_destroy", "pf_key_encode", "pf_store_attach_keys",
             "pf_draft_lookup_cosine", "pf_verify_query_key", "pf_verify_row_keys",
             "pf_ctl_create", "pf_ctl_destroy", "pf_ctl_get_state", "pf_ctl_set_state",
@@ -117,6 +119,9 @@ def lib():
             "pf_kv_commit": (i32, [vp, vp, vp, vp]),
             "pf_prefill": (i32, [vp, vp, vp, i32, i32, vp, vp]),
             "pf_verify_step_profiled": (i32, [vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]),
+            "pf_verify_step_trace": (i32, [vp, vp, vp, i32, i32, vp, vp, vp, vp]),
+            "pf_verify_kernel_repeat": (i32, [vp, vp, vp, i32, i32, i32, vp, vp]),
+            "pf_read_stream": (i32, [vp, i64, vp, vp]),
             "pf_keyproj_create": (i32, [vp, i32, vp]),
             "pf_keyproj_destroy": (None, [vp]),
             "pf_key_encode": (i32, [vp, vp, i32, i64, i64, vp, vp]),
@@ -496,6 +501,29 @@ def pf_verify_step(model: Model, kv: KVCache, draft, rows: int, tree: bool, logi
     _check(lib().pf_verify_step(model.h, ctypes.byref(kv.c), draft.data_ptr(), int(rows),
                                 int(bool(tree)), _ptr(logits), result.data_ptr(),
                                 _stream(stream)))
+
+
+def pf_verify_step_trace(model: Model, kv: KVCache, draft, rows: int, tree: bool, logits, result,
+                         resid, stream=None) -> None:
+    """pf_verify_step plus the residual stream after every layer into resid
+    (device fp32 [n_layers + 1][rows][hidden])."""
+    _check(lib().pf_verify_step_trace(model.h, ctypes.byref(kv.c), draft.data_ptr(), int(rows),
+                                      int(bool(tree)), _ptr(logits), result.data_ptr(),
+                                      _ptr(resid), _stream(stream)))
+
+
+def pf_verify_kernel_repeat(model: Model, kv: KVCache, draft, rows: int, tree: bool, kind: int,
+                            result, stream=None) -> None:
+    """Only the launches of one profiling kind of a verify step (benchmark)."""
+    _check(lib().pf_verify_kernel_repeat(model.h, ctypes.byref(kv.c), draft.data_ptr(), int(rows),
+                                         int(bool(tree)), int(kind), result.data_ptr(),
+                                         _stream(stream)))
+
+
+def pf_read_stream(buf, sink, stream=None) -> None:
+    """Plain streaming read of a device tensor (benchmark calibration)."""
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib().pf_read_stream(_ptr(buf), int(nbytes), _ptr(sink), _stream(stream)))
 
 
 def pf_verify_step_profiled(model: Model, kv: KVCache, draft, rows: int, tree: bool, logits,

@@ -908,10 +908,12 @@ static pf_status model_kv_match(const pf_model *m, const pf_kv_cache *kv, const 
   return PF_OK;
 }
 
+// Launch one kernel of the step, tagged with its profiling kind; with
+// only_kind >= 0 the launches of every other kind are skipped.
 #define PROF(k, call)                                                            \
   do {                                                                           \
     if (prof) prof->cur = (k);                                                   \
-    HIPCHK(call);                                                                \
+    if (only_kind < 0 || only_kind == (k)) HIPCHK(call);                         \
   } while (0)
 
 // Keys per attention key range. Ranges start at multiples of this length,
@@ -935,7 +937,7 @@ static int attn_range_keys(int64_t keys_max, bool bf, int nq, int wave_slots) {
 
 static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft, int32_t rows,
                              int32_t tree, float *logits, pf_verify_result *res, pf_stream s,
-                             Prof *prof) {
+                             Prof *prof, float *resid = nullptr, int only_kind = -1) {
   if (!m || !draft || !res) return fail(PF_EINVAL, "pf_verify_step: null pointer");
   if (pf_status r = kv_check(kv, "pf_verify_step")) return r;
   if (pf_status r = model_kv_match(m, kv, "pf_verify_step")) return r;
@@ -973,6 +975,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   PROF(0, launch_prep(sa, hs));
   PROF(0, launch_embed_norm(bf, m->embed, m->rowinfo, M, H, m->attn_norm, eps, m->x, m->xn, Hp,
                             true, hs));
+  if (resid && only_kind < 0) HIPCHK(launch_copy_rows(m->x, M, H, resid, hs));
 
   // attention geometry: key ranges over P + rows keys (P <= host bound)
   const int64_t keys_max = kv->host_bound + rows;
@@ -1076,6 +1079,8 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
     PROF(5, launch_residual_norm(bf, m->part, gd.splits, kRowPad, M, H, H, next_gain, eps, m->x, m->xn, Hp,
                                 true, hs));
+    if (resid && only_kind < 0)
+      HIPCHK(launch_copy_rows(m->x, M, H, resid + (int64_t)(l + 1) * M * H, hs));
   }
   // lm_head + greedy argmax partials
   GemmArgs gl{};
@@ -1094,14 +1099,43 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   const int nparts = (int)((m->plm.NT + gemm_tiles_per_block(EPI_ARGMAX, MT) - 1) /
                            gemm_tiles_per_block(EPI_ARGMAX, MT));
   PROF(9, launch_argmax_accept(m->amax, nparts, rows, tree, draft, m->pred, res, hs));
-  kv->pending = rows;
-  kv->pending_tree = tree;
+  if (only_kind < 0) {
+    kv->pending = rows;
+    kv->pending_tree = tree;
+  }
   return ok();
 }
 
 pf_status pf_verify_step(pf_model *m, pf_kv_cache *kv, const pf_draft *draft, int32_t rows,
                          int32_t tree, float *logits, pf_verify_result *res, pf_stream s) {
   return verify_impl(m, kv, draft, rows, tree, logits, res, s, nullptr);
+}
+
+pf_status pf_verify_kernel_repeat(pf_model *m, pf_kv_cache *kv, const pf_draft *draft,
+                                  int32_t rows, int32_t tree, int32_t kind,
+                                  pf_verify_result *res, pf_stream s) {
+  if (kind < 0 || kind >= PF_PROF_MARKER)
+    return fail(PF_EINVAL, "pf_verify_kernel_repeat: kind %d out of range", kind);
+  return verify_impl(m, kv, draft, rows, tree, nullptr, res, s, nullptr, nullptr, kind);
+}
+
+pf_status pf_read_stream(const void *buf, int64_t bytes, uint32_t *sink, pf_stream s) {
+  if (!buf || !sink) return fail(PF_EINVAL, "pf_read_stream: null pointer");
+  if (((uintptr_t)buf & 15) || bytes <= 0 || bytes % 16384 || bytes >= ((int64_t)1 << 31))
+    return fail(PF_EINVAL, "pf_read_stream: %lld bytes at %p (16-byte aligned multiple of 16 KiB, "
+                "below 2 GiB)", (long long)bytes, buf);
+  int dev = 0, cus = 0;
+  HIPCHK(hipGetDevice(&dev));
+  HIPCHK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  HIPCHK(launch_read_stream(buf, (uint32_t)bytes, cus, sink, st(s)));
+  return ok();
+}
+
+pf_status pf_verify_step_trace(pf_model *m, pf_kv_cache *kv, const pf_draft *draft, int32_t rows,
+                               int32_t tree, float *logits, pf_verify_result *res, float *resid,
+                               pf_stream s) {
+  if (!resid) return fail(PF_EINVAL, "pf_verify_step_trace: null residual buffer");
+  return verify_impl(m, kv, draft, rows, tree, logits, res, s, nullptr, resid);
 }
 
 pf_status pf_verify_step_profiled(pf_model *m, pf_kv_cache *kv, const pf_draft *draft,

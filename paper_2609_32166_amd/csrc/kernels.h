@@ -175,6 +175,12 @@ hipError_t launch_prefill_rows(const int32_t *tokens, int n, int V, const int32_
                                const double *inv_freq, int hd, int32_t *rowinfo, float *rope,
                                int32_t *status, hipStream_t s);
 hipError_t launch_add_int(int32_t *p, int32_t v, hipStream_t s);
+// dst[r][c] = x[r][c] for the first `rows` rows of the fp32 residual stream
+// (row stride H in both)
+hipError_t launch_copy_rows(const float *x, int rows, int H, float *dst, hipStream_t s);
+// plain streaming read of bytes (< 2^31) at buf over `blocks` 256-thread blocks
+hipError_t launch_read_stream(const void *buf, uint32_t bytes, int blocks, uint32_t *sink,
+                              hipStream_t s);
 hipError_t launch_pack_row(bool bf16, const void *src, void *dst, int64_t ld, hipStream_t s);
 
 // tiled GEMM for prefill chunks (gemm_big.hip): Y[M x N] = X[M x K] W^T,

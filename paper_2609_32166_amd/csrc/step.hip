@@ -612,6 +612,58 @@ hipError_t launch_add_int(int32_t *p, int32_t v, hipStream_t s) {
   return hipGetLastError();
 }
 
+__global__ void k_copy_rows(const float *__restrict__ x, int64_t n, float *__restrict__ dst) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = x[i];
+}
+
+hipError_t launch_copy_rows(const float *x, int rows, int H, float *dst, hipStream_t s) {
+  const int64_t n = (int64_t)rows * H;
+  const unsigned blocks = (unsigned)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+  PF_TRY(launch_k(k_copy_rows, blocks, 256, s, x, n, dst));
+  return hipGetLastError();
+}
+
+// Plain streaming read of a buffer: wave w of the grid reads 1 KiB chunks
+// j * waves + w, eight chunks in flight per wave; chunks past the end load
+// nothing (out-of-range buffer offsets). The XOR of the data decides whether
+// a word is written, so the loads cannot be dropped.
+__global__ __launch_bounds__(256) void k_read_stream(const void *buf, uint32_t bytes, int n,
+                                                     uint32_t *sink) {
+  constexpr int D = 8;
+  const int lane = threadIdx.x & 63;
+  const uint64_t nw = (uint64_t)gridDim.x * 4, gw = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const rsrc_t r = make_rsrc(buf, bytes);
+  auto off = [&](int j) -> uint32_t {
+    const uint64_t o = ((uint64_t)j * nw + gw) * 1024 + lane * 16;
+    return o < bytes ? (uint32_t)o : kOOB;
+  };
+  uint4 ring[D];
+  uint4 acc = make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int u = 0; u < D; ++u) ring[u] = bload16_stream(r, off(u));
+  for (int i = 0; i < n; i += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      acc.x ^= ring[u].x; acc.y ^= ring[u].y; acc.z ^= ring[u].z; acc.w ^= ring[u].w;
+      ring[u] = bload16_stream(r, off(i + D + u));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = acc.x;
+}
+
+hipError_t launch_read_stream(const void *buf, uint32_t bytes, int blocks, uint32_t *sink,
+                              hipStream_t s) {
+  const int64_t chunks = bytes / 1024;
+  const int64_t waves = (int64_t)blocks * 4;
+  int n = (int)((chunks + waves - 1) / waves);
+  n = (n + 7) / 8 * 8;
+  PF_TRY(launch_k(k_read_stream, (unsigned)blocks, 256, s, buf, bytes, n, sink));
+  return hipGetLastError();
+}
+
 // One row-major activation row -> row 0 of the fragment-packed layout.
 template <typename T> __global__ void k_pack_row(const T *src, T *dst, int64_t ld) {
   for (int64_t k = threadIdx.x; k < ld; k += blockDim.x) dst[act_off<T>(0, k, ld)] = src[k];

@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import synth
-from pfharness import Gpu, rel_err_rows, tol_of
+from pfharness import Gpu, check_accept_against_oracle, rel_err_rows, tol_of
 
 pytestmark = pytest.mark.gpu
 
@@ -135,18 +135,47 @@ def test_prefill_3b_widths_two_layers(pf):
 
 
 @pytest.mark.slow
-def test_prefill_7b_widths_two_layers(pf):
-    """7B-class widths and the carry-forward lengths (6144 reused + 2048 new in
-    512-row chunks) at 2 layers, so the oracle finishes in under a minute."""
+def test_carry_forward_7b_widths_two_layers(pf):
+    """The carry-forward workload at 7B-class widths and lengths, 2 layers (so
+    the oracle finishes in about a minute): 6144 reused positions, 2048 new
+    tokens prefilled in 512-row chunks, then a K=16 retrieval-drafted verify
+    step on the cache the prefill left (8192 positions), compared with the
+    oracle's verify over the oracle's own prefill of the same tokens
+    (Section 3.4, prompt-prefix KV-state carryover; Section 3.2, single-pass
+    verification)."""
     wl = synth.WORKLOADS["7b_carry"]
     shape = wl.model.with_layers(2)
+    seed = synth.case_seed(wl, 0)
     w, kv_host, toks, gpu, kv_new, logits = _prefill_case(
-        pf, shape, synth.case_seed(wl, 0), wl.prefill_reuse, wl.prefill_new, wl.prefill_chunk)
+        pf, shape, seed, wl.prefill_reuse, wl.prefill_new, wl.prefill_chunk)
     om = oracle.Model(shape, w)
     ref = oracle.prefill(om, kv_host, toks, wl.prefill_new)
     r = ref["kv_new"]
     e = np.abs(kv_new - r).max(axis=(2, 3, 4)) / np.abs(r).max(axis=(2, 3, 4))
+    print(f"prefill: K/V max rel err {e.max():.3e}", flush=True)
     assert e.max() <= tol_of(shape), e
     assert rel_err_rows(logits[None], ref["logits_last"][None]).max() <= tol_of(shape)
+    # the verify step on the prefilled cache
+    P = wl.prefill_reuse + wl.prefill_new
+    kv_ext = np.concatenate([kv_host, _to_storage(shape, r)], axis=3)
+    store = synth.make_store(wl, seed)
+    ctx, _ = synth.make_context(wl, seed, store, hit=True)
+    st = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
+    gpu.prefix = P
+    out = gpu.step(st, ctx, wl.k_max)
+    od = oracle.lookup(store.tokens, store.seq_offsets, wl.ngram, ctx, wl.k_max)
+    assert out["rows"] == wl.k_max + 1
+    ores = oracle.verify_batched(om, kv_ext, od, out["rows"], False)
+    nn = od["n_nodes"]
+    err = rel_err_rows(out["logits"][:nn], ores["logits"][:nn])
+    kvv = Gpu.to_np(out["kv_rows"])[:, :, :, :nn, :]
+    kref = ores["kv_new"][:, :, :, :nn, :]
+    ekv = np.abs(kvv - kref).max(axis=(2, 3, 4)) / np.abs(kref).max(axis=(2, 3, 4))
+    print(f"verify after prefill ({nn} nodes): logits max rel err {err.max():.3e}, K/V "
+          f"{ekv.max():.3e}, accept {int(out['res']['accept_len'])}", flush=True)
+    assert err.max() <= tol_of(shape), err
+    assert ekv.max() <= tol_of(shape), ekv
+    check_accept_against_oracle(out["res"], ores, ores["logits"], tol_of(shape))
+    assert out["kv_len"] == P + int(out["res"]["accept_len"]) + 1
     del gpu
     gc.collect()
