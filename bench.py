@@ -3,12 +3,19 @@
 A step is one decoding iteration: draft lookup -> verify forward (all layers,
 lm_head, greedy accept) -> KV commit, on seeded synthetic inputs already
 resident in HBM. The cache length and context are reset after every commit
-so the cached prefix P stays fixed. Default workload: the 3B-class bf16
-decoder, K = 16 linear draft over a 4096-token prefix.
+so the cached prefix P stays fixed. Default workload: the 7B-class bf16
+decoder, K = 32 linear draft over an 8192-token prefix (the largest
+single-GPU configuration); the line nests the 3B-class linear and tree
+workloads and the 7B carry-forward workload (prefill, then a K = 16 verify on
+the cache the prefill wrote), each with its own step time and roofline.
 
 Prints one JSON line. `value` is achieved HBM bandwidth of the whole step:
 algorithmic bytes (every weight once + the KV prefix read + the draft rows'
-KV read and written) divided by the measured step time.
+KV read and written) divided by the measured step time. `roofline` is the
+step's dominant kernel (the gate/up projection with SwiGLU): its algorithmic
+bytes per launch over its average launch duration, timed with HIP events as
+a graph of only that kernel's launches (every layer's, on the step's own
+buffers), with no correction subtracted.
 """
 from __future__ import annotations
 
@@ -40,15 +47,13 @@ def gate_up_bytes(wl) -> int:
     return esz * (2 * m.ffn * m.hidden + M * m.hidden + M * m.ffn)
 
 
-# HBM traffic of the gate/up kernel per launch, 3B workload, from two
+# HBM traffic of the gate/up kernel per launch, per workload, from two
 # rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) scaled by the counters'
-# reading for a 256 MiB device copy; the command and the figures are in
-# profiles/verify_step_3b_hbm_traffic.md. Valid only for the GEMM source it was
-# taken on (its SHA-256 below): after any change to that file it is reported
-# as null until measured again.
-GATE_UP_TRAFFIC = {"workload": "3b",
-                   "gemm_source_sha256": "c3791c7e1370cb73dfdb536fc3008739433edf066d22d7f32558f1b64323f5a8",
-                   "bytes": 91460000}
+# reading for a plain device copy of known size; commands and figures in
+# profiles/. Valid only for the GEMM source the counters were taken on (its
+# SHA-256): after any change to that file a workload's entry reads as null
+# until measured again.
+GATE_UP_TRAFFIC = {}
 
 
 def measured_traffic(wl):
@@ -56,8 +61,8 @@ def measured_traffic(wl):
     src = os.path.join(ROOT, "paper_2609_32166_amd", "csrc", "gemm.hip")
     with open(src, "rb") as f:
         digest = hashlib.sha256(f.read()).hexdigest()
-    t = GATE_UP_TRAFFIC
-    if t["bytes"] is None or t["workload"] != wl.name or t["gemm_source_sha256"] != digest:
+    t = GATE_UP_TRAFFIC.get(wl.name)
+    if t is None or t["gemm_source_sha256"] != digest:
         return None, "not measured for this GEMM source and workload"
     return t["bytes"], "rocprofv3 PMC FETCH_SIZE + WRITE_SIZE, copy-calibrated"
 
@@ -502,35 +507,57 @@ def carry_timings(torch, pf, wl, model, kv_host):
             "speedup_vs_prefill": round(pre_ms * 1e3 / us, 1)}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="3b", choices=sorted(synth.WORKLOADS))
-    ap.add_argument("--profile-steps", type=int, default=5)
-    ap.add_argument("--cpu-layers", type=int, default=0, help="0: every layer")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
-    ap.add_argument("--no-sweep", action="store_true",
-                    help="skip the phase split, percentiles, greedy and K-sweep timings")
-    ap.add_argument("--no-loop", action="store_true", help="skip the closed-loop decode timings")
-    ap.add_argument("--copy-calibration", type=int, default=0,
-                    help="also run a plain device copy of this many MiB (for counter scaling)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
-              f"sharding of this path is a design note, not a measured configuration",
-              file=sys.stderr)
-        sys.exit(2)
+def read_ceiling(torch, pf, nbytes=1 << 30, reps=10):
+    """Achievable HBM read rate: a plain streaming kernel (pf_read_stream)
+    over a buffer four times the 256 MB last-level cache, timed as a graph of
+    `reps` calls."""
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    pf.pf_read_stream(buf, sink)
+    g = _capture(torch, lambda: [pf.pf_read_stream(buf, sink) for _ in range(reps)])
+    ms = _time_graph(torch, g, 5) / reps
+    del buf, sink, g
+    torch.cuda.empty_cache()
+    return {"GBps": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes,
+            "us_per_read": round(ms * 1e3, 2),
+            "kernel": "pf_read_stream (one block per CU, 8 x 16 B loads in flight per lane)"}
 
-    import torch
 
-    import paper_2609_32166_amd as pf
+def kernel_times(torch, pf, wl, model, kv, c, ctx, st, draft, res, min_launches=24):
+    """Per-kind kernel durations of the verify step: for every launch kind, a
+    graph of only that kind's launches (pf_verify_kernel_repeat, every
+    layer's, repeated until at least `min_launches` launches), timed with
+    events around the replays; duration per launch = graph time / launches.
+    No correction is subtracted, so each figure includes the kernel boundary
+    inside a graph. Launch counts per kind come from one profiled step."""
+    max_nodes = wl.max_nodes if wl.tree else 64
+    n_cand = wl.n_cand if wl.tree else 1
+    pf.pf_kv_set_len(kv, wl.prefix)
+    pf.pf_context_init(c, len(ctx))
+    pf.pf_draft_lookup(st, c, wl.k_max, wl.tree, n_cand, max_nodes, draft)
+    _, cnt = pf.pf_verify_step_profiled(model, kv, draft, wl.rows, wl.tree, None, res)
+    out = {}
+    for kind, name in enumerate(pf.PROF_NAMES[:pf.PF_PROF_KINDS - 1]):
+        per_step = int(cnt[kind])
+        if per_step == 0:
+            continue
+        reps = max(1, (min_launches + per_step - 1) // per_step)
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    wl = synth.WORKLOADS[args.workload]
+        def fn():
+            for _ in range(reps):
+                pf.pf_verify_kernel_repeat(model, kv, draft, wl.rows, wl.tree, kind, res)
+        ms = _time_graph(torch, _capture(torch, fn), 10)
+        us = 1e3 * ms / (reps * per_step)
+        out[name] = {"avg_launch_us": round(us, 2), "launches_per_step": per_step,
+                     "ms_per_step": round(us * per_step / 1e3, 4)}
+    return out
+
+
+def measure(torch, pf, name, args, headline):
+    """Set up one workload, time its step, its kernels and its roofline; with
+    `headline` also the phase split, K sweep, cosine retrieval, closed-loop
+    decoding, carryover and the oracle's CPU baseline."""
+    wl = synth.WORKLOADS[name]
     shape = wl.model
     seed = synth.case_seed(wl, 0)
     t0 = time.perf_counter()
@@ -538,7 +565,7 @@ def main():
     kv_host = synth.make_kv_prefix(shape, seed, wl.prefix)
     store = synth.make_store(wl, seed)
     ctx, info = synth.make_context(wl, seed, store, hit=True)
-    log(f"inputs generated in {time.perf_counter() - t0:.1f} s (hit={info['hit']})")
+    log(f"[{name}] inputs generated in {time.perf_counter() - t0:.1f} s (hit={info['hit']})")
 
     t0 = time.perf_counter()
     wdev = pf.weights_to_device(w, shape.dtype)
@@ -551,12 +578,14 @@ def main():
     kvd = pf.array_to_device(kv_host)
     prefill = None
     if wl.prefill_new:
-        # carry-forward: keep the reused prefix, prefill the new chunk, then verify
+        # carry-forward: keep the reused prefix, prefill the new chunk; the
+        # verify step below then runs on the cache the prefill wrote
         ptoks = torch.from_numpy(synth.make_prefill_tokens(wl, seed, wl.prefill_new)).cuda()
         plog = torch.zeros(shape.vocab, device="cuda")
+        reuse = kvd[:, :, :, :wl.prefill_reuse].contiguous()
         pre_ms = []
         for it in range(3):
-            pf.pf_kv_import(kv, kvd[:, :, :, :wl.prefill_reuse].contiguous(), wl.prefill_reuse)
+            pf.pf_kv_import(kv, reuse, wl.prefill_reuse)
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
@@ -564,24 +593,28 @@ def main():
             e1.record()
             torch.cuda.synchronize()
             pre_ms.append(e0.elapsed_time(e1))
+        del reuse
+        assert int(kv.len.item()) == wl.prefix
         pms = min(pre_ms[1:])
         fl = prefill_flops(wl)
         prefill = {"ms": round(pms, 3), "tflops": round(fl / (pms * 1e-3) / 1e12, 1),
                    "frac_of_bf16_mfma_peak": round(fl / (pms * 1e-3) / 2.5e15, 4),
                    "algorithmic_tflop": round(fl / 1e12, 2),
-                   "reused": wl.prefill_reuse, "new": wl.prefill_new, "chunk": wl.prefill_chunk}
-        log(f"prefill {wl.prefill_new} tokens after {wl.prefill_reuse}: {pms:.2f} ms "
+                   "reused": wl.prefill_reuse, "new": wl.prefill_new, "chunk": wl.prefill_chunk,
+                   "verify_cache": "the prefilled cache (no re-import)"}
+        log(f"[{name}] prefill {wl.prefill_new} tokens after {wl.prefill_reuse}: {pms:.2f} ms "
             f"({prefill['tflops']} TFLOP/s)")
-        # the verify step then runs on the synthetic full prefix (same length)
-    pf.pf_kv_import(kv, kvd, wl.prefix)
+    else:
+        pf.pf_kv_import(kv, kvd, wl.prefix)
     st = pf.pf_store_build(store.tokens, store.seq_offsets, wl.ngram)
     c = pf.Context(ctx, len(ctx) + 2 * 65)
     draft, res = pf.new_draft(), pf.new_result()
     torch.cuda.synchronize()
     del kvd
-    log(f"model {model.bytes / 1e9:.2f} GB on device, set up in {time.perf_counter() - t0:.1f} s")
+    log(f"[{name}] model {model.bytes / 1e9:.2f} GB on device, set up in "
+        f"{time.perf_counter() - t0:.1f} s")
 
-    if args.copy_calibration:
+    if headline and args.copy_calibration:
         # a plain copy of known size: reference for the FETCH_SIZE/WRITE_SIZE counters
         src = torch.empty(args.copy_calibration << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -611,14 +644,7 @@ def main():
     ms = ms_eager
     if not args.no_graph:
         # the whole step (resets, lookup, verify, commit) as one HIP graph
-        graph = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            step()
-        torch.cuda.current_stream().wait_stream(side)
-        with torch.cuda.graph(graph):
-            step()
+        graph = _capture(torch, step)
         for _ in range(args.warmup):
             graph.replay()
         torch.cuda.synchronize()
@@ -628,93 +654,140 @@ def main():
         stop.record()
         torch.cuda.synchronize()
         ms = start.elapsed_time(stop) / args.steps
+        del graph
     r = pf.read_result(res)
     d = pf.read_draft(draft)
-    log(f"step {ms:.3f} ms (eager {ms_eager:.3f} ms), draft {int(d['n_nodes']) - 1} tokens, "
-        f"accepted {int(r['accept_len'])}")
+    log(f"[{name}] step {ms:.3f} ms (eager {ms_eager:.3f} ms), draft {int(d['n_nodes']) - 1} "
+        f"tokens, accepted {int(r['accept_len'])}")
 
     extra = {}
-    if not args.no_graph and not args.no_sweep:
+    if headline and not args.no_graph and not args.no_sweep:
         extra = phase_timings(torch, pf, wl, model, kv, st, c, ctx, draft, res, args, ms, step)
-        d = pf.read_draft(draft)  # the sweep reuses the buffers; restore the main step
         step()
         torch.cuda.synchronize()
         r = pf.read_result(res)
         d = pf.read_draft(draft)
 
-    # per-kernel durations: an event pair around every launch, the stream held
-    # until the step is enqueued, the cost of an empty pair subtracted
-    tot = np.zeros(pf.PF_PROF_KINDS)
-    cnt = np.zeros(pf.PF_PROF_KINDS, np.int64)
-    for _ in range(args.profile_steps):
-        pf.pf_kv_set_len(kv, wl.prefix)
-        pf.pf_context_init(c, len(ctx))
-        pf.pf_draft_lookup(st, c, wl.k_max, wl.tree, n_cand, max_nodes, draft)
-        m_, c_ = pf.pf_verify_step_profiled(model, kv, draft, wl.rows, wl.tree, None, res)
-        tot += m_
-        cnt += c_
-    kernels = {}
-    for i, name in enumerate(pf.PROF_NAMES):
-        if cnt[i]:
-            kernels[name] = {"ms_per_step": round(tot[i] / args.profile_steps, 4),
-                             "avg_launch_us": round(1000 * tot[i] / cnt[i], 2),
-                             "launches_per_step": int(cnt[i] // args.profile_steps)}
-    gu_us = 1000 * tot[6] / cnt[6] if cnt[6] else float("nan")
-    pair_us = 1000 * tot[10] / cnt[10] if cnt[10] else float("nan")
-    gu_gbs = gate_up_bytes(wl) / (gu_us * 1e-6) / 1e9 if cnt[6] else float("nan")
+    kernels = kernel_times(torch, pf, wl, model, kv, c, ctx, st, draft, res)
+    # leave the buffers as a normal step does
+    step()
+    torch.cuda.synchronize()
+    gu_us = kernels["gate_up"]["avg_launch_us"]
+    gu_gbs = gate_up_bytes(wl) / (gu_us * 1e-6) / 1e9
     traffic, traffic_note = measured_traffic(wl)
     nbytes = wl.verify_bytes()
     gbs = nbytes / (ms * 1e-3) / 1e9
     K = wl.k_max
     out = {
-        "metric": METRIC,
-        "value": round(gbs, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "ms_per_step_eager": round(ms_eager, 4),
-        "timing": "HIP graph replay of the whole step" if not args.no_graph else "eager launches",
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": shape.dtype,
-        "data": "synthetic (seeded random-init weights N(0,0.02), N(0,1) KV prefix, Zipf(1.1) store)",
+        "GBps": round(gbs, 2),
+        "hbm_frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
         "config": {"workload": f"{wl.name}: {shape.n_layers}L H{shape.hidden} "
                                f"{shape.n_heads}q/{shape.n_kv_heads}kv hd{shape.head_dim} "
                                f"F{shape.ffn} V{shape.vocab}, P={wl.prefix}, K={K} "
                                f"{'tree' if wl.tree else 'linear'}, {wl.ngram}-gram lookup",
                    "rows": wl.rows, "prefix": wl.prefix, "k_max": K,
                    "algorithmic_bytes_per_step": nbytes},
-        "hbm_frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
         "accepted_tokens_per_s": {f"l_acc={l}": round((l + 1) / (ms * 1e-3), 1)
                                   for l in (0, K // 2, K)},
         "roofline": {"bound": "hbm", "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "k_gemm<bf16,*,EPI_SWIGLU> (gate/up projection + SwiGLU)",
-                     "bytes_per_launch": gate_up_bytes(wl),
-                     "avg_launch_us": round(gu_us, 2),
-                     "event_pair_us_subtracted": round(pair_us, 2),
+                     "bytes_per_launch": gate_up_bytes(wl), "avg_launch_us": gu_us,
+                     "timing": "graph of the kernel's launches alone (every layer), events around "
+                               "the replays, nothing subtracted",
                      "traffic_source": traffic_note},
         "kernels": kernels,
+        "last_step": {"draft_tokens": int(d["n_nodes"]) - 1, "accept_len": int(r["accept_len"])},
     }
-    out.update(extra)
-    if not args.no_graph and not args.no_sweep:
-        out["cosine_retrieval"] = cosine_timings(torch, pf, wl, store, model, res, st, ctx)
     if prefill is not None:
         out["prefill"] = prefill
-    if not args.no_loop and not wl.tree:
+    out.update(extra)
+    if headline and not args.no_graph and not args.no_sweep:
+        out["cosine_retrieval"] = cosine_timings(torch, pf, wl, store, model, res, st, ctx)
+    if headline and not args.no_loop and not wl.tree:
         out["decode_loop"] = decode_loop(torch, pf, wl, model, kv_host, store, ctx)
-    if not args.no_sweep and wl.model.dtype == "bf16":
+    if headline and not args.no_sweep and wl.model.dtype == "bf16":
         out["rolling_image_carryover"] = carry_timings(torch, pf, wl, model, kv_host)
-    if not args.no_cpu_baseline:
+    if headline and not args.no_cpu_baseline:
         od = {"n_nodes": int(d["n_nodes"]), "token": np.array(d["token"][:int(d["n_nodes"])]),
               "parent": np.array(d["parent"][:int(d["n_nodes"])]),
               "depth": np.array(d["depth"][:int(d["n_nodes"])])}
         log("timing the oracle on the host ...")
         nl = args.cpu_layers if args.cpu_layers > 0 else shape.n_layers
         out["cpu_baseline"] = cpu_baseline(wl, w, kv_host, od, min(nl, shape.n_layers))
+    del model, kv, st
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="7b", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--nested", default="3b,3b_tree,7b_carry",
+                    help="workloads measured beside the headline one (comma list, '' for none)")
+    ap.add_argument("--cpu-layers", type=int, default=0,
+                    help="layers of the oracle's CPU sample (0: every layer)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the phase split, percentiles, greedy and K-sweep timings")
+    ap.add_argument("--no-loop", action="store_true", help="skip the closed-loop decode timings")
+    ap.add_argument("--copy-calibration", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (for counter scaling)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
+              f"sharding of this path is a design note, not a measured configuration",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_32166_amd as pf
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    ceiling = read_ceiling(torch, pf)
+    log(f"read-stream ceiling {ceiling['GBps']} GB/s")
+    head = measure(torch, pf, args.workload, args, headline=True)
+    nested = {}
+    for n in [x for x in args.nested.split(",") if x and x != args.workload]:
+        nested[n] = measure(torch, pf, n, args, headline=False)
+        nested[n]["roofline"]["frac_of_measured_read_ceiling"] = round(
+            nested[n]["roofline"]["achieved"] / ceiling["GBps"], 4)
+    head["roofline"]["measured_read_ceiling_GBps"] = ceiling["GBps"]
+    head["roofline"]["frac_of_measured_read_ceiling"] = round(
+        head["roofline"]["achieved"] / ceiling["GBps"], 4)
+    K = wl.k_max
+    out = {
+        "metric": METRIC,
+        "value": head.pop("GBps"),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head.pop("ms_per_step"),
+        "timing": "HIP graph replay of the whole step" if not args.no_graph else "eager launches",
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.model.dtype,
+        "data": "synthetic (seeded random-init weights N(0,0.02), N(0,1) KV prefix, Zipf(1.1) store)",
+        "config": head.pop("config"),
+        "hbm_frac_of_peak": head.pop("hbm_frac_of_peak"),
+        "roofline": head.pop("roofline"),
+        "read_ceiling": ceiling,
+    }
+    out.update(head)
+    if nested:
+        out["workloads"] = nested
     print(json.dumps(out), flush=True)
 
 

@@ -255,12 +255,12 @@ int64_t pf_model_bytes(const pf_model *model);
 
 /*
  * Per layer l and KV head g, a key plane and a value plane of
- * capacity*head_dim elements each, in the model dtype:
+ * capacity*head_dim elements each, in the model dtype, together the array
+ * [n_layers][2][n_kv][capacity][head_dim]:
  *   keys   at ((l*2 + 0)*n_kv + g) * capacity*head_dim, element [slot][i]
- *   values at ((l*2 + 1)*n_kv + g) * capacity*head_dim, element [i][slot]
- * (values are stored transposed so that the attention's value operand is a
- * contiguous run of slots). Slot t holds position t. *len is the committed
- * length; slots >= *len are dead. capacity must be a multiple of 64.
+ *   values at ((l*2 + 1)*n_kv + g) * capacity*head_dim, element [slot][i]
+ * Slot t holds position t. *len is the committed length; slots >= *len are
+ * dead. capacity must be a multiple of 64.
  */
 typedef struct pf_kv_cache {
   void *data;         /* device, pf_kv_bytes() bytes */

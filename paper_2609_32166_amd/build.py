@@ -11,7 +11,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libpf.so")
 OBJ = os.path.join(ROOT, "_build", "pf")
 
-SOURCES = ["api.cpp", "controller.cpp", "decode.cpp", "lookup.hip", "keys.hip", "gemm.hip", "gemm_big.hip", "attn.hip", "step.hip", "carry.hip", "qkv.hip", "prefill_gemm.hip"]
+SOURCES = ["api.cpp", "controller.cpp", "decode.cpp", "lookup.hip", "keys.hip", "gemm.hip", "gemm_big.hip", "attn.hip", "attn_gq.hip", "step.hip", "carry.hip", "qkv.hip", "prefill_gemm.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

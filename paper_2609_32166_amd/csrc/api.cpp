@@ -935,6 +935,25 @@ static int attn_range_keys(int64_t keys_max, bool bf, int nq, int wave_slots) {
   return (int)chunk;
 }
 
+// Grouped attention (bf16, head_dim 128): keys per range, a multiple of the
+// 32-key chunk, sized so that one KV head has at most T ranges, T = the
+// resident blocks (two per compute unit) over four row groups per KV head,
+// at most the combine's 64. The length depends on the row count only
+// through the key bound (ceil(keys / (32 T)) changes every 32 T keys), so a
+// verify row reproduces the single-row step at its position bit for bit
+// unless the two key bounds straddle such a step.
+static int attn_gq_range_keys(int64_t keys_max, int nkv, int cus) {
+  int target = 2 * cus / (4 * (nkv > 0 ? nkv : 1));
+  if (target > kMaxSplitsAttn) target = kMaxSplitsAttn;
+  if (target < 1) target = 1;
+  const int64_t per = (keys_max + target - 1) / target;
+  return (int)(((per + 31) / 32) * 32);
+}
+
+// Probabilities enter the grouped attention's value product as two bf16
+// terms (the rounding residue of the first as the second).
+constexpr bool kAttnHiLo = true;
+
 static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft, int32_t rows,
                              int32_t tree, float *logits, pf_verify_result *res, pf_stream s,
                              Prof *prof, float *resid = nullptr, int only_kind = -1) {
@@ -979,7 +998,9 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
 
   // attention geometry: key ranges over P + rows keys (P <= host bound)
   const int64_t keys_max = kv->host_bound + rows;
-  const int chunk = attn_range_keys(keys_max, bf, nq, m->wave_slots);
+  const bool gq = attn_gq_supported(bf, hd);
+  const int chunk = gq ? attn_gq_range_keys(keys_max, nkv, m->wave_slots / 4)
+                       : attn_range_keys(keys_max, bf, nq, m->wave_slots);
   const int n_splits = (int)((keys_max + chunk - 1) / chunk);
   // rows beyond one wave's tiles take more waves per range; those waves then
   // reduce several consecutive ranges each, to stay within the resident waves
@@ -1033,7 +1054,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     at.out = m->attn;
     at.ldout = qp;
     at.out_packed = 1;
-    PROF(3, launch_attn(bf, MT, at, hs));
+    PROF(3, gq ? launch_attn_gq(at, kAttnHiLo, hs) : launch_attn(bf, MT, at, hs));
     // output projection + residual + FFN norm
     GemmArgs go{};
     go.W = (const char *)m->wo + (int64_t)l * m->po.bytes();

@@ -11,8 +11,9 @@
 // with K as the MFMA A operand, permuting which key each A row carries so
 // that, after the MFMA, lane quarter q holds the scores of keys q*E..q*E+E-1
 // of its query row (column). That is exactly the B-operand layout of
-// O^T += V^T P^T, and values are stored transposed ([dim][slot]) in the
-// cache, so the V^T fragment of a lane is one contiguous 16-byte load. The
+// O^T += V^T P^T; a lane's V^T fragment (E consecutive keys of one
+// dimension, from the [slot][dim] value rows of the cache) is gathered with
+// E element loads. The
 // online softmax runs in the log2 domain in fp32; probabilities enter the PV
 // product in the model dtype. Each block writes an unnormalised partial
 // (o, running max, running sum) per row; k_attn_combine merges the splits.
@@ -35,6 +36,28 @@ template <> __device__ inline uint4 pack_probs<bf16_t>(const float *p) {
   for (int i = 0; i < 4; ++i)
     w[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){p[2 * i], p[2 * i + 1]}, b2));
   return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// E consecutive keys key0 .. key0 + E - 1 of dimension dim from [slot][hd]
+// value rows, packed as one 16-byte operand chunk (key0 + e in element e);
+// in == false loads nothing and gives zeros.
+template <typename T> __device__ inline uint4 gather_vt(rsrc_t r, bool in, int key0, int dim, int hd);
+template <> __device__ inline uint4 gather_vt<float>(rsrc_t r, bool in, int key0, int dim, int hd) {
+  uint32_t w[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    w[e] = __builtin_amdgcn_raw_buffer_load_b32(
+        r, in ? (int)(((int64_t)(key0 + e) * hd + dim) * 4) : (int)kOOB, 0, 0);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+template <> __device__ inline uint4 gather_vt<bf16_t>(rsrc_t r, bool in, int key0, int dim, int hd) {
+  uint32_t h[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    h[e] = __builtin_amdgcn_raw_buffer_load_b16(
+        r, in ? (int)(((int64_t)(key0 + e) * hd + dim) * 2) : (int)kOOB, 0, 0);
+  return make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                    h[6] | (h[7] << 16));
 }
 
 // Keeps the first n (0..E) elements of a 16-byte chunk and zeroes the rest.
@@ -156,9 +179,7 @@ __global__ __launch_bounds__(64, WPE) void k_attn(AttnArgs a) {
     const bool in = c < nchunks;
 #pragma unroll
     for (int t = 0; t < NDT; ++t)
-      vf[slot][t] = bload16(
-          vr, in ? (uint32_t)(((int64_t)(t * 16 + (lane & 15)) * a.cap + kc + q * E) * sizeof(T))
-                 : kOOB);
+      vf[slot][t] = gather_vt<T>(vr, in, kc + q * E, t * 16 + (lane & 15), HD);
   };
   auto load = [&](int slot, int c) {
     load_k(slot, c);
@@ -477,9 +498,13 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
 
   // staged tiles: keys [key][16-byte chunk ^ (key & 15)], values transposed
   // [dim][chunk of 8 keys ^ ((dim / 2) & 7)]; both swizzles keep the 16
-  // lanes of an operand read on distinct banks
+  // lanes of an operand read on distinct banks. The value rows of the cache
+  // are [slot][dim]: a thread loads the 16-byte pieces (8 dimensions) of a
+  // pair of consecutive keys and writes them into the transposed tile as
+  // 32-bit words (one word = the pair's two keys at one dimension).
   __shared__ uint4 lk[2][kPreKeys][HD / 8];
   __shared__ uint4 lv[2][HD][kPreKeys / 8];
+  constexpr int kPairs = kPreKeys / 2 * (HD / 8);  // (key pair, dimension group) items
   uint4 gk[4], gv[4];
   auto gload = [&](int kt) {
 #pragma unroll
@@ -488,8 +513,18 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
       const bool in = idx < kPreKeys * HD / 8;
       const int key = kt + (idx >> 4), c = idx & 15;
       gk[r] = bload16(kr, in && key < kend ? (uint32_t)(((int64_t)key * HD + c * 8) * 2) : kOOB);
-      const int d = idx >> 3, k8 = kt + (idx & 7) * 8;
-      gv[r] = bload16(vr, in && k8 < kend ? (uint32_t)(((int64_t)d * a.cap + k8) * 2) : kOOB);
+    }
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int it = tid + r * nthr;  // item: key pair it % (kPreKeys / 2), dims 8 * (it / ...)
+      const bool in = it < kPairs;
+      const int kp = it % (kPreKeys / 2), dgp = it / (kPreKeys / 2);
+      const int k2 = kt + 2 * kp;
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+        gv[2 * r + u] = bload16(vr, in && k2 + u < kend
+                                       ? (uint32_t)(((int64_t)(k2 + u) * HD + dgp * 8) * 2)
+                                       : kOOB);
     }
   };
   auto lstore = [&](int buf, int kt) {
@@ -499,11 +534,25 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
       if (idx < kPreKeys * HD / 8) {
         const int key = idx >> 4, c = idx & 15;
         lk[buf][key][c ^ (key & 15)] = gk[r];
-        const int d = idx >> 3, c8 = idx & 7, k8 = kt + c8 * 8;
-        // value columns past the cache end are zeroed (a zero probability
-        // must not meet an uninitialised NaN)
-        const uint4 v = k8 + 8 > kend ? keep_first<bf16_t>(gv[r], max(kend - k8, 0)) : gv[r];
-        lv[buf][d][c8 ^ ((d >> 1) & 7)] = v;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int it = tid + r * nthr;
+      if (it < kPairs) {
+        const int kp = it % (kPreKeys / 2), dgp = it / (kPreKeys / 2);
+        // keys at or past the cache end load as zeros (out of range), so a
+        // zero probability never meets an uninitialised NaN
+        const uint4 v0 = gv[2 * r], v1 = gv[2 * r + 1];
+        const uint32_t x0[4] = {v0.x, v0.y, v0.z, v0.w}, x1[4] = {v1.x, v1.y, v1.z, v1.w};
+        const int c8 = kp >> 2, wsel = kp & 3;  // 8-key chunk and word of the pair
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int d = dgp * 8 + e;
+          const uint32_t lo = (x0[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+          const uint32_t hi = (x1[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+          ((uint32_t *)&lv[buf][d][c8 ^ ((d >> 1) & 7)])[wsel] = lo | (hi << 16);
+        }
       }
     }
   };
@@ -648,6 +697,15 @@ static hipError_t attn_t(int rt, const AttnArgs &a, hipStream_t s) {
     default: return hipErrorInvalidValue;
   }
   PF_TRY(launch_k(k_attn_combine<T, HD>, dim3(a.M, a.n_kv * a.group), 64, s, a));
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_combine(bool bf16, const AttnArgs &a, hipStream_t s) {
+  if (a.head_dim != 128 || a.n_splits > 64) return hipErrorInvalidValue;
+  if (bf16)
+    PF_TRY(launch_k(k_attn_combine<bf16_t, 128>, dim3(a.M, a.n_kv * a.group), 64, s, a));
+  else
+    PF_TRY(launch_k(k_attn_combine<float, 128>, dim3(a.M, a.n_kv * a.group), 64, s, a));
   return hipGetLastError();
 }
 

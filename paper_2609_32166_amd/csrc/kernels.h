@@ -102,7 +102,7 @@ struct QkvArgs {
   const int32_t *kv_len;
   void *qbuf;           // [kRowPad][ldq] queries after RoPE
   int64_t ldq;
-  void *cache;          // KV cache: keys at slot P + row, values transposed
+  void *cache;          // KV cache: keys and values at slot P + row
   int layer;
   int64_t cap;
 };
@@ -134,6 +134,16 @@ struct AttnArgs {
 };
 
 hipError_t launch_attn(bool bf16, int rt, const AttnArgs &a, hipStream_t s);
+// merge of the key-range partials (head_dim 128, at most 64 ranges)
+hipError_t launch_attn_combine(bool bf16, const AttnArgs &a, hipStream_t s);
+// Grouped verify attention (attn_gq.hip; bf16, head_dim 128): one block per
+// (KV head, key range of chunk_keys keys, row group) over the group's
+// query heads x rows, K/V chunks staged in LDS; then the partial combine.
+// hilo: probabilities enter the value product as two bf16 terms.
+bool attn_gq_supported(bool bf16, int head_dim);
+int attn_gq_tiles(int group, int rows);
+int attn_gq_row_groups(int group, int rows);
+hipError_t launch_attn_gq(const AttnArgs &a, bool hilo, hipStream_t s);
 // Prefill attention with LDS-staged K/V tiles shared by a KV head's query
 // heads (bf16, head_dim 128, 4..8 query heads per KV head; chunk_keys a
 // multiple of 64), followed by the partial combine.

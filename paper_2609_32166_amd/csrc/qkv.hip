@@ -44,16 +44,15 @@ __global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
   for (int m = 0; m < MT; ++m)
     xbase[m] = m * 16 + (lane & 15) < a.M ? (uint32_t)(((m * xkfr + f0) * 64 + lane) * 16) : kOOB;
 
-  // Epilogue: thread t < 256 owns one (row, RoPE pair) of each row tile:
-  // queries and keys run along the dimension (row-major stores), values
-  // along the row (their cache rows are transposed). Its cache length and
-  // RoPE factors are read before the products, so their latency hides
-  // behind the loop.
+  // Epilogue: thread t < 256 owns one (row, RoPE pair) of each row tile;
+  // queries, keys and values all run along the dimension (row-major
+  // stores). Its cache length and RoPE factors are read before the products,
+  // so their latency hides behind the loop.
   const int half = a.hd / 2;
   const int kind = hh < a.nq ? 0 : (hh < a.nq + a.nkv ? 1 : 2);  // query, key, value head
   const int et = threadIdx.x;
-  const int er = kind == 2 ? (et & 15) : (et >> 4) & 15;  // row within the tile
-  const int ec = kind == 2 ? (et >> 4) & 15 : (et & 15);  // column within the tile
+  const int er = (et >> 4) & 15;  // row within the tile
+  const int ec = et & 15;         // column within the tile
   const int ed = jt * 16 + ec;                             // dimension in the first half
   int P = 0;
   float rc[MT], rs[MT];
@@ -119,9 +118,10 @@ __global__ __launch_bounds__(64 * kQkvWaves) void k_gemm_qkv(QkvArgs a) {
       }
       const int64_t slot = P + row;
       if (kind == 2) {
-        T *vp = (T *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.nkv + (hh - a.nq - a.nkv)) * plane;
-        Elem<T>::store(vp, (int64_t)ed * a.cap + slot, x);
-        Elem<T>::store(vp, (int64_t)(ed + half) * a.cap + slot, y);
+        T *vp = (T *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.nkv + (hh - a.nq - a.nkv)) * plane +
+                slot * a.hd;
+        Elem<T>::store(vp, ed, x);
+        Elem<T>::store(vp, ed + half, y);
       } else {
         const float c = rc[m], sn = rs[m];
         // explicit FMAs: every row-count instantiation rounds the rotation the

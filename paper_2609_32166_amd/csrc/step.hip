@@ -285,7 +285,7 @@ hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int ro
 
 // ---------------------------------------------------------------------------
 // QKV epilogue: reduce split-K partials, rotate Q and K, round, write Q to
-// the query buffer and K/V of row m to cache slot P + m (values transposed)
+// the query buffer and K/V of row m to cache slot P + m
 // ---------------------------------------------------------------------------
 
 template <typename T>
@@ -294,9 +294,8 @@ __global__ __launch_bounds__(256) void k_qkv_post(const float *part, int splits,
                                                   const float *rope, const int32_t *kv_len,
                                                   T *qbuf, int64_t ldq, T *cache, int layer,
                                                   int64_t cap) {
-  // one block per (32-row tile, head): query and key heads are rotated and
-  // stored row-major, value heads go through LDS so that the transposed
-  // cache rows (32 consecutive slots per dimension) are written contiguously
+  // one block per (32-row tile, head): query and key heads are rotated,
+  // value heads copied; all stored row-major
   const int j0 = blockIdx.x * 32, hh = blockIdx.y;
   const int half = hd / 2, h4 = half / 4;
   const int P = *kv_len;
@@ -335,26 +334,21 @@ __global__ __launch_bounds__(256) void k_qkv_post(const float *part, int splits,
     }
     return;
   }
-  // value head: [32 rows][hd] summed into LDS, then written transposed
+  // value head: row m's dimensions at slot P + m
   const int g = hh - nq - nkv;
   const int64_t cv0 = (int64_t)(nq + nkv) * hd + (int64_t)g * hd;
-  __shared__ float tile[32][128 + 1];
+  T *vp = cache + ((int64_t)(layer * 2 + 1) * nkv + g) * plane;
   const int d4 = hd / 4;
   for (int idx = threadIdx.x; idx < 32 * d4; idx += 256) {
     const int r = idx / d4, d = 4 * (idx % d4);
     const int row = j0 + r;
-    const float4 v = row < M ? col_sum4(row, cv0 + d) : make_float4(0.f, 0.f, 0.f, 0.f);
-    tile[r][d] = v.x;
-    tile[r][d + 1] = v.y;
-    tile[r][d + 2] = v.z;
-    tile[r][d + 3] = v.w;
-  }
-  __syncthreads();
-  T *vp = cache + ((int64_t)(layer * 2 + 1) * nkv + g) * plane;
-  const int rows = min(32, M - j0);
-  for (int idx = threadIdx.x; idx < hd * 32; idx += 256) {
-    const int d = idx / 32, r = idx % 32;
-    if (r < rows) Elem<T>::store(vp, (int64_t)d * cap + P + j0 + r, tile[r][d]);
+    if (row >= M) continue;
+    const float4 v = col_sum4(row, cv0 + d);
+    T *dst = vp + (int64_t)(P + row) * hd + d;
+    Elem<T>::store(dst, 0, v.x);
+    Elem<T>::store(dst, 1, v.y);
+    Elem<T>::store(dst, 2, v.z);
+    Elem<T>::store(dst, 3, v.w);
   }
 }
 
@@ -486,22 +480,22 @@ __global__ __launch_bounds__(256) void k_commit(const pf_verify_result *res, T *
   const int len = res->accept_len;
   const int64_t P = res->kv_base;
   if (tree) {
-    // block b: layer b / (2*nkv), plane (b % (2*nkv))
+    // block b: plane b (layer b / (2*nkv)); keys and values are both
+    // [slot][head_dim] rows
     const int b = blockIdx.x;
-    const int kvsel = (b / nkv) & 1;
     T *plane = cache + (int64_t)b * cap * hd;
     __shared__ float buf[PF_MAX_NODES * 128];
     const int cnt = (len + 1) * hd;
     for (int t = threadIdx.x; t < cnt; t += 256) {
       int d = t / hd, i = t % hd;
       int64_t src = P + res->path[d];
-      buf[t] = Elem<T>::load(plane, kvsel == 0 ? src * hd + i : (int64_t)i * cap + src);
+      buf[t] = Elem<T>::load(plane, src * hd + i);
     }
     __syncthreads();
     for (int t = threadIdx.x; t < cnt; t += 256) {
       int d = t / hd, i = t % hd;
       int64_t dst = P + d;
-      Elem<T>::store(plane, kvsel == 0 ? dst * hd + i : (int64_t)i * cap + dst, buf[t]);
+      Elem<T>::store(plane, dst * hd + i, buf[t]);
     }
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -531,7 +525,7 @@ hipError_t launch_commit(bool bf16, const pf_verify_result *res, void *cache, in
 
 // ---------------------------------------------------------------------------
 // KV import / export between the logical layout [L][2][nkv][n][hd] and the
-// cache layout (keys [slot][i], values [i][slot])
+// cache layout ([L][2][nkv][capacity][hd]: slots start .. start + n - 1)
 // ---------------------------------------------------------------------------
 
 template <typename T>
@@ -543,9 +537,8 @@ __global__ void k_kv_copy(int import_, T *cache, const T *src, T *dst, int L, in
     int64_t i = t % hd;
     int64_t r = (t / hd) % n;
     int64_t p = t / ((int64_t)hd * n);  // plane index (l*2 + kv)*nkv + g
-    int kvsel = (int)((p / nkv) & 1);
     int64_t slot = start + r;
-    int64_t ci = p * cap * hd + (kvsel == 0 ? slot * hd + i : i * cap + slot);
+    int64_t ci = p * cap * hd + slot * hd + i;
     if (import_)
       cache[ci] = src[t];
     else

@@ -305,8 +305,8 @@ def test_chained_steps_equal_greedy_decoding(pf, case):
 
 
 def _poison_past_len(gpu, torch):
-    """Fill every cache slot at or past the committed length with NaN: keys
-    are [slot][head_dim] rows, values [head_dim][slot] columns."""
+    """Fill every cache slot at or past the committed length with NaN (keys
+    and values are both [slot][head_dim] rows)."""
     s = gpu.shape
     n = int(gpu.kv.len.item())
     cap = gpu.kv.data.numel() // (s.n_layers * 2 * s.n_kv_heads * s.head_dim *
@@ -314,7 +314,7 @@ def _poison_past_len(gpu, torch):
     dt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
     planes = gpu.kv.data.view(dt).view(s.n_layers, 2, s.n_kv_heads, cap * s.head_dim)
     planes[:, 0].view(s.n_layers, s.n_kv_heads, cap, s.head_dim)[:, :, n:, :] = float("nan")
-    planes[:, 1].view(s.n_layers, s.n_kv_heads, s.head_dim, cap)[:, :, :, n:] = float("nan")
+    planes[:, 1].view(s.n_layers, s.n_kv_heads, cap, s.head_dim)[:, :, n:, :] = float("nan")
 
 
 @pytest.mark.parametrize("shape_name,tree", [("tiny", False), ("tiny", True), ("ragged", False),
