@@ -175,16 +175,36 @@ pf_status pf_keyproj_create(const float *R_host, int32_t hidden, pf_keyproj **ou
 void pf_keyproj_destroy(pf_keyproj *kp);
 
 /*
- * Keys of n states: h_dev [n][ld] (PF_DTYPE_F32 or PF_DTYPE_BF16 values, the
- * first `hidden` of each row used) -> keys_dev int8 [n][PF_KEY_DIM].
- * v = R h in fp64, each component summed as 16 interleaved fused
- * multiply-add chains (chain c takes k = c, c+16, ... in increasing order)
- * added in order c = 0..15; code_j = round-half-even(v_j * 127 / max|v|),
- * the zero key for v = 0. The codes are therefore identical on any IEEE
- * fp64 machine that follows the same order. n in [0, 2^20]; ld >= hidden.
+ * Keys of n states (Section 4, "Memory and retrieval": a fixed random
+ * projection of the final-layer state to 256 dimensions, int8): h_dev
+ * [n][ld] (PF_DTYPE_F32 or PF_DTYPE_BF16 values, the first `hidden` of each
+ * row used) -> keys_dev int8 [n][PF_KEY_DIM]. v = R h in fp64 (each
+ * component summed as 16 interleaved fused multiply-add chains, chain c
+ * taking k = c, c+16, ..., the chains added in order c = 0..15), then
+ * code_j = round-half-even(v_j * 127 / max|v|), the zero key for v = 0.
+ * Another fp64 summation order gives the same codes except where
+ * v_j * 127 / max|v| lies within the orders' rounding error of a
+ * half-integer. n in [0, 2^20]; ld >= hidden. The fp64 projections of each
+ * batch of 64 rows pass through the projection's work buffer (allocated by
+ * pf_keyproj_create): calls with one projection on overlapping streams race.
  */
 pf_status pf_key_encode(const pf_keyproj *kp, const void *h_dev, int32_t dtype, int64_t ld,
                         int64_t n, int8_t *keys_dev, pf_stream s);
+
+/*
+ * pf_key_encode for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * kernels and the same keys, but the fp64 projections of each batch of 64
+ * rows pass through a static device buffer of the library (64 x PF_KEY_DIM
+ * doubles, 128 KiB, one per GPU, held until the process ends) instead of the
+ * projection's work buffer. Calls nothing that allocates. Every call on one
+ * GPU shares that buffer, which keeps the last batch's projections: calls
+ * that overlap on one GPU (on different streams or host threads) race. The
+ * buffer is written in full before it is read, so no clearing is needed.
+ * Arguments and errors as for pf_key_encode (n in [0, 2^20]).
+ */
+pf_status pf_key_encode_static(const pf_keyproj *kp, const void *h_dev, int32_t dtype, int64_t ld,
+                               int64_t n, int8_t *keys_dev, pf_stream s);
 
 /*
  * Give a store its cosine index: keys_host int8 [T][PF_KEY_DIM], the key of

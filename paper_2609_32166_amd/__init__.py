@@ -41,7 +41,7 @@ EXPORTED = ["pf_last_error", "pf_version", "pf_context_init", "pf_context_sync_b
             "pf_kv_commit", "pf_prefill", "pf_verify_step_profiled", "pf_verify_step_trace",
             "pf_verify_kernel_repeat", "pf_read_stream",
             "pf_keyproj_create",
-            "pf_keyproj_destroy", "pf_key_encode", "pf_store_attach_keys",
+            "pf_keyproj_destroy", "pf_key_encode", "pf_key_encode_static", "pf_store_attach_keys",
             "pf_draft_lookup_cosine", "pf_verify_query_key", "pf_verify_row_keys",
             "pf_ctl_create", "pf_ctl_destroy", "pf_ctl_get_state", "pf_ctl_set_state",
             "pf_ctl_objective", "pf_ctl_choose", "pf_ctl_observe", "pf_decode_iteration",
@@ -125,6 +125,7 @@ def lib():
             "pf_keyproj_create": (i32, [vp, i32, vp]),
             "pf_keyproj_destroy": (None, [vp]),
             "pf_key_encode": (i32, [vp, vp, i32, i64, i64, vp, vp]),
+            "pf_key_encode_static": (i32, [vp, vp, i32, i64, i64, vp, vp]),
             "pf_store_attach_keys": (i32, [vp, vp, vp]),
             "pf_draft_lookup_cosine": (i32, [vp, vp, vp, i32, i32, i32, i32, vp, vp]),
             "pf_verify_query_key": (i32, [vp, vp, vp, vp, vp]),
@@ -369,6 +370,17 @@ def pf_key_encode(kp: KeyProj, h, keys, stream=None) -> None:
     assert keys.shape == (h.shape[0], KEY_DIM) and keys.is_contiguous()
     _check(lib().pf_key_encode(kp.h, h.data_ptr(), dt, int(h.stride(0)), int(h.shape[0]),
                                keys.data_ptr(), _stream(stream)))
+
+
+def pf_key_encode_static(kp: KeyProj, h, keys, stream=None) -> None:
+    """pf_key_encode through the library's static projection buffer (no
+    allocation); same arguments."""
+    torch = _torch()
+    dt = {torch.float32: PF_DTYPE_F32, torch.bfloat16: PF_DTYPE_BF16}[h.dtype]
+    assert h.dim() == 2 and h.stride(1) == 1 and keys.dtype == torch.int8
+    assert keys.shape == (h.shape[0], KEY_DIM) and keys.is_contiguous()
+    _check(lib().pf_key_encode_static(kp.h, h.data_ptr(), dt, int(h.stride(0)), int(h.shape[0]),
+                                      keys.data_ptr(), _stream(stream)))
 
 
 def pf_store_attach_keys(store: "Store", keys: np.ndarray, stream=None) -> None:

@@ -334,9 +334,12 @@ void pf_keyproj_destroy(pf_keyproj *kp) {
   delete kp;
 }
 
-// keys of n rows in batches that fit the projection's work buffer
+// keys of n rows in batches that fit a projection work buffer of kKeyBatch
+// rows (the projection's own, or the given one)
 static pf_status encode_rows(const pf_keyproj *kp, bool bf16, bool packed, const void *h,
-                             int64_t ld, int64_t n, int8_t *keys, hipStream_t hs) {
+                             int64_t ld, int64_t n, int8_t *keys, hipStream_t hs,
+                             double *work = nullptr) {
+  double *v = work ? work : kp->v;
   const size_t esz = bf16 ? 2 : 4;
   for (int64_t b = 0; b < n; b += kKeyBatch) {
     const int nb = (int)std::min<int64_t>(kKeyBatch, n - b);
@@ -345,12 +348,12 @@ static pf_status encode_rows(const pf_keyproj *kp, bool bf16, bool packed, const
       // tiles (kKeyBatch is a multiple of 16), so shift by whole tiles
       const int kf = bf16 ? 32 : 16;
       const char *hb = (const char *)h + (size_t)(b / 16) * (size_t)(ld / kf) * 1024;
-      HIPCHK(launch_key_project(bf16, true, kp->Rc, kp->H, kp->Lc, hb, ld, nb, nullptr, kp->v, hs));
+      HIPCHK(launch_key_project(bf16, true, kp->Rc, kp->H, kp->Lc, hb, ld, nb, nullptr, v, hs));
     } else {
       HIPCHK(launch_key_project(bf16, false, kp->Rc, kp->H, kp->Lc,
-                                (const char *)h + (size_t)b * ld * esz, ld, nb, nullptr, kp->v, hs));
+                                (const char *)h + (size_t)b * ld * esz, ld, nb, nullptr, v, hs));
     }
-    HIPCHK(launch_key_quant(kp->v, nb, keys + b * PF_KEY_DIM, hs));
+    HIPCHK(launch_key_quant(v, nb, keys + b * PF_KEY_DIM, hs));
   }
   return PF_OK;
 }
@@ -363,6 +366,26 @@ pf_status pf_key_encode(const pf_keyproj *kp, const void *h, int32_t dtype, int6
   if (n < 0 || n > (1 << 20)) return fail(PF_EINVAL, "pf_key_encode: n %lld out of range", (long long)n);
   if (ld < kp->H) return fail(PF_EINVAL, "pf_key_encode: ld %lld < hidden %d", (long long)ld, kp->H);
   if (pf_status r = encode_rows(kp, dtype == PF_DTYPE_BF16, false, h, ld, n, keys, st(s))) return r;
+  return ok();
+}
+
+pf_status pf_key_encode_static(const pf_keyproj *kp, const void *h, int32_t dtype, int64_t ld,
+                               int64_t n, int8_t *keys, pf_stream s) {
+  if (!kp || (n > 0 && (!h || !keys))) return fail(PF_EINVAL, "pf_key_encode_static: null pointer");
+  if (dtype != PF_DTYPE_F32 && dtype != PF_DTYPE_BF16)
+    return fail(PF_EINVAL, "pf_key_encode_static: dtype %d", dtype);
+  if (n < 0 || n > (1 << 20))
+    return fail(PF_EINVAL, "pf_key_encode_static: n %lld out of range [0, 2^20]", (long long)n);
+  if (ld < kp->H)
+    return fail(PF_EINVAL, "pf_key_encode_static: ld %lld < hidden %d", (long long)ld, kp->H);
+  double *work = nullptr;
+  int64_t elems = 0;
+  HIPCHK(key_scratch(&work, &elems));
+  if (elems < (int64_t)kKeyBatch * PF_KEY_DIM)
+    return fail(PF_EINVAL, "pf_key_encode_static: static buffer of %lld values below one batch",
+                (long long)elems);
+  if (pf_status r = encode_rows(kp, dtype == PF_DTYPE_BF16, false, h, ld, n, keys, st(s), work))
+    return r;
   return ok();
 }
 

@@ -384,6 +384,9 @@ hipError_t launch_key_project(bool bf16, bool packed, const float *Rc, int H, in
                               const void *h, int64_t ld, int n, const pf_verify_result *sel,
                               double *v, hipStream_t s);
 hipError_t launch_key_quant(const double *v, int n, int8_t *keys, hipStream_t s);
+// Device address of the static projection buffer (one batch of kKeyBatch
+// rows) on the current device, and its size in doubles.
+hipError_t key_scratch(double **out, int64_t *elems);
 
 hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers, int64_t src_layer_stride,
                        bool bf16, const Packed &geom, void *dst, hipStream_t s);

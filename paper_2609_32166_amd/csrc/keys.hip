@@ -14,6 +14,8 @@
 // integer order (cosine sign class, then dot^2 * |k'|^2 against dot'^2 * |k|^2,
 // then proposal length, then position), blocks reduce theirs in LDS, and one
 // block merges the block results and builds the draft.
+#include <mutex>
+
 #include "kernels.h"
 
 namespace pf {
@@ -121,6 +123,34 @@ hipError_t launch_key_project(bool bf16, bool packed, const float *Rc, int H, in
                     sel, v);
   return launch_k(k_key_project<float, false>, grid, 256, s, Rc, H, Lc, (const float *)h, ld, n,
                   sel, v);
+}
+
+// Static projection buffer of pf_key_encode_static: one batch of fp64
+// projections in a file-scope device array, so that entry point allocates
+// nothing. In host code the array's name is only a stand-in for its symbol;
+// its device address, different on every GPU, is looked up once per device
+// (with that device current) and kept.
+static __device__ __align__(256) double scratch[kKeyBatch * kKeyDim];
+constexpr int kMaxDevices = 64;
+static double *g_scratch_ptr[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+hipError_t key_scratch(double **out, int64_t *elems) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    double *p = nullptr;
+    e = hipGetSymbolAddress((void **)&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  *elems = (int64_t)kKeyBatch * kKeyDim;
+  return hipSuccess;
 }
 
 hipError_t launch_key_quant(const double *v, int n, int8_t *keys, hipStream_t s) {
