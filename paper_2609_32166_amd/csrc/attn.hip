@@ -349,69 +349,70 @@ __global__ __launch_bounds__(64, WPE) void k_attn(AttnArgs a) {
   if (nchunks % cps != 0) flush(sp);
 }
 
-// Merge the key-range partials of one (row, head) and round the result:
-// lane s reads split s's (max, sum). The (max, sum) pairs and the first 16
-// splits' outputs are loaded before anything waits (they do not depend on
-// the cache length, which only decides how many splits count), so the
-// kernel pays one memory round trip for up to 16 splits; further splits
-// follow eight at a time. Splits are added in index order.
+// Merge the key-range partials of one (row, head) and round the result. Four
+// waves: wave w takes splits w, w + 4, ... (up to 16 each) and loads their
+// outputs before anything waits (they do not depend on the cache length,
+// which only decides how many splits count); wave 0's lane s reads split s's
+// (max, sum). Each wave adds its splits in index order, then the four waves'
+// sums are added in wave order, so the result does not depend on timing.
 template <typename T, int HD>
-__global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
-  constexpr int NB = 16, NC = HD / 64;
-  const int j = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
+  constexpr int NU = 16, NC = HD / 64;
+  const int j = blockIdx.x, h = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const float *pml = a.part_ml + ((int64_t)h * a.n_splits * a.rowpad) * 2;
   const float *po = a.part_o + ((int64_t)h * a.n_splits * a.rowpad) * HD;
   const int ns = a.n_splits;
+  float v[NU][NC];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+    const int sp = wid + 4 * u;
+#pragma unroll
+    for (int i = 0; i < NC; ++i)
+      v[u][i] = sp < ns ? po[((int64_t)sp * a.rowpad + j) * HD + lane + 64 * i] : 0.f;
+  }
   float mv = -INFINITY, lv = 0.f;
-  if (lane < ns) {
+  if (wid == 0 && lane < ns) {
     mv = pml[((int64_t)lane * a.rowpad + j) * 2];
     lv = pml[((int64_t)lane * a.rowpad + j) * 2 + 1];
   }
-  float v0[NB][NC];
-#pragma unroll
-  for (int u = 0; u < NB; ++u)
-#pragma unroll
-    for (int i = 0; i < NC; ++i)
-      v0[u][i] = u < ns ? po[((int64_t)u * a.rowpad + j) * HD + lane + 64 * i] : 0.f;
   const int P = *a.kv_len;
   const int used = min(ns, (P + a.M + a.chunk_keys - 1) / a.chunk_keys);
-  // splits past the used ones hold stale data: weight zero, and their
-  // outputs are skipped, not multiplied
-  const float m = lane < used ? mv : -INFINITY, l = lane < used ? lv : 0.f;
-  const float mx = wave_max(m);
-  const float w = m == -INFINITY ? 0.f : exp2f(m - mx);
-  const float den = wave_sum(w * l);
   __shared__ float ws[64];
-  ws[lane] = w;
+  __shared__ float s_den;
+  __shared__ float red[4][HD];
+  if (wid == 0) {
+    // splits past the used ones hold stale data: weight zero, outputs skipped
+    const float m = lane < used ? mv : -INFINITY, l = lane < used ? lv : 0.f;
+    const float mx = wave_max(m);
+    const float w = m == -INFINITY ? 0.f : exp2f(m - mx);
+    const float den = wave_sum(w * l);
+    ws[lane] = w;
+    if (lane == 0) s_den = den;
+  }
   __syncthreads();
   float acc[NC];
 #pragma unroll
   for (int i = 0; i < NC; ++i) acc[i] = 0.f;
 #pragma unroll
-  for (int u = 0; u < NB; ++u)
+  for (int u = 0; u < NU; ++u) {
+    const int sp = wid + 4 * u;
 #pragma unroll
-    for (int i = 0; i < NC; ++i) acc[i] += u < used ? ws[u] * v0[u][i] : 0.f;
-  int s = NB;
-  for (; s + 8 <= used; s += 8) {
-    float v[8][NC];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-#pragma unroll
-      for (int i = 0; i < NC; ++i) v[u][i] = po[((int64_t)(s + u) * a.rowpad + j) * HD + lane + 64 * i];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-#pragma unroll
-      for (int i = 0; i < NC; ++i) acc[i] += ws[s + u] * v[u][i];
+    for (int i = 0; i < NC; ++i) acc[i] += sp < used ? ws[sp] * v[u][i] : 0.f;
   }
-  for (; s < used; ++s)
 #pragma unroll
-    for (int i = 0; i < NC; ++i) acc[i] += ws[s] * po[((int64_t)s * a.rowpad + j) * HD + lane + 64 * i];
+  for (int i = 0; i < NC; ++i) red[wid][lane + 64 * i] = acc[i];
+  __syncthreads();
+  if (wid != 0) return;
+  const float den = s_den;
   T *out = (T *)a.out;
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
-    const int64_t k = h * HD + lane + 64 * i;
+    const int d = lane + 64 * i;
+    const float tot = ((red[0][d] + red[1][d]) + red[2][d]) + red[3][d];
+    const int64_t k = h * HD + d;
     Elem<T>::store(out, a.out_packed ? act_off<T>(j, k, a.ldout) : (int64_t)j * a.ldout + k,
-                   acc[i] / den);
+                   tot / den);
   }
 }
 
@@ -678,7 +679,7 @@ hipError_t launch_attn_prefill(const AttnArgs &a, hipStream_t s) {
   const int nsub = (a.group + 3) / 4;
   dim3 grid(8 * ((npairs + 7) / 8) * rtiles * nsub);
   PF_TRY(launch_k(k_attn_prefill, grid, dim3(256), s, a));
-  PF_TRY(launch_k(k_attn_combine<bf16_t, 128>, dim3(a.M, a.n_kv * a.group), 64, s, a));
+  PF_TRY(launch_k(k_attn_combine<bf16_t, 128>, dim3(a.M, a.n_kv * a.group), 256, s, a));
   return hipGetLastError();
 }
 
@@ -696,16 +697,16 @@ static hipError_t attn_t(int rt, const AttnArgs &a, hipStream_t s) {
     case 3: PF_TRY(launch_k(k_attn<T, 3, HD, 1, 1>, grid, block, s, a)); break;
     default: return hipErrorInvalidValue;
   }
-  PF_TRY(launch_k(k_attn_combine<T, HD>, dim3(a.M, a.n_kv * a.group), 64, s, a));
+  PF_TRY(launch_k(k_attn_combine<T, HD>, dim3(a.M, a.n_kv * a.group), 256, s, a));
   return hipGetLastError();
 }
 
 hipError_t launch_attn_combine(bool bf16, const AttnArgs &a, hipStream_t s) {
   if (a.head_dim != 128 || a.n_splits > 64) return hipErrorInvalidValue;
   if (bf16)
-    PF_TRY(launch_k(k_attn_combine<bf16_t, 128>, dim3(a.M, a.n_kv * a.group), 64, s, a));
+    PF_TRY(launch_k(k_attn_combine<bf16_t, 128>, dim3(a.M, a.n_kv * a.group), 256, s, a));
   else
-    PF_TRY(launch_k(k_attn_combine<float, 128>, dim3(a.M, a.n_kv * a.group), 64, s, a));
+    PF_TRY(launch_k(k_attn_combine<float, 128>, dim3(a.M, a.n_kv * a.group), 256, s, a));
   return hipGetLastError();
 }
 

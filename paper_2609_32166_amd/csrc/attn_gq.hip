@@ -184,11 +184,15 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
 
   const float sc = a.scale_log2;
   constexpr float kSlack = 8.f;  // log2 headroom of the reference maximum
-  auto compute = [&](int c, int stage) {
+  const int r = lane & 15;
+  // Scores of chunk c: S^T = K Q^T (keys permuted so that lane quarter q ends
+  // up with keys q*E .. q*E + E - 1 of its row). Issued one chunk ahead of
+  // the softmax that uses them, so the matrix products of chunk c + 1 run
+  // while the vector units do chunk c's softmax.
+  auto qk = [&](int c, int stage, float (&sv)[RT][E]) {
     const int kc = k0 + c * GQ_KC;
     if (c >= nchunks || kc >= k1) return;  // uniform over the block
     const unsigned char *st = lds + stage * GQ_STAGE;
-    const int r = lane & 15;
     uint4 kf[2][NDS];
 #pragma unroll
     for (int cg = 0; cg < 2; ++cg) {
@@ -197,23 +201,32 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
       for (int d = 0; d < NDS; ++d)
         kf[cg][d] = *(const uint4 *)(st + kl * GQ_KROW + (((4 * d + q) ^ gq_swz(kl)) * 16));
     }
-    uint4 vf[NDT];
 #pragma unroll
-    for (int u = 0; u < NDT; ++u)
-      vf[u] = *(const uint4 *)(st + GQ_KBYTES + (u * 16 + r) * GQ_VROW + q * 16);
-    const int kl0 = kc + q * E;  // first key of this lane's score chunk
-    const bool all_visible = kc + GQ_KC <= min(P, k1);
-#pragma unroll
-    for (int t = 0; t < RT; ++t) {
-      float sv[E];
+    for (int t = 0; t < RT; ++t)
 #pragma unroll
       for (int cg = 0; cg < 2; ++cg) {
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int d = 0; d < NDS; ++d) acc = mma<bf16_t>(kf[cg][d], qf[t][d], acc);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) sv[4 * cg + i] = acc[i];
+        for (int i = 0; i < 4; ++i) sv[t][4 * cg + i] = acc[i];
       }
+  };
+  // softmax of chunk c and O^T += V^T P^T
+  auto soft_pv = [&](int c, int stage, float (&sin)[RT][E]) {
+    const int kc = k0 + c * GQ_KC;
+    if (c >= nchunks || kc >= k1) return;  // uniform over the block
+    const unsigned char *st = lds + stage * GQ_STAGE;
+    auto vfrag = [&](int u) {
+      return *(const uint4 *)(st + GQ_KBYTES + (u * 16 + r) * GQ_VROW + q * 16);
+    };
+    const int kl0 = kc + q * E;  // first key of this lane's score chunk
+    const bool all_visible = kc + GQ_KC <= min(P, k1);
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+      float sv[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) sv[e] = sin[t][e];
       if (!all_visible) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
@@ -223,9 +236,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
           sv[e] = vis ? sv[e] : -INFINITY;
         }
       }
-      float cmax = sv[0];
-#pragma unroll
-      for (int e = 1; e < E; ++e) cmax = fmaxf(cmax, sv[e]);
+      float cmax = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                         fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
       cmax = gq_row_max4(cmax);
       // the reference maximum of a row moves only when that row outgrows it
       // (rows that did not grow scale by exactly 1)
@@ -239,16 +251,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
         m_run[t] = m_new;
       }
       const float msc = m_run[t] == -INFINITY ? 0.f : m_run[t] * sc;
-      float p[E], psum = 0.f;
+      float p[E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(fmaf(sv[e], sc, -msc));  // exp2(-inf) = 0
-        psum += p[e];
-      }
-      l_run[t] += psum;
+      for (int e = 0; e < E; ++e) p[e] = __builtin_amdgcn_exp2f(fmaf(sv[e], sc, -msc));  // exp2(-inf) = 0
+      l_run[t] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
       const uint4 phi = pack8_bf16(p);
-#pragma unroll
-      for (int u = 0; u < NDT; ++u) o[t][u] = mma<bf16_t>(vf[u], phi, o[t][u]);
+      uint4 plo = make_uint4(0, 0, 0, 0);
       if (HILO) {
         float lo[E];
         const uint32_t w[4] = {phi.x, phi.y, phi.z, phi.w};
@@ -257,19 +265,27 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
           const uint32_t h16 = (w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
           lo[e] = p[e] - __uint_as_float(h16 << 16);
         }
-        const uint4 plo = pack8_bf16(lo);
+        plo = pack8_bf16(lo);
+      }
 #pragma unroll
-        for (int u = 0; u < NDT; ++u) o[t][u] = mma<bf16_t>(vf[u], plo, o[t][u]);
+      for (int u = 0; u < NDT; ++u) {
+        const uint4 vf = vfrag(u);
+        o[t][u] = mma<bf16_t>(vf, phi, o[t][u]);
+        if (HILO) o[t][u] = mma<bf16_t>(vf, plo, o[t][u]);
       }
     }
   };
 
+  float sA[RT][E], sB[RT][E];
+  qk(0, 0, sA);
   for (int c = 0; c < nchunks; c += 2) {
-    compute(c, c % GQ_NST);
+    qk(c + 1, (c + 1) % GQ_NST, sB);
+    soft_pv(c, c % GQ_NST, sA);
     stash(pa, c + 2, (c + 2) % GQ_NST);
     issue(pa, c + 4);
     __syncthreads();
-    compute(c + 1, (c + 1) % GQ_NST);
+    qk(c + 2, (c + 2) % GQ_NST, sA);
+    soft_pv(c + 1, (c + 1) % GQ_NST, sB);
     stash(pb, c + 3, (c + 3) % GQ_NST);
     issue(pb, c + 5);
     __syncthreads();
@@ -298,8 +314,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
 
 // Tiles per wave: one (16 virtual rows per wave, 64 per block); a step's
 // virtual rows are spread over row groups of blocks, each with its own K/V
-// chunks from L2. Measured against 2-4 tiles per wave (fewer blocks, more
-// serial work per wave): one is fastest on the 3B and 7B steps.
+// chunks from L2. Two tiles per wave (half the blocks) and twice the key
+// ranges measured the same or slower on the 7B step (20.7-25.7 us).
 int attn_gq_tiles(int group, int rows) {
   (void)group;
   (void)rows;
