@@ -53,7 +53,13 @@ def gate_up_bytes(wl) -> int:
 # profiles/. Valid only for the GEMM source the counters were taken on (its
 # SHA-256): after any change to that file a workload's entry reads as null
 # until measured again.
-GATE_UP_TRAFFIC = {}
+GATE_UP_SHA = "c3791c7e1370cb73dfdb536fc3008739433edf066d22d7f32558f1b64323f5a8"
+GATE_UP_TRAFFIC = {
+    "7b": {"bytes": 275342732, "gemm_source_sha256": GATE_UP_SHA},
+    "3b": {"bytes": 91459556, "gemm_source_sha256": GATE_UP_SHA},
+    "3b_tree": {"bytes": 93277885, "gemm_source_sha256": GATE_UP_SHA},
+    "7b_carry": {"bytes": 273728161, "gemm_source_sha256": GATE_UP_SHA},
+}
 
 
 def measured_traffic(wl):
@@ -668,7 +674,10 @@ def measure(torch, pf, name, args, headline):
         r = pf.read_result(res)
         d = pf.read_draft(draft)
 
-    kernels = kernel_times(torch, pf, wl, model, kv, c, ctx, st, draft, res)
+    if args.no_kernel_times:
+        kernels = {"gate_up": {"avg_launch_us": float("nan")}}
+    else:
+        kernels = kernel_times(torch, pf, wl, model, kv, c, ctx, st, draft, res)
     # leave the buffers as a normal step does
     step()
     torch.cuda.synchronize()
@@ -740,6 +749,9 @@ def main():
     ap.add_argument("--no-loop", action="store_true", help="skip the closed-loop decode timings")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="also run a plain device copy of this many MiB (for counter scaling)")
+    ap.add_argument("--no-kernel-times", action="store_true",
+                    help="skip the per-kind kernel timings (short counter runs)")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the read-stream ceiling")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
@@ -754,7 +766,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
-    ceiling = read_ceiling(torch, pf)
+    ceiling = {"GBps": float("nan")} if args.no_ceiling else read_ceiling(torch, pf)
     log(f"read-stream ceiling {ceiling['GBps']} GB/s")
     head = measure(torch, pf, args.workload, args, headline=True)
     nested = {}
