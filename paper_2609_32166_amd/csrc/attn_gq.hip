@@ -27,17 +27,20 @@ namespace {
 
 constexpr int GQ_HD = 128;
 constexpr int GQ_KC = 32;                          // keys per chunk
-// Staged keys: [key][16-byte granule g ^ swz(key)] rows of 256 bytes; staged
-// values: [dim][32 keys] rows padded to 80 bytes. The swizzle spreads the 16
-// keys one operand read touches (keys 0-3, 8-11, 16-19, 24-27 plus 4 for the
-// second group) over 16 distinct granules, and the 80-byte value rows put
-// the 16 dimensions of a read on distinct banks, so neither read conflicts.
-constexpr int GQ_KROW = GQ_HD * 2;                 // 256
+// Staged keys: [key] rows of 256 bytes padded to 272, so the 16 consecutive
+// keys one operand read touches start on 16 distinct 16-byte bank groups.
+// Staged values: [dim] rows of the chunk's 32 keys (80 bytes with padding, so
+// the 16 dimensions of a read fall on distinct bank groups), keys permuted
+// within the row to match the score layout: key k = 16a + 4c + b sits at
+// position 8c + 4a + b, so lane quarter c finds the eight keys its
+// probabilities belong to (4c..4c+3 and 16+4c..16+4c+3) in one 16-byte read.
+constexpr int GQ_KROW = GQ_HD * 2 + 16;            // 272
 constexpr int GQ_VROW = GQ_KC * 2 + 16;            // 80
-constexpr int GQ_KBYTES = GQ_KC * GQ_KROW;         // 8192
-constexpr int GQ_STAGE = GQ_KBYTES + GQ_HD * GQ_VROW;  // 18432
-__device__ inline int gq_swz(int key) { return (key & 15) ^ ((key >> 4) << 2); }
+constexpr int GQ_KBYTES = GQ_KC * GQ_KROW;         // 8704
+constexpr int GQ_STAGE = GQ_KBYTES + GQ_HD * GQ_VROW;  // 18944
 constexpr int GQ_NST = 3;                          // LDS stages
+constexpr int GQ_CHUNK_BYTES = GQ_KC * GQ_HD * 2;  // 8192 bytes of one plane per chunk
+__device__ constexpr int gq_vpos(int k) { return ((k >> 2) & 3) * 8 + (k >> 4) * 4 + (k & 3); }
 
 __device__ inline uint4 pack8_bf16(const float *p) {
   typedef float f2 __attribute__((ext_vector_type(2)));
@@ -60,6 +63,13 @@ __device__ __forceinline__ float gq_row_sum4(float x) {
   x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
   auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// The whole offset goes in the vector operand: the descriptor's bound checks
+// that operand (plus the instruction's constant), not the scalar offset.
+__device__ __forceinline__ uint4 gq_load(rsrc_t r, uint32_t off) {
+  v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
 }
 
 // Two blocks per compute unit (two waves per SIMD, so one wave's products
@@ -87,56 +97,75 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
   const int kb = min(k0 + a.chunk_keys, a.keys_bound);
   const int nchunks = kb > k0 ? (kb - k0 + GQ_KC - 1) / GQ_KC : 0;
 
-  // K/V planes of (layer, g)
-  const bf16_t *kplane = (const bf16_t *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.n_kv + g) * a.plane;
-  const bf16_t *vplane = (const bf16_t *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.n_kv + g) * a.plane;
-  const uint32_t plane_bytes = (uint32_t)(a.plane * 2);
-  const rsrc_t kr_ = make_rsrc(kplane, plane_bytes);
-  const rsrc_t vr_ = make_rsrc(vplane, plane_bytes);
+  // K/V rows of the range in (layer, g): buffer resources based at its
+  // first key and bounded at its last (keys, which masking hides past the
+  // cache end) or at the cache end (values: slots past it are not
+  // initialised for this step and a zero probability must not meet a NaN),
+  // so loads past either bound return zeros without a select
+  const int64_t roff = (int64_t)k0 * GQ_HD;
+  const bf16_t *kplane = (const bf16_t *)a.cache + ((int64_t)(a.layer * 2 + 0) * a.n_kv + g) * a.plane + roff;
+  const bf16_t *vplane = (const bf16_t *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.n_kv + g) * a.plane + roff;
+  const rsrc_t kr_ = make_rsrc(kplane, (uint32_t)max(kb - k0, 0) * (GQ_HD * 2));
 
-  // chunk loads: thread tid carries K pieces tid, tid + 256 (key = p / 16,
-  // 16-byte piece p % 16 of its row) and the V pieces of keys 2 kp, 2 kp + 1
-  // (kp = tid % 16) at dimensions 8 dg .. 8 dg + 7 (dg = tid / 16)
+  // chunk loads: thread tid carries K pieces tid, tid + 256 (16-byte piece
+  // p % 16 of key p / 16) and the V pieces of keys 2 kp, 2 kp + 1 (kp = tid %
+  // 16) at dimensions 8 dg .. 8 dg + 7 (dg = tid / 16)
   uint4 pa[4], pb[4];
   const int kp = tid & 15, dg = tid >> 4;
-  auto issue = [&](uint4 *pr, int c) {
-    const int kc = k0 + c * GQ_KC;
-    const bool in = c < nchunks;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int p = tid + 256 * i;
-      const int key = kc + (p >> 4);
-      pr[i] = bload16(kr_, in && key < kb ? (uint32_t)(((int64_t)key * GQ_HD + (p & 15) * E) * 2) : kOOB);
-      const int vk = kc + 2 * kp + i;
-      pr[2 + i] = bload16(vr_, in && vk < kb ? (uint32_t)(((int64_t)vk * GQ_HD + dg * E) * 2) : kOOB);
-    }
+  const uint32_t koff = (uint32_t)tid * 16u;
+  const uint32_t voff = (uint32_t)(2 * kp * GQ_HD + dg * E) * 2u;
+  auto issue_k = [&](uint4 *pr, int c) {
+    const uint32_t so = (uint32_t)c * GQ_CHUNK_BYTES;
+    pr[0] = gq_load(kr_, koff + so);
+    pr[1] = gq_load(kr_, koff + so + 4096u);
   };
-  // values of keys at or past the cache end are zeroed (those slots are not
-  // initialised for this step; a zero probability must not meet a NaN)
-  int kend = 0;
-  auto stash = [&](const uint4 *pr, int c, int stage) {
-    const int kc = k0 + c * GQ_KC;
-    unsigned char *st = lds + stage * GQ_STAGE;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int p = tid + 256 * i, key = p >> 4;
-      *(uint4 *)(st + key * GQ_KROW + (((p & 15) ^ gq_swz(key)) * 16)) = pr[i];
-    }
-    const int v0 = kc + 2 * kp;
-    const uint4 a0 = v0 < kend ? pr[2] : make_uint4(0, 0, 0, 0);
-    const uint4 a1 = v0 + 1 < kend ? pr[3] : make_uint4(0, 0, 0, 0);
-    const uint32_t x0[4] = {a0.x, a0.y, a0.z, a0.w}, x1[4] = {a1.x, a1.y, a1.z, a1.w};
-    unsigned char *vt = st + GQ_KBYTES + kp * 4;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const uint32_t lo = (x0[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-      const uint32_t hi = (x1[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-      *(uint32_t *)(vt + (dg * E + e) * GQ_VROW) = lo | (hi << 16);
-    }
+  // the first two chunks' values are fetched before the cache length is
+  // known (bounded at the range end) and zeroed past the cache end on the way
+  // into LDS; later chunks use the resource bounded at the cache end
+  auto issue_v = [&](rsrc_t vr, uint4 *pr, int c) {
+    const uint32_t so = (uint32_t)c * GQ_CHUNK_BYTES;
+    pr[2] = gq_load(vr, voff + so);
+    pr[3] = gq_load(vr, voff + so + GQ_HD * 2u);
+  };
+  {
+    const rsrc_t vr0 = make_rsrc(vplane, (uint32_t)max(kb - k0, 0) * (GQ_HD * 2));
+    issue_k(pa, 0);
+    issue_v(vr0, pa, 0);
+    issue_k(pb, 1);
+    issue_v(vr0, pb, 1);
+  }
+  const int P = *a.kv_len;
+  const int kend = P + M;
+  const rsrc_t vr_ = make_rsrc(vplane, (uint32_t)max(min(kb, kend) - k0, 0) * (GQ_HD * 2));
+  auto issue = [&](uint4 *pr, int c) {
+    issue_k(pr, c);
+    issue_v(vr_, pr, c);
   };
 
-  issue(pa, 0);
-  issue(pb, 1);
+  // LDS addresses: stores of a thread's pieces, operand reads of a lane
+  const int kst = (tid >> 4) * GQ_KROW + (tid & 15) * 16;          // key piece tid
+  const int vst = GQ_KBYTES + 8 * dg * GQ_VROW + gq_vpos(2 * kp) * 2;  // dim 8 dg, keys 2kp, 2kp+1
+  const int r = lane & 15;
+  const int kld = r * GQ_KROW + q * 16;                             // key r (+16 cg), granule q (+4 d)
+  const int vld = GQ_KBYTES + r * GQ_VROW + q * 16;                 // dim r (+16 u), keys of quarter q
+  auto stash = [&](const uint4 *pr, int stage, int zero_from) {
+    unsigned char *st = lds + stage * GQ_STAGE;
+    *(uint4 *)(st + kst) = pr[0];
+    *(uint4 *)(st + kst + 16 * GQ_KROW) = pr[1];
+    // zero_from: first key (relative to the chunk) whose values are zeroed
+    // here (only the first two chunks need it)
+    const uint4 a0 = 2 * kp < zero_from ? pr[2] : make_uint4(0, 0, 0, 0);
+    const uint4 a1 = 2 * kp + 1 < zero_from ? pr[3] : make_uint4(0, 0, 0, 0);
+    const uint32_t x0[4] = {a0.x, a0.y, a0.z, a0.w};
+    const uint32_t x1[4] = {a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      // low half: key 2kp, high half: key 2kp + 1, at dimension 8 dg + e
+      const uint32_t w = (e & 1) ? __builtin_amdgcn_perm(x1[e >> 1], x0[e >> 1], 0x07060302u)
+                                 : __builtin_amdgcn_perm(x1[e >> 1], x0[e >> 1], 0x05040100u);
+      *(uint32_t *)(st + vst + e * GQ_VROW) = w;
+    }
+  };
 
   // query fragments and per-row visibility of the wave's virtual rows
   const int vbase = (rg * 4 + wid) * RT * 16;
@@ -154,8 +183,6 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
     for (int d = 0; d < NDS; ++d)
       qf[t][d] = real ? *(const uint4 *)(qrow + d * KF + q * E) : make_uint4(0, 0, 0, 0);
   }
-  const int P = *a.kv_len;
-  kend = P + M;
   const int k1 = min(k0 + a.chunk_keys, kend);
   int lim[RT];
   uint64_t anc[RT];
@@ -176,31 +203,34 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
     for (int u = 0; u < NDT; ++u) o[t][u] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  stash(pa, 0, 0);
+  stash(pa, 0, kend - k0);
   issue(pa, 2);
-  stash(pb, 1, 1);
+  stash(pb, 1, kend - k0 - GQ_KC);
   issue(pb, 3);
   __syncthreads();
 
   const float sc = a.scale_log2;
   constexpr float kSlack = 8.f;  // log2 headroom of the reference maximum
-  const int r = lane & 15;
-  // Scores of chunk c: S^T = K Q^T (keys permuted so that lane quarter q ends
-  // up with keys q*E .. q*E + E - 1 of its row). Issued one chunk ahead of
-  // the softmax that uses them, so the matrix products of chunk c + 1 run
-  // while the vector units do chunk c's softmax.
-  auto qk = [&](int c, int stage, float (&sv)[RT][E]) {
+  // Scores of chunk c: S^T = K Q^T over two 16-key tiles; lane quarter c of
+  // row lane % 16 ends up with keys 4c..4c+3 (first tile) and 16+4c..16+4c+3
+  // (second tile). Issued one chunk ahead of the softmax that uses them, so
+  // the matrix products of chunk c + 1 run while the vector units do chunk
+  // c's softmax.
+  auto load_k = [&](int stage, uint4 (&kf)[2][NDS]) {
+    const unsigned char *st = lds + stage * GQ_STAGE + kld;
+#pragma unroll
+    for (int cg = 0; cg < 2; ++cg)
+#pragma unroll
+      for (int d = 0; d < NDS; ++d) kf[cg][d] = *(const uint4 *)(st + cg * 16 * GQ_KROW + d * 64);
+  };
+  auto load_v = [&](int stage, uint4 (&vf)[NDT]) {
+    const unsigned char *st = lds + stage * GQ_STAGE + vld;
+#pragma unroll
+    for (int u = 0; u < NDT; ++u) vf[u] = *(const uint4 *)(st + u * 16 * GQ_VROW);
+  };
+  auto qk = [&](int c, const uint4 (&kf)[2][NDS], float (&sv)[RT][E]) {
     const int kc = k0 + c * GQ_KC;
     if (c >= nchunks || kc >= k1) return;  // uniform over the block
-    const unsigned char *st = lds + stage * GQ_STAGE;
-    uint4 kf[2][NDS];
-#pragma unroll
-    for (int cg = 0; cg < 2; ++cg) {
-      const int kl = E * (r >> 2) + 4 * cg + (r & 3);
-#pragma unroll
-      for (int d = 0; d < NDS; ++d)
-        kf[cg][d] = *(const uint4 *)(st + kl * GQ_KROW + (((4 * d + q) ^ gq_swz(kl)) * 16));
-    }
 #pragma unroll
     for (int t = 0; t < RT; ++t)
 #pragma unroll
@@ -213,14 +243,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
       }
   };
   // softmax of chunk c and O^T += V^T P^T
-  auto soft_pv = [&](int c, int stage, float (&sin)[RT][E]) {
+  auto soft_pv = [&](int c, const uint4 (&vf)[NDT], float (&sin)[RT][E]) {
     const int kc = k0 + c * GQ_KC;
     if (c >= nchunks || kc >= k1) return;  // uniform over the block
-    const unsigned char *st = lds + stage * GQ_STAGE;
-    auto vfrag = [&](int u) {
-      return *(const uint4 *)(st + GQ_KBYTES + (u * 16 + r) * GQ_VROW + q * 16);
-    };
-    const int kl0 = kc + q * E;  // first key of this lane's score chunk
+    const int kl0 = kc + q * 4;  // keys kl0 + (e & 3) + 16 (e >> 2) of this lane's scores
     const bool all_visible = kc + GQ_KC <= min(P, k1);
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
@@ -230,7 +256,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
       if (!all_visible) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          const int key = kl0 + e;
+          const int key = kl0 + (e & 3) + 16 * (e >> 2);
           bool vis = key < lim[t];
           if (a.tree) vis &= (key < P) | (((anc[t] >> ((key - P) & 63)) & 1ull) != 0);
           sv[e] = vis ? sv[e] : -INFINITY;
@@ -262,33 +288,41 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
         const uint32_t w[4] = {phi.x, phi.y, phi.z, phi.w};
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          const uint32_t h16 = (w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-          lo[e] = p[e] - __uint_as_float(h16 << 16);
+          const uint32_t h = (e & 1) ? (w[e >> 1] & 0xFFFF0000u) : (w[e >> 1] << 16);
+          lo[e] = p[e] - __uint_as_float(h);
         }
         plo = pack8_bf16(lo);
       }
 #pragma unroll
       for (int u = 0; u < NDT; ++u) {
-        const uint4 vf = vfrag(u);
-        o[t][u] = mma<bf16_t>(vf, phi, o[t][u]);
-        if (HILO) o[t][u] = mma<bf16_t>(vf, plo, o[t][u]);
+        o[t][u] = mma<bf16_t>(vf[u], phi, o[t][u]);
+        if (HILO) o[t][u] = mma<bf16_t>(vf[u], plo, o[t][u]);
       }
     }
   };
 
+  // One phase: the LDS reads of chunk c + 1's keys and chunk c's values go
+  // out first, then chunk c + 1's score products, chunk c's softmax and
+  // value products, the stash of chunk c + 2 and the loads of chunk c + 4.
   float sA[RT][E], sB[RT][E];
-  qk(0, 0, sA);
+  {
+    uint4 kf[2][NDS];
+    load_k(0, kf);
+    qk(0, kf, sA);
+  }
+  auto phase = [&](int c, float (&scur)[RT][E], float (&snext)[RT][E], uint4 *pr) {
+    uint4 kf[2][NDS], vf[NDT];
+    load_k((c + 1) % GQ_NST, kf);
+    load_v(c % GQ_NST, vf);
+    qk(c + 1, kf, snext);
+    soft_pv(c, vf, scur);
+    stash(pr, (c + 2) % GQ_NST, GQ_KC);
+    issue(pr, c + 4);
+    __syncthreads();
+  };
   for (int c = 0; c < nchunks; c += 2) {
-    qk(c + 1, (c + 1) % GQ_NST, sB);
-    soft_pv(c, c % GQ_NST, sA);
-    stash(pa, c + 2, (c + 2) % GQ_NST);
-    issue(pa, c + 4);
-    __syncthreads();
-    qk(c + 2, (c + 2) % GQ_NST, sA);
-    soft_pv(c + 1, (c + 1) % GQ_NST, sB);
-    stash(pb, c + 3, (c + 3) % GQ_NST);
-    issue(pb, c + 5);
-    __syncthreads();
+    phase(c, sA, sB, pa);
+    phase(c + 1, sB, sA, pb);
   }
 
   // partial of key range kr: lane holds O^T[d = u*16 + 4q + i][row lane%16]
