@@ -818,7 +818,8 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
   int64_t zb[] = {kRowPad * H * 4, kRowPad * Hp * m->esz, kRowPad * q * m->esz,
                   kRowPad * qp * m->esz, kRowPad * Fp * m->esz};
   for (int i = 0; i < 5 && e == hipSuccess; ++i) e = hipMemsetAsync(zero[i], 0, zb[i], hs);
-  if (e == hipSuccess) e = launch_pack(w->wqkv, q + 2 * kv, H, L, (q + 2 * kv) * H, bf, m->pqkv, m->wqkv, hs);
+  if (e == hipSuccess) e = launch_pack(w->wqkv, q + 2 * kv, H, L, (q + 2 * kv) * H, bf, m->pqkv, m->wqkv, hs,
+                                           c.head_dim);
   if (e == hipSuccess) e = launch_pack(w->wo, H, q, L, H * q, bf, m->po, m->wo, hs);
   if (e == hipSuccess) e = launch_pack(w->wgu, 2 * F, H, L, 2 * F * H, bf, m->pgu, m->wgu, hs);
   if (e == hipSuccess) e = launch_pack(w->wd, H, F, L, H * F, bf, m->pd, m->wd, hs);
@@ -1050,7 +1051,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     qa.cache = kv->data;
     qa.layer = l;
     qa.cap = kv->capacity;
-    PROF(1, launch_gemm_qkv(bf, MT, qa, hs));
+    PROF(1, launch_gemm_qkv(bf, MT, qa, m->wave_slots / 4, hs));
     // attention
     AttnArgs at{};
     at.q = m->qb;

@@ -14,9 +14,20 @@ namespace pf {
 // weight packing
 // ---------------------------------------------------------------------------
 
+// Source row of packed row n when the rows are attention heads of rope_hd
+// dimensions packed RoPE-paired: tile t of a head (16 rows) holds dimensions
+// 8t .. 8t+7 and their rotation partners rope_hd/2 + 8t .. rope_hd/2 + 8t+7,
+// so a 16-column output tile can be rotated without its neighbours.
+__device__ inline int64_t rope_paired_row(int64_t n, int rope_hd) {
+  const int64_t head = n / rope_hd;
+  const int w = (int)(n % rope_hd), t = w / 16, c = w % 16;
+  const int dim = c < 8 ? 8 * t + c : rope_hd / 2 + 8 * t + (c - 8);
+  return head * rope_hd + dim;
+}
+
 template <typename T>
 __global__ void k_pack(const T *__restrict__ src, int64_t N, int64_t K, int64_t KFr,
-                       int64_t NT, int64_t layers, int64_t src_layer_stride,
+                       int64_t NT, int64_t layers, int64_t src_layer_stride, int rope_hd,
                        uint4 *__restrict__ dst) {
   constexpr int E = Elem<T>::E;
   constexpr int KF = 4 * E;
@@ -34,11 +45,12 @@ __global__ void k_pack(const T *__restrict__ src, int64_t N, int64_t K, int64_t 
       uint4 v;
       T e[E];
     } u;
-    const T *row = src + l * src_layer_stride + n * K;
+    const int64_t ns = rope_hd > 0 ? rope_paired_row(n, rope_hd) : n;
+    const T *row = src + l * src_layer_stride + ns * K;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       int64_t k = k0 + e;
-      if (n < N && k < K) {
+      if (n < N && ns < N && k < K) {
         u.e[e] = row[k];
       } else {
         memset(&u.e[e], 0, sizeof(T));
@@ -50,16 +62,17 @@ __global__ void k_pack(const T *__restrict__ src, int64_t N, int64_t K, int64_t 
 
 hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers,
                        int64_t src_layer_stride, bool bf16, const Packed &g, void *dst,
-                       hipStream_t s) {
+                       hipStream_t s, int rope_hd) {
+  if (rope_hd > 0 && (rope_hd % 16 != 0 || N % rope_hd != 0)) return hipErrorInvalidValue;
   int64_t total = g.NT * g.KFr * 64 * layers;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 65536) blocks = 65536;
   if (bf16)
     PF_TRY(launch_k(k_pack<bf16_t>, (unsigned)blocks, 256, s, (const bf16_t *)src, N, K, g.KFr, g.NT, layers,
-                                                    src_layer_stride, (uint4 *)dst));
+                                                    src_layer_stride, rope_hd, (uint4 *)dst));
   else
     PF_TRY(launch_k(k_pack<float>, (unsigned)blocks, 256, s, (const float *)src, N, K, g.KFr, g.NT, layers,
-                                                   src_layer_stride, (uint4 *)dst));
+                                                   src_layer_stride, rope_hd, (uint4 *)dst));
   return hipGetLastError();
 }
 

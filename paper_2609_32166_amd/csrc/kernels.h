@@ -106,7 +106,9 @@ struct QkvArgs {
   int layer;
   int64_t cap;
 };
-hipError_t launch_gemm_qkv(bool bf16, int mt, const QkvArgs &a, hipStream_t s);
+// cus: compute units of the device (the block shape depends on the model's
+// tile count against it, never on the rows)
+hipError_t launch_gemm_qkv(bool bf16, int mt, const QkvArgs &a, int cus, hipStream_t s);
 
 struct AttnArgs {
   const void *q;        // [kRowPad][ldq] queries after RoPE
@@ -388,8 +390,16 @@ hipError_t launch_key_quant(const double *v, int n, int8_t *keys, hipStream_t s)
 // rows) on the current device, and its size in doubles.
 hipError_t key_scratch(double **out, int64_t *elems);
 
+// Packs W [N][K] (per layer) into MFMA fragments. rope_hd > 0 packs the rows
+// of each rope_hd-row head RoPE-paired: 16-row tile t of a head holds
+// dimensions 8t..8t+7, then rope_hd/2 + 8t..rope_hd/2 + 8t+7.
 hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers, int64_t src_layer_stride,
-                       bool bf16, const Packed &geom, void *dst, hipStream_t s);
+                       bool bf16, const Packed &geom, void *dst, hipStream_t s, int rope_hd = 0);
+// Column of dimension d (0 <= d < hd) of a head in a RoPE-paired packed output.
+__host__ __device__ inline int rope_paired_col(int d, int hd) {
+  const int half = hd / 2, e = d < half ? d : d - half;
+  return (e / 8) * 16 + (e % 8) + (d < half ? 0 : 8);
+}
 
 // Tiles per block along N for each epilogue.
 int gemm_tiles_per_block(int epi, int mt);

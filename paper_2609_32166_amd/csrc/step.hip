@@ -295,7 +295,10 @@ __global__ __launch_bounds__(256) void k_qkv_post(const float *part, int splits,
                                                   T *qbuf, int64_t ldq, T *cache, int layer,
                                                   int64_t cap) {
   // one block per (32-row tile, head): query and key heads are rotated,
-  // value heads copied; all stored row-major
+  // value heads copied; all stored row-major. The projection's columns are
+  // RoPE-paired within each head (the packed weight's row order): four
+  // consecutive dimensions d..d+3 (d a multiple of 4) sit in four
+  // consecutive columns, rope_paired_col(d).
   const int j0 = blockIdx.x * 32, hh = blockIdx.y;
   const int half = hd / 2, h4 = half / 4;
   const int P = *kv_len;
@@ -320,7 +323,8 @@ __global__ __launch_bounds__(256) void k_qkv_post(const float *part, int splits,
       const int r = idx / h4, i = 4 * (idx % h4);
       const int row = j0 + r;
       if (row >= M) continue;
-      const float4 a4 = col_sum4(row, c0 + i), b4 = col_sum4(row, c0 + i + half);
+      const int ci = rope_paired_col(i, hd);
+      const float4 a4 = col_sum4(row, c0 + ci), b4 = col_sum4(row, c0 + ci + 8);
       const float4 cs0 = *(const float4 *)(rope + ((int64_t)row * half + i) * 2);
       const float4 cs1 = *(const float4 *)(rope + ((int64_t)row * half + i) * 2 + 4);
       const float av[4] = {a4.x, a4.y, a4.z, a4.w}, bv[4] = {b4.x, b4.y, b4.z, b4.w};
@@ -343,7 +347,7 @@ __global__ __launch_bounds__(256) void k_qkv_post(const float *part, int splits,
     const int r = idx / d4, d = 4 * (idx % d4);
     const int row = j0 + r;
     if (row >= M) continue;
-    const float4 v = col_sum4(row, cv0 + d);
+    const float4 v = col_sum4(row, cv0 + rope_paired_col(d, hd));
     T *dst = vp + (int64_t)(P + row) * hd + d;
     Elem<T>::store(dst, 0, v.x);
     Elem<T>::store(dst, 1, v.y);
@@ -356,7 +360,7 @@ hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int rowpad,
                            int nkv, int hd, int64_t ldpart, const float *rope, const int32_t *kv_len,
                            void *qbuf, int64_t ldq, void *cache, int layer, int64_t cap,
                            hipStream_t s) {
-  if (hd > 128 || hd % 8 != 0) return hipErrorInvalidValue;
+  if (hd > 128 || hd % 16 != 0) return hipErrorInvalidValue;
   dim3 grid((M + 31) / 32, nq + 2 * nkv);
   if (bf16)
     PF_TRY(launch_k(k_qkv_post<bf16_t>, grid, 256, s, part, splits, rowpad, M, nq, nkv, hd, ldpart,
