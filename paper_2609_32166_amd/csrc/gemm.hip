@@ -82,20 +82,24 @@ hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers,
 
 
 // n tiles per block. With three 16-row X tiles the X fragments outweigh the
-// W fragments they meet, so a wave takes four W tiles (two gate/up pairs) to
-// reuse each X fragment twice as often (more tiles would cost occupancy).
-// Per tile the sums are the same: a tile's k range and its split of the
-// range over the waves do not depend on how many tiles share the block.
+// W fragments they meet, and each X load instruction costs about as much as a
+// W load whatever its bytes, so a wave takes four W tiles (the partial-sum
+// projections) or six (gate/up: three gate/up pairs, three fragment slots in
+// flight, two blocks per CU) to reuse each X fragment more often. Per tile the
+// sums are the same: a tile's k range and its split of the range over the
+// waves do not depend on how many tiles share the block.
 template <int EPI, int MT> struct EpiTiles {
-  static constexpr int NT = EPI == EPI_ARGMAX ? 4 : MT == 3 ? 4 : 2;  // SwiGLU: gate, up pairs
+  static constexpr int NT = EPI == EPI_ARGMAX ? 4 : MT == 3 ? (EPI == EPI_SWIGLU ? 6 : 4) : 2;
+  static constexpr int kU = NT >= 6 ? 3 : NT >= 4 ? 4 : 6;  // fragment slots in flight per wave
+  static constexpr int MinBlocks = EPI == EPI_SWIGLU && MT == 3 ? 2 : 1;  // blocks per CU
 };
 
 __device__ inline float silu(float g) { return g / (1.0f + expf(-g)); }
 
 template <typename T, int MT, int EPI>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+__global__ __launch_bounds__(256, (EpiTiles<EPI, MT>::MinBlocks)) void k_gemm(GemmArgs a) {
   constexpr int NT = EpiTiles<EPI, MT>::NT;
-  constexpr int kU = NT >= 4 ? 4 : 6;  // fragment slots in flight per wave
+  constexpr int kU = EpiTiles<EPI, MT>::kU;
   constexpr int E = Elem<T>::E;
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
@@ -297,7 +301,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 int gemm_tiles_per_block(int epi, int mt) {
   // SwiGLU blocks are counted in gate tiles (each with its up tile)
   if (epi == EPI_ARGMAX) return 4;
-  const int nt = mt == 3 ? 4 : 2;
+  const int nt = mt == 3 ? (epi == EPI_SWIGLU ? 6 : 4) : 2;
   return epi == EPI_SWIGLU ? nt / 2 : nt;
 }
 
