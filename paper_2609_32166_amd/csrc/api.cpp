@@ -56,17 +56,24 @@ Packed geom(int64_t N, int64_t K, int kf) {
   return p;
 }
 
-// split-K factor for a partial-sum GEMM: about 256 blocks (one per CU), at
-// least two fragments per wave. Measured over 256..1024-block targets for
-// the O and down projections of both models: 256 is best or level (3B O
-// 3.3 -> 2.1 us, 7B O 9.5 -> 7.6 us; 512 costs the 7B down projection 20%).
-int splits_for(int64_t nblocks, int64_t KFr) {
-  int64_t s = (256 + nblocks - 1) / nblocks;
+// split-K factor for a partial-sum GEMM, from its shape and the CU count
+// only (never the row count, so every row's summation order is fixed): the
+// smallest factor from about one block per CU up whose blocks (counted at two
+// n tiles per block) fill the CUs evenly, at least 7/8 of the slots of the
+// busiest CU count in use, with at least two fragments per wave. Measured on
+// both models: 7B O and down 3 -> 4 splits (336 -> 448 blocks; 33 rows:
+// down 30.6 -> 25.8 us, O 9.0 -> 7.9; 17 rows: down 32.7 -> 27.2); 3B keeps
+// 4 (256 blocks), where 6 costs O 4.6 -> 5.9 us and down 11.2 -> 12.7.
+int splits_for(int64_t nblocks, int64_t KFr, int cus) {
   int64_t cap = KFr / 8;
   if (cap < 1) cap = 1;
-  if (s > cap) s = cap;
-  if (s < 1) s = 1;
-  return (int)s;
+  if (cus < 1) cus = 1;
+  const int64_t s0 = (cus + nblocks - 1) / nblocks;
+  for (int64_t s = s0; s <= cap; ++s) {
+    const int64_t b = nblocks * s, per_cu = (b + cus - 1) / cus;
+    if (8 * b >= 7 * per_cu * cus) return (int)s;
+  }
+  return (int)(s0 < cap ? s0 : cap);
 }
 
 // blocks of a partial-sum GEMM counted at two n tiles per block whatever the
@@ -780,14 +787,6 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
   // step work buffers
   const int64_t Hp = roundup(H, kf), qp = roundup(q, kf), Fp = roundup(F, kf);
   int64_t part = 0;
-  const Packed *pg[] = {&m->pqkv, &m->po, &m->pd};
-  for (const Packed *p : pg) {
-    int64_t nb = partial_blocks(*p);
-    int64_t e = (int64_t)splits_for(nb, p->KFr) * kRowPad * p->NT * 16;
-    if (e > part) part = e;
-  }
-  m->part_elems = part;
-  m->apart_rows = (int64_t)c.n_heads * kMaxSplitsAttn * kRowPad;
   {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
@@ -795,6 +794,14 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
         cus > 0)
       m->wave_slots = 4 * cus;
   }
+  const Packed *pg[] = {&m->pqkv, &m->po, &m->pd};
+  for (const Packed *p : pg) {
+    int64_t nb = partial_blocks(*p);
+    int64_t e = (int64_t)splits_for(nb, p->KFr, m->wave_slots / 4) * kRowPad * p->NT * 16;
+    if (e > part) part = e;
+  }
+  m->part_elems = part;
+  m->apart_rows = (int64_t)c.n_heads * kMaxSplitsAttn * kRowPad;
   m->amax_elems = ((m->plm.NT + 3) / 4) * kRowPad;
   ALLOC(m->x, kRowPad * H * 4);
   ALLOC(m->xn, kRowPad * Hp * m->esz);
@@ -1088,7 +1095,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     go.X = m->attn;
     go.ldx = qp;
     go.M = M;
-    go.splits = splits_for(partial_blocks(m->po), m->po.KFr);
+    go.splits = splits_for(partial_blocks(m->po), m->po.KFr, m->wave_slots / 4);
     go.out = m->part;
     go.ldo = H;
     PROF(4, launch_gemm(bf, EPI_PARTIAL, MT, go, hs));
@@ -1117,7 +1124,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     gd.X = m->act;
     gd.ldx = Fp;
     gd.M = M;
-    gd.splits = splits_for(partial_blocks(m->pd), m->pd.KFr);
+    gd.splits = splits_for(partial_blocks(m->pd), m->pd.KFr, m->wave_slots / 4);
     gd.out = m->part;
     gd.ldo = H;
     PROF(7, launch_gemm(bf, EPI_PARTIAL, MT, gd, hs));
