@@ -1098,7 +1098,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     go.splits = splits_for(partial_blocks(m->po), m->po.KFr, m->wave_slots / 4);
     go.out = m->part;
     go.ldo = H;
-    PROF(4, launch_gemm(bf, EPI_PARTIAL, MT, go, hs));
+    PROF(4, launch_gemm(bf, EPI_PARTIAL, MT, go, m->wave_slots / 4, hs));
     PROF(5, launch_residual_norm(bf, m->part, go.splits, kRowPad, M, H, H, m->ffn_norm + (int64_t)l * H, eps,
                                 m->x, m->xn, Hp, true, hs));
     // gate/up + SwiGLU
@@ -1114,7 +1114,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     gg.act = m->act;
     gg.ldact = Fp;
     gg.up_tile_off = F / 16;
-    PROF(6, launch_gemm(bf, EPI_SWIGLU, MT, gg, hs));
+    PROF(6, launch_gemm(bf, EPI_SWIGLU, MT, gg, m->wave_slots / 4, hs));
     // down projection + residual + next norm
     GemmArgs gd{};
     gd.W = (const char *)m->wd + (int64_t)l * m->pd.bytes();
@@ -1127,7 +1127,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     gd.splits = splits_for(partial_blocks(m->pd), m->pd.KFr, m->wave_slots / 4);
     gd.out = m->part;
     gd.ldo = H;
-    PROF(7, launch_gemm(bf, EPI_PARTIAL, MT, gd, hs));
+    PROF(7, launch_gemm(bf, EPI_PARTIAL, MT, gd, m->wave_slots / 4, hs));
     const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
     PROF(5, launch_residual_norm(bf, m->part, gd.splits, kRowPad, M, H, H, next_gain, eps, m->x, m->xn, Hp,
                                 true, hs));
@@ -1147,7 +1147,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   gl.amax = m->amax;
   gl.logits = logits;
   gl.ldlog = V;
-  PROF(8, launch_gemm(bf, EPI_ARGMAX, MT, gl, hs));
+  PROF(8, launch_gemm(bf, EPI_ARGMAX, MT, gl, m->wave_slots / 4, hs));
   const int nparts = (int)((m->plm.NT + gemm_tiles_per_block(EPI_ARGMAX, MT) - 1) /
                            gemm_tiles_per_block(EPI_ARGMAX, MT));
   PROF(9, launch_argmax_accept(m->amax, nparts, rows, tree, draft, m->pred, res, hs));
@@ -1571,7 +1571,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       gl.amax = m->amax;
       gl.logits = logits_last;
       gl.ldlog = V;
-      HIPCHK(launch_gemm(bf, EPI_ARGMAX, 1, gl, hs));
+      HIPCHK(launch_gemm(bf, EPI_ARGMAX, 1, gl, m->wave_slots / 4, hs));
     }
   }
   kv->host_bound += n;

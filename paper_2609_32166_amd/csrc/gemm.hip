@@ -81,25 +81,27 @@ hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers,
 // ---------------------------------------------------------------------------
 
 
-// n tiles per block. With three 16-row X tiles the X fragments outweigh the
-// W fragments they meet, and each X load instruction costs about as much as a
-// W load whatever its bytes, so a wave takes four W tiles (the partial-sum
-// projections) or six (gate/up: three gate/up pairs, three fragment slots in
-// flight, two blocks per CU) to reuse each X fragment more often. Per tile the
-// sums are the same: a tile's k range and its split of the range over the
-// waves do not depend on how many tiles share the block.
-template <int EPI, int MT> struct EpiTiles {
-  static constexpr int NT = EPI == EPI_ARGMAX ? 4 : MT == 3 ? (EPI == EPI_SWIGLU ? 6 : 4) : 2;
+// n tiles per block. Each X load instruction costs about as much as a W
+// load whatever its bytes, so the more X tiles (rows) a step has, the more W
+// tiles a block should meet each X fragment with. The partial-sum projections
+// take four W tiles at three X tiles, two otherwise. Gate/up takes NP
+// gate/up pairs, chosen on the host from the model's gate tiles against the
+// CUs (gemm_swiglu_pairs). Per tile the sums are the same: a tile's k range
+// and its split of the range over the waves do not depend on how many tiles
+// share the block.
+template <int EPI, int MT, int NP> struct EpiTiles {
+  static constexpr int NT = EPI == EPI_ARGMAX ? 4 : EPI == EPI_SWIGLU ? 2 * NP : MT == 3 ? 4 : 2;
   static constexpr int kU = NT >= 6 ? 3 : NT >= 4 ? 4 : 6;  // fragment slots in flight per wave
-  static constexpr int MinBlocks = EPI == EPI_SWIGLU && MT == 3 ? 2 : 1;  // blocks per CU
+  // three pairs at three X tiles run two blocks per CU (206 registers)
+  static constexpr int MinBlocks = EPI == EPI_SWIGLU && NP == 3 && MT == 3 ? 2 : 1;
 };
 
 __device__ inline float silu(float g) { return g / (1.0f + expf(-g)); }
 
-template <typename T, int MT, int EPI>
-__global__ __launch_bounds__(256, (EpiTiles<EPI, MT>::MinBlocks)) void k_gemm(GemmArgs a) {
-  constexpr int NT = EpiTiles<EPI, MT>::NT;
-  constexpr int kU = EpiTiles<EPI, MT>::kU;
+template <typename T, int MT, int EPI, int NP>
+__global__ __launch_bounds__(256, (EpiTiles<EPI, MT, NP>::MinBlocks)) void k_gemm(GemmArgs a) {
+  constexpr int NT = EpiTiles<EPI, MT, NP>::NT;
+  constexpr int kU = EpiTiles<EPI, MT, NP>::kU;
   constexpr int E = Elem<T>::E;
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
@@ -110,9 +112,9 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT>::MinBlocks)) void k_gemm(Ge
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
     if (EPI == EPI_SWIGLU) {  // gate tiles first, then their up tiles
-      constexpr int NP = NT / 2;
-      const int64_t t = (int64_t)blockIdx.x * NP + j % NP;
-      tile[j] = j < NP ? t : t + a.up_tile_off;
+      constexpr int PR = NT / 2;
+      const int64_t t = (int64_t)blockIdx.x * PR + j % PR;
+      tile[j] = j < PR ? t : t + a.up_tile_off;
       tv[j] = t < a.up_tile_off;
     } else {
       tile[j] = (int64_t)blockIdx.x * NT + j;
@@ -207,13 +209,13 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT>::MinBlocks)) void k_gemm(Ge
         *(float4 *)(a.out + (s * kRowPad + row) * a.ldo + col) = make_float4(v[0], v[1], v[2], v[3]);
       }
     } else {  // EPI_SWIGLU
-      constexpr int NP = NT / 2;
+      constexpr int PR = NT / 2;
 #pragma unroll
-      for (int k = 0; k < MT * NP; ++k) {
-        const int m = k / NP, p = k % NP;
+      for (int k = 0; k < MT * PR; ++k) {
+        const int m = k / PR, p = k % PR;
         const int row = m * 16 + (lane & 15);
         if (k % 4 != wid || row >= a.M || !tv[p]) continue;
-        const f32x4 g = sum4(m, p), u = sum4(m, p + NP);
+        const f32x4 g = sum4(m, p), u = sum4(m, p + PR);
         // act is the next GEMM's X: fragment-packed; the four columns stay in
         // one E-element chunk
         const int64_t col = tile[p] * 16 + 4 * q;
@@ -299,37 +301,51 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT>::MinBlocks)) void k_gemm(Ge
 }
 
 int gemm_tiles_per_block(int epi, int mt) {
-  // SwiGLU blocks are counted in gate tiles (each with its up tile)
   if (epi == EPI_ARGMAX) return 4;
-  const int nt = mt == 3 ? (epi == EPI_SWIGLU ? 6 : 4) : 2;
-  return epi == EPI_SWIGLU ? nt / 2 : nt;
+  return mt == 3 ? 4 : 2;  // partial-sum projections
 }
 
-template <typename T, int EPI>
+// Gate/up pairs per block: three when the three-pair blocks fit one per CU,
+// or (at three X tiles, where X reuse matters most) two per CU; otherwise
+// one, whose many small blocks fill the CUs more evenly. Measured: 3B (688
+// gate tiles) three pairs at 17 rows 19.4 -> 18.1 us, at 49 rows 25.0 -> 19.6
+// us; 7B (1184) at 33 rows two pairs 53.7 us, three 52.2 us; at 17 rows one
+// pair 49.2 us, three 49.6 us.
+int gemm_swiglu_pairs(int mt, int64_t gate_tiles, int cus) {
+  const int64_t b3 = (gate_tiles + 2) / 3;
+  if (b3 <= cus || (mt == 3 && b3 <= 2 * (int64_t)cus)) return 3;
+  return 1;
+}
+
+template <typename T, int EPI, int NP>
 static hipError_t launch_t(int mt, const GemmArgs &a, dim3 grid, hipStream_t s) {
   switch (mt) {
-    case 1: return launch_k(k_gemm<T, 1, EPI>, grid, 256, s, a);
-    case 2: return launch_k(k_gemm<T, 2, EPI>, grid, 256, s, a);
-    case 3: return launch_k(k_gemm<T, 3, EPI>, grid, 256, s, a);
-    case 4: return launch_k(k_gemm<T, 4, EPI>, grid, 256, s, a);
-    case 5: return launch_k(k_gemm<T, 5, EPI>, grid, 256, s, a);
+    case 1: return launch_k(k_gemm<T, 1, EPI, NP>, grid, 256, s, a);
+    case 2: return launch_k(k_gemm<T, 2, EPI, NP>, grid, 256, s, a);
+    case 3: return launch_k(k_gemm<T, 3, EPI, NP>, grid, 256, s, a);
+    case 4: return launch_k(k_gemm<T, 4, EPI, NP>, grid, 256, s, a);
+    case 5: return launch_k(k_gemm<T, 5, EPI, NP>, grid, 256, s, a);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
-hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, hipStream_t s) {
+hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, int cus, hipStream_t s) {
+  if (epi == EPI_SWIGLU) {
+    const int np = gemm_swiglu_pairs(mt, a.up_tile_off, cus);
+    const dim3 grid((unsigned)((a.up_tile_off + np - 1) / np), (unsigned)a.splits);
+    if (np == 3) return bf16 ? launch_t<bf16_t, EPI_SWIGLU, 3>(mt, a, grid, s)
+                             : launch_t<float, EPI_SWIGLU, 3>(mt, a, grid, s);
+    return bf16 ? launch_t<bf16_t, EPI_SWIGLU, 1>(mt, a, grid, s) : launch_t<float, EPI_SWIGLU, 1>(mt, a, grid, s);
+  }
   const int tpb = gemm_tiles_per_block(epi, mt);
-  const int64_t nb = ((epi == EPI_SWIGLU ? a.up_tile_off : a.NTtot) + tpb - 1) / tpb;
+  const int64_t nb = (a.NTtot + tpb - 1) / tpb;
   dim3 grid((unsigned)nb, (unsigned)a.splits);
   if (bf16) {
-    if (epi == EPI_PARTIAL) return launch_t<bf16_t, EPI_PARTIAL>(mt, a, grid, s);
-    if (epi == EPI_SWIGLU) return launch_t<bf16_t, EPI_SWIGLU>(mt, a, grid, s);
-    return launch_t<bf16_t, EPI_ARGMAX>(mt, a, grid, s);
+    if (epi == EPI_PARTIAL) return launch_t<bf16_t, EPI_PARTIAL, 0>(mt, a, grid, s);
+    return launch_t<bf16_t, EPI_ARGMAX, 0>(mt, a, grid, s);
   }
-  if (epi == EPI_PARTIAL) return launch_t<float, EPI_PARTIAL>(mt, a, grid, s);
-  if (epi == EPI_SWIGLU) return launch_t<float, EPI_SWIGLU>(mt, a, grid, s);
-  return launch_t<float, EPI_ARGMAX>(mt, a, grid, s);
+  if (epi == EPI_PARTIAL) return launch_t<float, EPI_PARTIAL, 0>(mt, a, grid, s);
+  return launch_t<float, EPI_ARGMAX, 0>(mt, a, grid, s);
 }
 
 }  // namespace pf

@@ -402,7 +402,11 @@ __host__ __device__ inline int rope_paired_col(int d, int hd) {
 }
 
 // Tiles per block along N for each epilogue.
-int gemm_tiles_per_block(int epi, int mt);
-hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, hipStream_t s);
+int gemm_tiles_per_block(int epi, int mt);  // partial-sum and argmax epilogues
+// gate/up pairs per block for a model with gate_tiles 16-row gate tiles
+int gemm_swiglu_pairs(int mt, int64_t gate_tiles, int cus);
+// cus: compute units of the device (gate/up's block shape depends on the
+// model's tiles against it)
+hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, int cus, hipStream_t s);
 
 }  // namespace pf
