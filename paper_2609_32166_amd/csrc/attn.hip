@@ -357,19 +357,26 @@ __global__ __launch_bounds__(64, WPE) void k_attn(AttnArgs a) {
 // sums are added in wave order, so the result does not depend on timing.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
-  constexpr int NU = 16, NC = HD / 64;
+  // A split's partial row (HD floats) is read by HD/4 lanes with 16-byte
+  // loads, so one wave load covers SPW splits; wave w takes splits w, w + 4,
+  // ... (up to 64 in all). Sums per dimension: over a lane's splits in
+  // order, then over the lanes holding the same dimensions (xor pattern, in
+  // fixed order), then over the waves 0..3.
+  constexpr int LPS = HD / 4;     // lanes per split row
+  constexpr int SPW = 64 / LPS;   // splits per wave load
+  constexpr int NUI = 16 / SPW;   // wave loads per lane (16 splits per wave)
   const int j = blockIdx.x, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int sub = lane / LPS, c4 = lane % LPS;
   const float *pml = a.part_ml + ((int64_t)h * a.n_splits * a.rowpad) * 2;
   const float *po = a.part_o + ((int64_t)h * a.n_splits * a.rowpad) * HD;
   const int ns = a.n_splits;
-  float v[NU][NC];
+  float4 v[NUI];
 #pragma unroll
-  for (int u = 0; u < NU; ++u) {
-    const int sp = wid + 4 * u;
-#pragma unroll
-    for (int i = 0; i < NC; ++i)
-      v[u][i] = sp < ns ? po[((int64_t)sp * a.rowpad + j) * HD + lane + 64 * i] : 0.f;
+  for (int u = 0; u < NUI; ++u) {
+    const int sp = wid + 4 * (u * SPW + sub);
+    v[u] = sp < ns ? *(const float4 *)(po + ((int64_t)sp * a.rowpad + j) * HD + 4 * c4)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   float mv = -INFINITY, lv = 0.f;
   if (wid == 0 && lane < ns) {
@@ -380,7 +387,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   const int used = min(ns, (P + a.M + a.chunk_keys - 1) / a.chunk_keys);
   __shared__ float ws[64];
   __shared__ float s_den;
-  __shared__ float red[4][HD];
+  __shared__ float4 red[4][LPS];
   if (wid == 0) {
     // splits past the used ones hold stale data: weight zero, outputs skipped
     const float m = lane < used ? mv : -INFINITY, l = lane < used ? lv : 0.f;
@@ -391,28 +398,44 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
     if (lane == 0) s_den = den;
   }
   __syncthreads();
-  float acc[NC];
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int i = 0; i < NC; ++i) acc[i] = 0.f;
-#pragma unroll
-  for (int u = 0; u < NU; ++u) {
-    const int sp = wid + 4 * u;
-#pragma unroll
-    for (int i = 0; i < NC; ++i) acc[i] += sp < used ? ws[sp] * v[u][i] : 0.f;
+  for (int u = 0; u < NUI; ++u) {
+    const int sp = wid + 4 * (u * SPW + sub);
+    if (sp < used) {
+      const float w = ws[sp];
+      acc.x += w * v[u].x;
+      acc.y += w * v[u].y;
+      acc.z += w * v[u].z;
+      acc.w += w * v[u].w;
+    }
   }
+  // lanes c4 + LPS * sub hold the same dimensions: add them in sub order
 #pragma unroll
-  for (int i = 0; i < NC; ++i) red[wid][lane + 64 * i] = acc[i];
+  for (int o = LPS; o < 64; o <<= 1) {
+    float4 b;
+    b.x = __shfl_xor(acc.x, o, 64);
+    b.y = __shfl_xor(acc.y, o, 64);
+    b.z = __shfl_xor(acc.z, o, 64);
+    b.w = __shfl_xor(acc.w, o, 64);
+    const bool low = (lane & o) == 0;  // the lower sub keeps its sum first
+    acc = low ? make_float4(acc.x + b.x, acc.y + b.y, acc.z + b.z, acc.w + b.w)
+              : make_float4(b.x + acc.x, b.y + acc.y, b.z + acc.z, b.w + acc.w);
+  }
+  if (sub == 0) red[wid][c4] = acc;
   __syncthreads();
-  if (wid != 0) return;
+  if (wid != 0 || sub != 0) return;
   const float den = s_den;
+  const float4 r0 = red[0][c4], r1 = red[1][c4], r2 = red[2][c4], r3 = red[3][c4];
+  const float tot[4] = {((r0.x + r1.x) + r2.x) + r3.x, ((r0.y + r1.y) + r2.y) + r3.y,
+                        ((r0.z + r1.z) + r2.z) + r3.z, ((r0.w + r1.w) + r2.w) + r3.w};
   T *out = (T *)a.out;
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int d = lane + 64 * i;
-    const float tot = ((red[0][d] + red[1][d]) + red[2][d]) + red[3][d];
+  for (int i = 0; i < 4; ++i) {
+    const int d = 4 * c4 + i;
     const int64_t k = h * HD + d;
     Elem<T>::store(out, a.out_packed ? act_off<T>(j, k, a.ldout) : (int64_t)j * a.ldout + k,
-                   tot / den);
+                   tot[i] / den);
   }
 }
 
