@@ -522,11 +522,20 @@ def read_ceiling(torch, pf, nbytes=1 << 30, reps=10):
     pf.pf_read_stream(buf, sink)
     g = _capture(torch, lambda: [pf.pf_read_stream(buf, sink) for _ in range(reps)])
     ms = _time_graph(torch, g, 5) / reps
-    del buf, sink, g
+    del buf, g
+    # kernel boundary inside a graph: the same kernel over 16 KiB (one block
+    # per CU, next to no work), many launches back to back
+    small = torch.ones(4096, dtype=torch.int32, device="cuda")
+    n_small = 200
+    pf.pf_read_stream(small, sink)
+    g = _capture(torch, lambda: [pf.pf_read_stream(small, sink) for _ in range(n_small)])
+    us_launch = _time_graph(torch, g, 5) / n_small * 1e3
+    del small, sink, g
     torch.cuda.empty_cache()
     return {"GBps": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes,
             "us_per_read": round(ms * 1e3, 2),
-            "kernel": "pf_read_stream (one block per CU, 8 x 16 B loads in flight per lane)"}
+            "kernel": "pf_read_stream (one block per CU, 8 x 16 B loads in flight per lane)",
+            "us_per_graph_launch_16KiB": round(us_launch, 2)}
 
 
 def kernel_times(torch, pf, wl, model, kv, c, ctx, st, draft, res, min_launches=24):

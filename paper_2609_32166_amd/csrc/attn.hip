@@ -37,6 +37,19 @@ template <> __device__ inline uint4 pack_probs<bf16_t>(const float *p) {
     w[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){p[2 * i], p[2 * i + 1]}, b2));
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
+// The rounding residue of eight bf16-packed probabilities as a second bf16
+// operand: the value product takes each probability as hi + lo, about 16
+// significant bits (the precision contract rounds no probability).
+__device__ inline uint4 pack_probs_lo(const float *p, const uint4 &hi) {
+  const uint32_t w[4] = {hi.x, hi.y, hi.z, hi.w};
+  float lo[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint32_t h = (e & 1) ? (w[e >> 1] & 0xFFFF0000u) : (w[e >> 1] << 16);
+    lo[e] = p[e] - __uint_as_float(h);
+  }
+  return pack_probs<bf16_t>(lo);
+}
 
 // E consecutive keys key0 .. key0 + E - 1 of dimension dim from [slot][hd]
 // value rows, packed as one 16-byte operand chunk (key0 + e in element e);
@@ -275,6 +288,11 @@ __global__ __launch_bounds__(64, WPE) void k_attn(AttnArgs a) {
       const uint4 pu = pack_probs<T>(p);
 #pragma unroll
       for (int t = 0; t < NDT; ++t) o[r][t] = mma<T>(vf[slot][t], pu, o[r][t]);
+      if constexpr (sizeof(T) == 2) {
+        const uint4 pl = pack_probs_lo(p, pu);
+#pragma unroll
+        for (int t = 0; t < NDT; ++t) o[r][t] = mma<T>(vf[slot][t], pl, o[r][t]);
+      }
     }
     if constexpr (NS == 1) load_v(0, c + 1);
   };
@@ -640,7 +658,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
       m_run = m_new;
     }
     const float msc = m_run == -INFINITY ? 0.f : m_run * sc;
-    uint4 pb[2][2];  // P^T operand of each 16-key step
+    uint4 pb[2][2], pl[2][2];  // P^T operand of each 16-key step, as hi + lo
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
@@ -652,6 +670,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
           l_run += pv[e];
         }
         pb[st][s2] = pack_probs<bf16_t>(pv);
+        pl[st][s2] = pack_probs_lo(pv, pb[st][s2]);
       }
 #pragma unroll
     for (int st = 0; st < 2; ++st)
@@ -660,7 +679,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
 #pragma unroll
         for (int dt = 0; dt < HD / 32; ++dt) {
           const int d = 32 * dt + r32, c = 4 * st + 2 * s2 + hh;
-          o[dt] = mma32(lv[buf][d][c ^ ((d >> 1) & 7)], pb[st][s2], o[dt]);
+          const uint4 vv = lv[buf][d][c ^ ((d >> 1) & 7)];
+          o[dt] = mma32(vv, pb[st][s2], o[dt]);
+          o[dt] = mma32(vv, pl[st][s2], o[dt]);
         }
     }
     if (it + 1 < ntiles) lstore(buf ^ 1, kt + kPreKeys);
