@@ -84,13 +84,13 @@ hipError_t launch_pack(const void *src, int64_t N, int64_t K, int64_t layers,
 // n tiles per block. Each X load instruction costs about as much as a W
 // load whatever its bytes, so the more X tiles (rows) a step has, the more W
 // tiles a block should meet each X fragment with. The partial-sum projections
-// take four W tiles at three X tiles, two otherwise. Gate/up takes NP
-// gate/up pairs, chosen on the host from the model's gate tiles against the
-// CUs (gemm_swiglu_pairs). Per tile the sums are the same: a tile's k range
-// and its split of the range over the waves do not depend on how many tiles
-// share the block.
+// take NP = 2 or 4 W tiles (gemm_partial_tiles), gate/up NP gate/up pairs
+// (gemm_swiglu_pairs), both chosen on the host from the model's tiles against
+// the CUs; the lm_head takes four. Per tile the sums are the same: a tile's k
+// range and its split of the range over the waves do not depend on how many
+// tiles share the block.
 template <int EPI, int MT, int NP> struct EpiTiles {
-  static constexpr int NT = EPI == EPI_ARGMAX ? 4 : EPI == EPI_SWIGLU ? 2 * NP : MT == 3 ? 4 : 2;
+  static constexpr int NT = EPI == EPI_ARGMAX ? 4 : EPI == EPI_SWIGLU ? 2 * NP : NP;
   static constexpr int kU = NT >= 6 ? 3 : NT >= 4 ? 4 : 6;  // fragment slots in flight per wave
   // three pairs at three X tiles run two blocks per CU (206 registers)
   static constexpr int MinBlocks = EPI == EPI_SWIGLU && NP == 3 && MT == 3 ? 2 : 1;
@@ -301,8 +301,19 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT, NP>::MinBlocks)) void k_gem
 }
 
 int gemm_tiles_per_block(int epi, int mt) {
-  if (epi == EPI_ARGMAX) return 4;
-  return mt == 3 ? 4 : 2;  // partial-sum projections
+  (void)mt;
+  return epi == EPI_ARGMAX ? 4 : 2;  // argmax; partial-sum projections counted at two
+}
+
+// W tiles per block of a partial-sum projection: four at three X tiles, and
+// at two or more while the four-tile blocks (ntiles/4 x splits) still fill
+// 7/8 of the CUs; two otherwise. Measured: 7B (224 tiles, 4 splits) at 17
+// rows down 27.2 -> 23.9 us and O 9.0 -> 7.1 us with four; 3B (128 tiles)
+// keeps two (four at 8 splits: down 11.2 -> 11.8 us).
+int gemm_partial_tiles(int mt, int64_t ntiles, int splits, int cus) {
+  if (mt == 3) return 4;
+  const int64_t b4 = (ntiles + 3) / 4 * splits;
+  return mt >= 2 && 8 * b4 >= 7 * (int64_t)cus ? 4 : 2;
 }
 
 // Gate/up pairs per block: three when the three-pair blocks fit one per CU,
@@ -337,15 +348,16 @@ hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, int cus, h
                              : launch_t<float, EPI_SWIGLU, 3>(mt, a, grid, s);
     return bf16 ? launch_t<bf16_t, EPI_SWIGLU, 1>(mt, a, grid, s) : launch_t<float, EPI_SWIGLU, 1>(mt, a, grid, s);
   }
-  const int tpb = gemm_tiles_per_block(epi, mt);
-  const int64_t nb = (a.NTtot + tpb - 1) / tpb;
-  dim3 grid((unsigned)nb, (unsigned)a.splits);
-  if (bf16) {
-    if (epi == EPI_PARTIAL) return launch_t<bf16_t, EPI_PARTIAL, 0>(mt, a, grid, s);
-    return launch_t<bf16_t, EPI_ARGMAX, 0>(mt, a, grid, s);
+  if (epi == EPI_PARTIAL) {
+    const int nt = gemm_partial_tiles(mt, a.NTtot, a.splits, cus);
+    const dim3 grid((unsigned)((a.NTtot + nt - 1) / nt), (unsigned)a.splits);
+    if (nt == 4) return bf16 ? launch_t<bf16_t, EPI_PARTIAL, 4>(mt, a, grid, s)
+                             : launch_t<float, EPI_PARTIAL, 4>(mt, a, grid, s);
+    return bf16 ? launch_t<bf16_t, EPI_PARTIAL, 2>(mt, a, grid, s) : launch_t<float, EPI_PARTIAL, 2>(mt, a, grid, s);
   }
-  if (epi == EPI_PARTIAL) return launch_t<float, EPI_PARTIAL, 0>(mt, a, grid, s);
-  return launch_t<float, EPI_ARGMAX, 0>(mt, a, grid, s);
+  const int tpb = gemm_tiles_per_block(epi, mt);
+  const dim3 grid((unsigned)((a.NTtot + tpb - 1) / tpb), (unsigned)a.splits);
+  return bf16 ? launch_t<bf16_t, EPI_ARGMAX, 0>(mt, a, grid, s) : launch_t<float, EPI_ARGMAX, 0>(mt, a, grid, s);
 }
 
 }  // namespace pf

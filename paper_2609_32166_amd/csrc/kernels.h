@@ -402,7 +402,9 @@ __host__ __device__ inline int rope_paired_col(int d, int hd) {
 }
 
 // Tiles per block along N for each epilogue.
-int gemm_tiles_per_block(int epi, int mt);  // partial-sum and argmax epilogues
+int gemm_tiles_per_block(int epi, int mt);  // argmax; partial-sum counted at two
+// W tiles per block of a partial-sum projection (ntiles 16-row tiles, splits)
+int gemm_partial_tiles(int mt, int64_t ntiles, int splits, int cus);
 // gate/up pairs per block for a model with gate_tiles 16-row gate tiles
 int gemm_swiglu_pairs(int mt, int64_t gate_tiles, int cus);
 // cus: compute units of the device (gate/up's block shape depends on the
