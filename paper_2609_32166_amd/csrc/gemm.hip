@@ -316,26 +316,36 @@ int gemm_partial_tiles(int mt, int64_t ntiles, int splits, int cus) {
   return mt >= 2 && 8 * b4 >= 7 * (int64_t)cus ? 4 : 2;
 }
 
-// Gate/up pairs per block: three when the three-pair blocks fit one per CU,
-// or (at three X tiles, where X reuse matters most) two per CU; otherwise
-// one, whose many small blocks fill the CUs more evenly. Measured: 3B (688
-// gate tiles) three pairs at 17 rows 19.4 -> 18.1 us, at 49 rows 25.0 -> 19.6
-// us; 7B (1184) at 33 rows two pairs 53.7 us, three 52.2 us; at 17 rows one
-// pair 49.2 us, three 49.6 us.
+// Gate/up pairs per block: the fewest of three or five whose blocks fit one
+// per CU (five only up to three X tiles, whose epilogue then fills 120 KB of
+// LDS), else three at three X tiles where those blocks fit two per CU (X reuse
+// matters most there), else one: many small blocks fill the CUs evenly.
+// Measured: 3B (688 gate tiles) three pairs, at 17 rows 19.4 -> 18.1 us and
+// at 49 rows 25.0 -> 19.5 us against one; 7B (1184) five pairs (237 blocks),
+// at 33 rows 52.4 us with three -> 49.3 us, at 17 rows 49.2 us with one ->
+// 48.1 us.
 int gemm_swiglu_pairs(int mt, int64_t gate_tiles, int cus) {
-  const int64_t b3 = (gate_tiles + 2) / 3;
-  if (b3 <= cus || (mt == 3 && b3 <= 2 * (int64_t)cus)) return 3;
+  const int64_t b3 = (gate_tiles + 2) / 3, b5 = (gate_tiles + 4) / 5;
+  if (b3 <= cus) return 3;
+  if (mt <= 3 && b5 <= cus) return 5;
+  if (mt == 3 && b3 <= 2 * (int64_t)cus) return 3;
   return 1;
 }
 
 template <typename T, int EPI, int NP>
 static hipError_t launch_t(int mt, const GemmArgs &a, dim3 grid, hipStream_t s) {
+  // five gate/up pairs exist up to three X tiles only (LDS)
+  constexpr bool wide = EPI == EPI_SWIGLU && NP == 5;
   switch (mt) {
     case 1: return launch_k(k_gemm<T, 1, EPI, NP>, grid, 256, s, a);
     case 2: return launch_k(k_gemm<T, 2, EPI, NP>, grid, 256, s, a);
     case 3: return launch_k(k_gemm<T, 3, EPI, NP>, grid, 256, s, a);
-    case 4: return launch_k(k_gemm<T, 4, EPI, NP>, grid, 256, s, a);
-    case 5: return launch_k(k_gemm<T, 5, EPI, NP>, grid, 256, s, a);
+    case 4:
+      if constexpr (!wide) return launch_k(k_gemm<T, 4, EPI, NP>, grid, 256, s, a);
+      return hipErrorInvalidValue;
+    case 5:
+      if constexpr (!wide) return launch_k(k_gemm<T, 5, EPI, NP>, grid, 256, s, a);
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }
@@ -346,6 +356,8 @@ hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, int cus, h
     const dim3 grid((unsigned)((a.up_tile_off + np - 1) / np), (unsigned)a.splits);
     if (np == 3) return bf16 ? launch_t<bf16_t, EPI_SWIGLU, 3>(mt, a, grid, s)
                              : launch_t<float, EPI_SWIGLU, 3>(mt, a, grid, s);
+    if (np == 5) return bf16 ? launch_t<bf16_t, EPI_SWIGLU, 5>(mt, a, grid, s)
+                             : launch_t<float, EPI_SWIGLU, 5>(mt, a, grid, s);
     return bf16 ? launch_t<bf16_t, EPI_SWIGLU, 1>(mt, a, grid, s) : launch_t<float, EPI_SWIGLU, 1>(mt, a, grid, s);
   }
   if (epi == EPI_PARTIAL) {
