@@ -967,10 +967,10 @@ static int attn_range_keys(int64_t keys_max, bool bf, int nq, int wave_slots) {
 }
 
 // Grouped attention (bf16, head_dim 128): keys per range, a multiple of the
-// 32-key chunk, sized so that one KV head has at most T ranges, T = the
+// 64-key phase, sized so that one KV head has at most T ranges, T = the
 // resident blocks (two per compute unit) over four row groups per KV head,
 // at most the combine's 64. The length depends on the row count only
-// through the key bound (ceil(keys / (32 T)) changes every 32 T keys), so a
+// through the key bound (ceil(keys / (64 T)) changes every 64 T keys), so a
 // verify row reproduces the single-row step at its position bit for bit
 // unless the two key bounds straddle such a step.
 static int attn_gq_range_keys(int64_t keys_max, int nkv, int cus) {
@@ -978,7 +978,10 @@ static int attn_gq_range_keys(int64_t keys_max, int nkv, int cus) {
   if (target > kMaxSplitsAttn) target = kMaxSplitsAttn;
   if (target < 1) target = 1;
   const int64_t per = (keys_max + target - 1) / target;
-  return (int)(((per + 31) / 32) * 32);
+  // whole 64-key phases of the kernel: a range that ends half way through a
+  // phase costs the phase anyway (3B: 96 -> 128 keys, 43 -> 33 ranges, 264 ->
+  // 216 blocks; 3B tree 616 -> 504 blocks, within the resident 512)
+  return (int)(((per + 63) / 64) * 64);
 }
 
 // Probabilities enter the grouped attention's value product as two bf16
