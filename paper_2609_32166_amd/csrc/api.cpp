@@ -131,11 +131,11 @@ template <typename T> pf_status dev_alloc(T **p, int64_t bytes, int64_t *total) 
 void prefill_free(pf_model *m) {
   void *ptrs[] = {m->pre_x, m->pre_y, m->pre_rope, m->pre_apo, m->pre_apml, m->pre_xn,
                   m->pre_qb, m->pre_attn, m->pre_act, m->pre_rowinfo, m->pre_status,
-                  m->pre_part};
+                  m->pre_part, m->pre_xb};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   m->pre_x = m->pre_y = m->pre_rope = m->pre_apo = m->pre_apml = m->pre_part = nullptr;
-  m->pre_xn = m->pre_qb = m->pre_attn = m->pre_act = nullptr;
+  m->pre_xn = m->pre_qb = m->pre_attn = m->pre_act = m->pre_xb = nullptr;
   m->pre_rowinfo = m->pre_status = nullptr;
   m->pre_rows = 0;
 }
@@ -1390,12 +1390,17 @@ static pf_status prefill_alloc(pf_model *m, int64_t rows) {
   PALLOC(m->pre_act, R * Fp * m->esz);
   PALLOC(m->pre_rowinfo, R * 4 * 4);
   PALLOC(m->pre_status, 64);
-  if (m->cfg.dtype == PF_DTYPE_BF16)
+  if (m->cfg.dtype == PF_DTYPE_BF16) {
     PALLOC(m->pre_part, (int64_t)kPreSplitsMax * R * std::max<int64_t>(q + 2 * kv, H) * 4);
+    PALLOC(m->pre_xb, R * Hp * 2);
+  }
 #undef PALLOC
-  void *zero[] = {m->pre_xn, m->pre_qb, m->pre_attn, m->pre_act, m->pre_status};
-  int64_t zb[] = {R * Hp * m->esz, R * q * m->esz, R * qp * m->esz, R * Fp * m->esz, 64};
-  for (int i = 0; i < 5; ++i) HIPCHK(hipMemset(zero[i], 0, zb[i]));
+  // zero padding columns and rows stay zero: the norms write columns < H and
+  // the GEMM epilogues skip rows past the chunk
+  void *zero[] = {m->pre_xn, m->pre_qb, m->pre_attn, m->pre_act, m->pre_status, m->pre_xb};
+  int64_t zb[] = {R * Hp * m->esz, R * q * m->esz, R * qp * m->esz, R * Fp * m->esz, 64, R * Hp * 2};
+  for (int i = 0; i < 6; ++i)
+    if (zero[i]) HIPCHK(hipMemset(zero[i], 0, zb[i]));
   HIPCHK(hipDeviceSynchronize());
   m->pre_rows = R;
   return PF_OK;
@@ -1510,9 +1515,10 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
         go.y = m->pre_part;
         go.ystride = (int64_t)R * H;
         HIPCHK(prefill_gemm(bf, BIG_STORE, go, hs));
+        // the FFN input goes out in the 32-row packed layout of the SwiGLU GEMM
         HIPCHK(launch_residual_norm(bf, m->pre_part, go.splits, R, rows, H, H,
-                                    m->ffn_norm + (int64_t)l * H, eps, m->pre_x, m->pre_xn, Hp,
-                                    false, hs));
+                                    m->ffn_norm + (int64_t)l * H, eps, m->pre_x, m->pre_xb, Hp, 2,
+                                    hs));
       } else {
         go.y = m->pre_x;
         HIPCHK(prefill_gemm(bf, BIG_RESID, go, hs));
@@ -1531,7 +1537,12 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
       gg.act = m->pre_act;
       gg.ldact = Fp;
       gg.up_tile_off = F / 16;
-      HIPCHK(prefill_gemm(bf, BIG_SWIGLU, gg, hs));
+      if (bf) {
+        gg.X = m->pre_xb;
+        HIPCHK(launch_gemm_ffn(gg, hs));
+      } else {
+        HIPCHK(prefill_gemm(bf, BIG_SWIGLU, gg, hs));
+      }
       BigGemmArgs gd{};
       gd.W = (const char *)m->wd + (int64_t)l * m->pd.bytes();
       gd.W_bytes = m->pd.bytes();

@@ -174,14 +174,16 @@ struct StepArgs {
 hipError_t launch_prep(const StepArgs &a, hipStream_t s);
 hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
                              const float *gain, float eps, float *x, void *xn, int64_t ldxn,
-                             bool packed, hipStream_t s);
+                             int packed, hipStream_t s);
 hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int rowpad, int M, int nq,
                            int nkv, int hd, int64_t ldpart, const float *rope, const int32_t *kv_len,
                            void *qbuf, int64_t ldq, void *cache, int layer, int64_t cap,
                            hipStream_t s);
+// packed: the xn layout (xn_index: 0 row-major, 1 verify fragment-packed,
+// 2 prefill 32-row packed, bf16 only)
 hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
                                 int64_t ldpart, const float *gain, float eps, float *x, void *xn,
-                                int64_t ldxn, bool packed, hipStream_t s);
+                                int64_t ldxn, int packed, hipStream_t s);
 // prefill rows: tokens[i] at position P + i (P = *kv_len), RoPE table, rowinfo
 hipError_t launch_prefill_rows(const int32_t *tokens, int n, int V, const int32_t *kv_len,
                                const double *inv_freq, int hd, int32_t *rowinfo, float *rope,
@@ -221,6 +223,9 @@ hipError_t launch_gemm_big(bool bf16, int epi, const BigGemmArgs &a, hipStream_t
 // 32x32 matrix instructions
 // (prefill_gemm.hip); needs x_rows % 128 == 0 and ldx % 32 == 0
 hipError_t launch_gemm_pre(int epi, const BigGemmArgs &a, hipStream_t s);
+// bf16 prefill SwiGLU GEMM over whole chunks (prefill_gemm.hip): X in the
+// 32-row packed layout (xb32_off), x_rows % 32 == 0, ldx >= 32 * KFr
+hipError_t launch_gemm_ffn(const BigGemmArgs &a, hipStream_t s);
 hipError_t launch_argmax_accept(const ArgmaxPart *amax, int nparts, int rows, int tree,
                                 const pf_draft *draft, int32_t *pred, pf_verify_result *res,
                                 hipStream_t s);

@@ -66,6 +66,17 @@ template <typename T> __device__ inline int64_t act_off(int row, int64_t k, int6
          k % E;
 }
 
+// bf16 activation layout read by the prefill SwiGLU GEMM ("32-row packed"):
+// for every 32-row tile and every 16-k step, the 64 lanes' 8-element chunks of
+// the 32x32x16 matrix instruction's B operand are stored contiguously (lane =
+// row % 32 + 32 * (k / 8 % 2)), so a wave's operand is one 1 KiB load. `ld`
+// is the padded row length (a multiple of 32); the size equals that of a
+// row-major [rows][ld] array with rows a multiple of 32.
+__host__ __device__ inline int64_t xb32_off(int row, int64_t k, int64_t ld) {
+  return (((int64_t)(row >> 5) * (ld >> 4) + (k >> 4)) * 64 + ((k >> 3) & 1) * 32 + (row & 31)) * 8 +
+         (k & 7);
+}
+
 // ---------------------------------------------------------------------------
 // MFMA step: D(16x16) += A(16 x KF) * B(KF x 16) where every lane supplies
 // one 16-byte chunk of A and of B. Lane l carries row l%16 of A and column
@@ -175,6 +186,7 @@ struct pf_model {
   void *pre_xn = nullptr, *pre_qb = nullptr, *pre_attn = nullptr, *pre_act = nullptr;
   int32_t *pre_rowinfo = nullptr, *pre_status = nullptr;
   float *pre_part = nullptr;  // split-K partial sums of the bf16 prefill GEMMs
+  void *pre_xb = nullptr;     // bf16: FFN input rows in the 32-row packed layout
   // pinned host staging of the decode iteration (draft and result copies),
   // allocated on its first use
   void *stage = nullptr;

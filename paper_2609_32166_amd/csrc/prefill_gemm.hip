@@ -202,7 +202,156 @@ __global__ __launch_bounds__(256, MINB) void k_gemm_pre(BigGemmArgs a, PreGrid p
   }
 }
 
+// ---------------------------------------------------------------------------
+// SwiGLU projection of a whole chunk, act = silu(X Wg^T) * (X Wu^T), as one
+// pass over the chunk's rows: a block owns NJ gate tiles of 16 columns for up
+// to 512 rows of X, so the 7B-class FFN (1184 gate tiles) takes 237 blocks,
+// one per CU, in a single round. The block's W rows form NJ 32-row A tiles,
+// each the 16 gate rows over the 16 up rows of the same columns, so a lane's
+// gate and up sums of one output sit in the same accumulator (values v and
+// v + 8). Each of the 8 waves owns 64 rows of X (two 32-row B tiles): 16 NJ
+// accumulator tiles of 32x32 per block, 10 per wave.
+//
+// W is read by all eight waves: it is staged in LDS, 64 k a stage (NJ x 4
+// KiB, the packed fragments copied as they are, so a 16-lane group's operand
+// read is 256 contiguous bytes), double-buffered through registers. X is read
+// by one wave only: it comes straight from the 32-row packed layout into the
+// B operands, one 1 KiB load per tile and 16-k step, four steps in flight.
+// ---------------------------------------------------------------------------
+template <int NJ>
+__global__ __launch_bounds__(512, 1) void k_gemm_ffn(BigGemmArgs a) {
+  constexpr int D = 4;               // X ring: one stage of 16-k steps
+  constexpr int WCH = NJ * 256;      // 16-byte W chunks a stage
+  constexpr int WPT = (WCH + 511) / 512;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int r32 = lane & 31, hi = lane >> 5;
+  const int64_t gate_tiles = a.up_tile_off;
+  const int64_t g0 = (int64_t)blockIdx.x * NJ;
+  const int64_t xrow0 = (int64_t)blockIdx.y * 512 + wid * 64;
+  const bool active = xrow0 < a.x_rows;  // wave-uniform
+  const int64_t KFr = a.KFr, ksteps = 2 * KFr, nst = (KFr + 1) / 2;
+  const rsrc_t wr = make_rsrc(a.W, (uint32_t)a.W_bytes);
+  const rsrc_t xr = make_rsrc(a.X, (uint32_t)(a.x_rows * a.ldx * 2));
+
+  // stage chunk c: A tile c >> 8, gate (0) or up (1) half (c >> 7) & 1, byte
+  // (c & 127) * 16 of the two fragments' 2 KiB; tiles past the FFN load zeros
+  __shared__ uint4 lw[2][WCH];
+  uint32_t woff[WPT];
+  bool wval[WPT];
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int c = tid + 512 * i;
+    const int64_t g = g0 + (c >> 8);
+    wval[i] = c < WCH && g < gate_tiles;
+    const int64_t t = g + (((c >> 7) & 1) ? gate_tiles : 0);
+    woff[i] = wval[i] ? (uint32_t)(t * KFr * 1024 + (c & 127) * 16) : 0u;
+  }
+  uint4 ws[WPT];
+  auto wload = [&](int64_t st) {
+#pragma unroll
+    for (int i = 0; i < WPT; ++i) {
+      const int c = tid + 512 * i;
+      // the second fragment of an odd last stage is past the matrix row
+      const bool in = wval[i] && 2 * st + ((c & 127) >> 6) < KFr;
+      ws[i] = bload16_stream(wr, in ? woff[i] + (uint32_t)(st * 2048) : kOOB);
+    }
+  };
+  auto wstore = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < WPT; ++i) {
+      const int c = tid + 512 * i;
+      if (c < WCH) lw[b][c] = ws[i];
+    }
+  };
+
+  // B operand of 16-k step i, tile u: lane's 16 bytes of the 1 KiB chunk
+  const int64_t ldk = a.ldx >> 4;
+  const uint32_t xbase = (uint32_t)((xrow0 >> 5) * ldk * 1024 + lane * 16);
+  uint4 xq[D][2];
+  auto xload = [&](int slot, int64_t i) {
+    const bool in = active && i < ksteps;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      xq[slot][u] = bload16(xr, in ? xbase + (uint32_t)((u * ldk + i) * 1024) : kOOB);
+  };
+  // A operand of step s of a stage, tile j: row r32 (gate rows 0-15, up rows
+  // 16-31), k = 16 (s % 2) + 8 hi .. + 8 of fragment s / 2
+  auto aidx = [&](int j, int s) {
+    return ((j * 2 + (r32 >> 4)) * 2 + (s >> 1)) * 64 + (2 * (s & 1) + hi) * 16 + (r32 & 15);
+  };
+
+  f32x16 acc[NJ][2];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[j][u][v] = 0.f;
+
+#pragma unroll
+  for (int i = 0; i < D; ++i) xload(i, i);
+  wload(0);
+  wstore(0);
+  __syncthreads();
+  for (int64_t st = 0; st < nst; ++st) {
+    const int b = (int)(st & 1);
+    if (st + 1 < nst) wload(st + 1);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (active) {
+        uint4 af[NJ];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) af[j] = lw[b][aidx(j, s)];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) acc[j][u] = mma32(af[j], xq[s][u], acc[j][u]);
+      }
+      xload(s, st * 4 + s + D);
+    }
+    if (st + 1 < nst) wstore(b ^ 1);
+    __syncthreads();
+  }
+  if (!active) return;
+
+  // lane holds D[n = 8 (v / 4) + 4 hi + v % 4][row r32 of its B tile]: gate
+  // column n for v < 8, its up partner at v + 8
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int64_t g = g0 + j;
+    if (g >= gate_tiles) continue;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t row = xrow0 + 32 * u + r32;
+      if (row >= a.M) continue;
+      bf16_t *dst = (bf16_t *)a.act + row * a.ldact + g * 16 + 4 * hi;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        uint2 pk;
+        uint32_t h[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          h[e] = f32_to_bf16(silu_f(acc[j][u][4 * q + e]) * acc[j][u][8 + 4 * q + e]);
+        pk.x = h[0] | (h[1] << 16);
+        pk.y = h[2] | (h[3] << 16);
+        *(uint2 *)(dst + 8 * q) = pk;
+      }
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_gemm_ffn(const BigGemmArgs &a, hipStream_t s) {
+  constexpr int NJ = 5;
+  if (a.x_rows % 32 != 0 || a.ldx % 32 != 0 || a.ldx < 32 * a.KFr || a.ldact % 4 != 0 ||
+      a.W_bytes >= ((int64_t)1 << 31) || a.x_rows * a.ldx * 2 >= ((int64_t)1 << 31) ||
+      a.up_tile_off < 1 || a.M > a.x_rows)
+    return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((a.up_tile_off + NJ - 1) / NJ), (unsigned)((a.x_rows + 511) / 512));
+  PF_TRY(launch_k(k_gemm_ffn<NJ>, grid, 512, s, a));
+  return hipGetLastError();
+}
 
 hipError_t launch_gemm_pre(int epi, const BigGemmArgs &a, hipStream_t s) {
   if (a.x_rows % 128 != 0 || a.ldx % 32 != 0 || a.W_bytes >= ((int64_t)1 << 31) ||

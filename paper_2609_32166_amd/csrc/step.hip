@@ -68,10 +68,13 @@ __device__ inline float block_sum256(float v, float *sh) {
   return sh[0] + sh[1] + sh[2] + sh[3];
 }
 
-// Index of element (row, k) of a normalised-activation buffer: row-major
-// [row][ld], or the fragment-packed layout of the verify GEMM.
+// Index of element (row, k) of a normalised-activation buffer by layout:
+// 0 row-major [row][ld], 1 the fragment-packed layout of the verify GEMM, 2
+// the 32-row packed layout of the prefill SwiGLU GEMM (bf16 only).
 template <typename T> __device__ inline int64_t xn_index(int packed, int row, int64_t k, int64_t ld) {
-  return packed ? act_off<T>(row, k, ld) : (int64_t)row * ld + k;
+  return packed == 1   ? act_off<T>(row, k, ld)
+         : packed == 2 ? xb32_off(row, k, ld)
+                       : (int64_t)row * ld + k;
 }
 
 template <typename T>
@@ -100,13 +103,14 @@ __global__ __launch_bounds__(256) void k_embed_norm(const T *embed, const int32_
 
 hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
                              const float *gain, float eps, float *x, void *xn, int64_t ldxn,
-                             bool packed, hipStream_t s) {
+                             int packed, hipStream_t s) {
+  if (!bf16 && packed == 2) return hipErrorInvalidValue;
   if (bf16)
     PF_TRY(launch_k(k_embed_norm<bf16_t>, M, 256, s, (const bf16_t *)embed, rowinfo, H, gain, eps, x,
-                    (bf16_t *)xn, ldxn, (int)packed));
+                    (bf16_t *)xn, ldxn, packed));
   else
     PF_TRY(launch_k(k_embed_norm<float>, M, 256, s, (const float *)embed, rowinfo, H, gain, eps, x,
-                    (float *)xn, ldxn, (int)packed));
+                    (float *)xn, ldxn, packed));
   return hipGetLastError();
 }
 
@@ -259,27 +263,28 @@ __global__ __launch_bounds__(1024) void k_residual_norm_wide(const float *part, 
 
 hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
                                 int64_t ldpart, const float *gain, float eps, float *x, void *xn,
-                                int64_t ldxn, bool packed, hipStream_t s) {
+                                int64_t ldxn, int packed, hipStream_t s) {
+  if (!bf16 && packed == 2) return hipErrorInvalidValue;
   // rows up to 2048 columns: 256 threads, eight partials in flight; wider
   // rows: a thread per four columns (up to 1024), sixteen in flight
   // (measured: 7B-wide rows 5.6 -> 3.9 us; the wide form was slower at 2048)
   if (H <= 2048) {
     if (bf16)
       PF_TRY(launch_k(k_residual_norm<bf16_t>, M, 256, s, part, splits, rowpad, H, ldpart, gain,
-                      eps, x, (bf16_t *)xn, ldxn, (int)packed));
+                      eps, x, (bf16_t *)xn, ldxn, packed));
     else
       PF_TRY(launch_k(k_residual_norm<float>, M, 256, s, part, splits, rowpad, H, ldpart, gain,
-                      eps, x, (float *)xn, ldxn, (int)packed));
+                      eps, x, (float *)xn, ldxn, packed));
     return hipGetLastError();
   }
   int threads = ((H / 4 + 63) / 64) * 64;
   if (threads > 1024) threads = 1024;
   if (bf16)
     PF_TRY(launch_k(k_residual_norm_wide<bf16_t>, M, threads, s, part, splits, rowpad, H, ldpart, gain,
-                    eps, x, (bf16_t *)xn, ldxn, (int)packed));
+                    eps, x, (bf16_t *)xn, ldxn, packed));
   else
     PF_TRY(launch_k(k_residual_norm_wide<float>, M, threads, s, part, splits, rowpad, H, ldpart, gain,
-                    eps, x, (float *)xn, ldxn, (int)packed));
+                    eps, x, (float *)xn, ldxn, packed));
   return hipGetLastError();
 }
 

@@ -18,6 +18,10 @@ RAGGED = synth.ModelShape(2, 512, 8, 2, 128, 1360, 4000, 1e6, 1e-6, "bf16")
 # query heads per KV head): two heads per KV head, and head_dim 64
 GROUP2 = synth.ModelShape(2, 512, 4, 2, 128, 1360, 4000, 1e6, 1e-6, "bf16")
 HD64 = synth.ModelShape(2, 512, 8, 2, 64, 1360, 4000, 1e4, 1e-6, "bf16")
+# ragged widths for the chunk-wide SwiGLU GEMM: hidden 528 is 17 k fragments
+# of 32 (its last 64-k stage holds one), FFN 1392 is 87 gate tiles of 16
+# columns (its last block of five holds two)
+RAGGED_W = synth.ModelShape(2, 528, 8, 2, 128, 1392, 4000, 1e6, 1e-6, "bf16")
 
 
 @pytest.fixture(scope="module")
@@ -62,8 +66,10 @@ def _prefill_case(pf, shape, seed, P, n, chunk, cap_extra=128):
     (GROUP2, 200, 150, 64),
     (HD64, 200, 150, 64),
     (RAGGED, 100, 5, 1),
+    (RAGGED_W, 150, 130, 130),
+    (RAGGED, 100, 600, 600),
 ], ids=["bf16_chunks", "bf16_one_chunk", "f32_chunks", "bf16_group2", "bf16_hd64",
-        "bf16_single_rows"])
+        "bf16_single_rows", "bf16_ragged_widths", "bf16_chunk_over_512_rows"])
 def test_prefill_matches_oracle(pf, shape, P, n, chunk):
     seed = 4242 + n
     w, kv_host, toks, gpu, kv_new, logits = _prefill_case(pf, shape, seed, P, n, chunk)
