@@ -16,6 +16,8 @@
 // time on one XCD and the slice comes from HBM once into that XCD's L2.
 // Narrow outputs split K into partial sums that the following reduction
 // kernel adds in split order.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace pf {
@@ -212,17 +214,77 @@ __global__ __launch_bounds__(256, MINB) void k_gemm_pre(BigGemmArgs a, PreGrid p
 // v + 8). Each of the 8 waves owns 64 rows of X (two 32-row B tiles): 16 NJ
 // accumulator tiles of 32x32 per block, 10 per wave.
 //
-// W is read by all eight waves: it is staged in LDS, 64 k a stage (NJ x 4
-// KiB, the packed fragments copied as they are, so a 16-lane group's operand
-// read is 256 contiguous bytes), double-buffered through registers. X is read
-// by one wave only: it comes straight from the 32-row packed layout into the
-// B operands, one 1 KiB load per tile and 16-k step, four steps in flight.
+// W is read by all eight waves: it goes from HBM straight into LDS (16-byte
+// load-to-LDS instructions, no registers), 64 k a stage, three stage buffers
+// with the loads two stages ahead; the packed fragments are copied as they
+// are, so a 16-lane group's operand read is 256 contiguous bytes. X is read by
+// one wave only: it comes straight from the 32-row packed layout into the B
+// operands, one 1 KiB load per tile and 16-k step, six steps in flight.
+//
+// Loads complete in issue order as far as the wait counter is concerned, so
+// waiting for an X load also waits for every W load issued before it: the W
+// loads of a stage go out right after the first X refill of the stage two
+// before, which gives them seven steps. Every stage issues the same loads
+// (zero-fill offsets past the matrix), so one wait count before each barrier
+// is exact, and the barrier is a bare s_barrier: a block-wide fence would
+// wait for every load in flight, the X ring included.
 // ---------------------------------------------------------------------------
+
+// s_waitcnt immediate (gfx9 encoding) that waits until at most n vector
+// memory loads are outstanding and leaves the other counters alone
+constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+// A-operand reads of the SwiGLU kernel, issued as plain LDS reads the
+// compiler does not track: it cannot always prove that a read of the current
+// stage misses the buffer the load-to-LDS instructions are filling, and then
+// waits for every load in flight before the read. lds_wait<N> waits until at
+// most N LDS operations are outstanding (they complete in order; anything
+// else outstanding only makes the wait stricter) and passes the operand
+// through, so the products that use it cannot move above the wait.
+// (These and the load-to-LDS builtin below are compiled in the device pass
+// only: in the host pass they keep the kernel's launch stub from being
+// emitted, without an error.)
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+template <int OFF> __device__ inline v4u lds_read16(uint32_t addr) {
+  v4u r = {0u, 0u, 0u, 0u};
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF) : "memory");
+#endif
+  return r;
+}
+template <int N> __device__ inline void lds_wait(v4u &r) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(r) : "i"(N) : "memory");
+#endif
+}
+// 16-byte load from a buffer resource straight into LDS: the wave's 64 lanes
+// write their 16 bytes contiguously from the wave-uniform address `lds`; an
+// offset past the resource writes zeros and fetches nothing
+__device__ inline void bload16_lds(rsrc_t r, void *lds, uint32_t off) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)lds, 16, off,
+                                           0, 0, kPolicyNT);
+#endif
+}
+__device__ inline uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+__device__ inline f32x16 mma32v(v4u a, const uint4 &b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+template <int I, int N, typename F> __device__ inline void static_for(F &&f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
 template <int NJ>
 __global__ __launch_bounds__(512, 1) void k_gemm_ffn(BigGemmArgs a) {
-  constexpr int D = 4;               // X ring: one stage of 16-k steps
-  constexpr int WCH = NJ * 256;      // 16-byte W chunks a stage
-  constexpr int WPT = (WCH + 511) / 512;
+  constexpr int D = 6;                       // X ring: 16-k steps in flight
+  constexpr int WPT = (NJ * 256 + 511) / 512;  // 16-byte W chunks per thread and stage
+  constexpr int WSTAGE = WPT * 512;          // chunks a stage buffer holds
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r32 = lane & 31, hi = lane >> 5;
   const int64_t gate_tiles = a.up_tile_off;
@@ -234,33 +296,29 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ffn(BigGemmArgs a) {
   const rsrc_t xr = make_rsrc(a.X, (uint32_t)(a.x_rows * a.ldx * 2));
 
   // stage chunk c: A tile c >> 8, gate (0) or up (1) half (c >> 7) & 1, byte
-  // (c & 127) * 16 of the two fragments' 2 KiB; tiles past the FFN load zeros
-  __shared__ uint4 lw[2][WCH];
+  // (c & 127) * 16 of the two fragments' 2 KiB. Chunks past NJ * 256 (the
+  // stage is padded to whole rounds of 512) and tiles past the FFN load
+  // zeros, so every thread issues the same loads.
+  __shared__ uint4 lw0[WSTAGE], lw1[WSTAGE], lw2[WSTAGE];
   uint32_t woff[WPT];
   bool wval[WPT];
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
     const int c = tid + 512 * i;
     const int64_t g = g0 + (c >> 8);
-    wval[i] = c < WCH && g < gate_tiles;
+    wval[i] = c < NJ * 256 && g < gate_tiles;
     const int64_t t = g + (((c >> 7) & 1) ? gate_tiles : 0);
     woff[i] = wval[i] ? (uint32_t)(t * KFr * 1024 + (c & 127) * 16) : 0u;
   }
-  uint4 ws[WPT];
-  auto wload = [&](int64_t st) {
+  // a wave's load-to-LDS writes its 64 lanes' 16 bytes contiguously from
+  // the wave-uniform address it is given
+  auto wload = [&](uint4 *buf, int64_t st) {
 #pragma unroll
     for (int i = 0; i < WPT; ++i) {
       const int c = tid + 512 * i;
-      // the second fragment of an odd last stage is past the matrix row
-      const bool in = wval[i] && 2 * st + ((c & 127) >> 6) < KFr;
-      ws[i] = bload16_stream(wr, in ? woff[i] + (uint32_t)(st * 2048) : kOOB);
-    }
-  };
-  auto wstore = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < WPT; ++i) {
-      const int c = tid + 512 * i;
-      if (c < WCH) lw[b][c] = ws[i];
+      // stages past the end, and the second fragment of an odd last stage
+      const bool in = wval[i] && st < nst && 2 * st + ((c & 127) >> 6) < KFr;
+      bload16_lds(wr, buf + 512 * i + 64 * wid, in ? woff[i] + (uint32_t)(st * 2048) : kOOB);
     }
   };
 
@@ -275,10 +333,9 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ffn(BigGemmArgs a) {
       xq[slot][u] = bload16(xr, in ? xbase + (uint32_t)((u * ldk + i) * 1024) : kOOB);
   };
   // A operand of step s of a stage, tile j: row r32 (gate rows 0-15, up rows
-  // 16-31), k = 16 (s % 2) + 8 hi .. + 8 of fragment s / 2
-  auto aidx = [&](int j, int s) {
-    return ((j * 2 + (r32 >> 4)) * 2 + (s >> 1)) * 64 + (2 * (s & 1) + hi) * 16 + (r32 & 15);
-  };
+  // 16-31), k = 16 (s % 2) + 8 hi .. + 8 of fragment s / 2; byte address
+  // lane part + j * 4096 + (s / 2) * 1024 + (s % 2) * 512 of the stage buffer
+  const uint32_t alane = (uint32_t)((r32 >> 4) * 2048 + hi * 256 + (r32 & 15) * 16);
 
   f32x16 acc[NJ][2];
 #pragma unroll
@@ -288,30 +345,60 @@ __global__ __launch_bounds__(512, 1) void k_gemm_ffn(BigGemmArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[j][u][v] = 0.f;
 
+  // loads issued after the W loads of stage st + 1 by the end of stage st:
+  // the last three X refills of stage st - 1, the first X refill and the W
+  // loads of stage st, its last three X refills (the prologue issues more
+  // after stage 1's, so the same count waits a little early there)
+  constexpr int kAfterW = 2 * 3 + 2 + WPT + 2 * 3;
+  wload(lw0, 0);
+  wload(lw1, 1);
 #pragma unroll
   for (int i = 0; i < D; ++i) xload(i, i);
-  wload(0);
-  wstore(0);
-  __syncthreads();
-  for (int64_t st = 0; st < nst; ++st) {
-    const int b = (int)(st & 1);
-    if (st + 1 < nst) wload(st + 1);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(WPT + 2 * D));
+  __builtin_amdgcn_s_barrier();
+
+  // stage st reads buffer st % 3; within a run of three stages starting at a
+  // multiple of three, its X slots are (4 u + s) % D
+  auto run = [&](auto uc, const uint4 *cur, uint4 *ahead, int64_t st) {
+    constexpr int u = decltype(uc)::value;
+    const uint32_t abase = lds_addr(cur) + alane;
+    static_for<0, 4>([&](auto sc) {
+      constexpr int s = decltype(sc)::value;
+      constexpr int slot = (4 * u + s) % D;
       if (active) {
-        uint4 af[NJ];
+        v4u af[NJ];
+        static_for<0, NJ>([&](auto jc) {
+          constexpr int j = decltype(jc)::value;
+          af[j] = lds_read16<j * 4096 + (s >> 1) * 1024 + (s & 1) * 512>(abase);
+        });
+        static_for<0, NJ>([&](auto jc) {
+          constexpr int j = decltype(jc)::value;
+          lds_wait<NJ - 1 - j>(af[j]);
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) af[j] = lw[b][aidx(j, s)];
-#pragma unroll
-        for (int j = 0; j < NJ; ++j)
-#pragma unroll
-          for (int u = 0; u < 2; ++u) acc[j][u] = mma32(af[j], xq[s][u], acc[j][u]);
+          for (int t = 0; t < 2; ++t) acc[j][t] = mma32v(af[j], xq[slot][t], acc[j][t]);
+          // each operand's products right behind its own wait
+          __builtin_amdgcn_sched_barrier(0);
+        });
       }
-      xload(s, st * 4 + s + D);
-    }
-    if (st + 1 < nst) wstore(b ^ 1);
-    __syncthreads();
+      xload(slot, st * 4 + s + D);
+      if (s == 0) wload(ahead, st + 2);
+    });
+    // stage st + 1's W is in LDS for every wave; this stage's reads are done
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kAfterW));
+    __builtin_amdgcn_s_barrier();
+  };
+  auto stage = [&](auto uc, int64_t st) {
+    constexpr int u = decltype(uc)::value;
+    run(uc, u == 0 ? lw0 : u == 1 ? lw1 : lw2, u == 0 ? lw2 : u == 1 ? lw0 : lw1, st);
+  };
+  int64_t st = 0;
+  for (; st + 3 <= nst; st += 3) {
+    stage(std::integral_constant<int, 0>{}, st);
+    stage(std::integral_constant<int, 1>{}, st + 1);
+    stage(std::integral_constant<int, 2>{}, st + 2);
   }
+  if (st < nst) stage(std::integral_constant<int, 0>{}, st);
+  if (st + 1 < nst) stage(std::integral_constant<int, 1>{}, st + 1);
   if (!active) return;
 
   // lane holds D[n = 8 (v / 4) + 4 hi + v % 4][row r32 of its B tile]: gate
