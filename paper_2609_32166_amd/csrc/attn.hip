@@ -468,8 +468,10 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
 // 32x32x16 products (K rows permuted so that each lane ends up with eight
 // consecutive keys of its query row per 16-key step, the B-operand layout of
 // the value product), the online softmax in fp32 with the reference-maximum
-// rescale of the verify kernel, then O^T += V^T P^T. Loads of the next tile
-// are in flight while the current one is multiplied. Each block writes one
+// rescale of the verify kernel, then O^T += V^T P^T. K and V tiles are staged
+// row-major as they sit in the cache; the V^T operand comes from transposing
+// LDS reads. Loads of the next tile are in flight while the current one is
+// multiplied. Each block writes one
 // partial per (row, head) for k_attn_combine.
 // ---------------------------------------------------------------------------
 
@@ -492,6 +494,18 @@ __device__ inline int score_key(int i) {
 }
 
 constexpr int kPreKeys = 64;  // keys per staged tile
+
+// Two transposing 64-bit LDS reads (gfx950 ds_read_b64_tr_b16), the first
+// giving elements 0-3 of the 16-byte operand, the second elements 4-7.
+typedef short v4s16 __attribute__((ext_vector_type(4)));
+__device__ inline uint4 lds_read_tr16x2(const char *p0, const char *p1) {
+  const v4s16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s16 *)(const_cast<char *>(p0)));
+  const v4s16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s16 *)(const_cast<char *>(p1)));
+  const uint2 x = __builtin_bit_cast(uint2, a), y = __builtin_bit_cast(uint2, b);
+  return make_uint4(x.x, x.y, y.x, y.y);
+}
 
 }  // namespace
 
@@ -538,66 +552,54 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
   const int k_hi = min(min(k_lo + a.chunk_keys, P + min(j0 + 32, a.M)), kend);
   const int ntiles = k_hi > k_lo ? (k_hi - k_lo + kPreKeys - 1) / kPreKeys : 0;
 
-  // staged tiles: keys [key][16-byte chunk ^ (key & 15)], values transposed
-  // [dim][chunk of 8 keys ^ ((dim / 2) & 7)]; both swizzles keep the 16
-  // lanes of an operand read on distinct banks. The value rows of the cache
-  // are [slot][dim]: a thread loads the 16-byte pieces (8 dimensions) of a
-  // pair of consecutive keys and writes them into the transposed tile as
-  // 32-bit words (one word = the pair's two keys at one dimension).
+  // staged tiles, keys and values alike: [key][16-byte chunk ^ (key & 15)]
+  // (row-major as in the cache, the swizzle keeps the lanes of an operand
+  // read on distinct banks). Keys or values at or past the cache end load as
+  // zeros (out of range), so a zero probability never meets an
+  // uninitialised NaN.
+  static_assert(kPreKeys * HD / 8 == 4 * nthr, "four 16-byte chunks of K and of V per thread");
   __shared__ uint4 lk[2][kPreKeys][HD / 8];
-  __shared__ uint4 lv[2][HD][kPreKeys / 8];
-  constexpr int kPairs = kPreKeys / 2 * (HD / 8);  // (key pair, dimension group) items
+  __shared__ uint4 lv[2][kPreKeys][HD / 8];
   uint4 gk[4], gv[4];
   auto gload = [&](int kt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int idx = tid + r * nthr;
-      const bool in = idx < kPreKeys * HD / 8;
       const int key = kt + (idx >> 4), c = idx & 15;
-      gk[r] = bload16(kr, in && key < kend ? (uint32_t)(((int64_t)key * HD + c * 8) * 2) : kOOB);
-    }
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int it = tid + r * nthr;  // item: key pair it % (kPreKeys / 2), dims 8 * (it / ...)
-      const bool in = it < kPairs;
-      const int kp = it % (kPreKeys / 2), dgp = it / (kPreKeys / 2);
-      const int k2 = kt + 2 * kp;
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-        gv[2 * r + u] = bload16(vr, in && k2 + u < kend
-                                       ? (uint32_t)(((int64_t)(k2 + u) * HD + dgp * 8) * 2)
-                                       : kOOB);
+      const uint32_t off = key < kend ? (uint32_t)(((int64_t)key * HD + c * 8) * 2) : kOOB;
+      gk[r] = bload16(kr, off);
+      gv[r] = bload16(vr, off);
     }
   };
   auto lstore = [&](int buf, int kt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int idx = tid + r * nthr;
-      if (idx < kPreKeys * HD / 8) {
-        const int key = idx >> 4, c = idx & 15;
-        lk[buf][key][c ^ (key & 15)] = gk[r];
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int it = tid + r * nthr;
-      if (it < kPairs) {
-        const int kp = it % (kPreKeys / 2), dgp = it / (kPreKeys / 2);
-        // keys at or past the cache end load as zeros (out of range), so a
-        // zero probability never meets an uninitialised NaN
-        const uint4 v0 = gv[2 * r], v1 = gv[2 * r + 1];
-        const uint32_t x0[4] = {v0.x, v0.y, v0.z, v0.w}, x1[4] = {v1.x, v1.y, v1.z, v1.w};
-        const int c8 = kp >> 2, wsel = kp & 3;  // 8-key chunk and word of the pair
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int d = dgp * 8 + e;
-          const uint32_t lo = (x0[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-          const uint32_t hi = (x1[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-          ((uint32_t *)&lv[buf][d][c8 ^ ((d >> 1) & 7)])[wsel] = lo | (hi << 16);
-        }
-      }
+      const int key = idx >> 4, c = idx & 15;
+      lk[buf][key][c ^ (key & 15)] = gk[r];
+      lv[buf][key][c ^ (key & 15)] = gv[r];
     }
   };
+  // The value product needs V^T: lane l of the A operand holds dimension
+  // d = 32 dt + l % 32 of eight consecutive keys. Two transposing LDS reads
+  // give them (gfx950: within a group of 16 lanes, the lanes' four 16-bit
+  // elements are concatenated, A[4 s + e], and lane i receives A[i + 16 j],
+  // j = 0..3). Source lane s of group G points at key kb + s / 4, dimensions
+  // d0 + 4 (s % 4) .. + 3 with d0 = 32 dt + 16 (G % 2), kb = the step's first
+  // key + 8 (G / 2) (+ 4 for the second read), so lane i receives dimension
+  // d0 + i of keys kb .. kb + 3. voff: byte offsets within a 16-key step.
+  uint32_t voff[HD / 32][2];
+  {
+    const int s16 = lane & 15, G = lane >> 4;
+#pragma unroll
+    for (int dt = 0; dt < HD / 32; ++dt)
+#pragma unroll
+      for (int rr = 0; rr < 2; ++rr) {
+        const int kl = 8 * (G >> 1) + 4 * rr + (s16 >> 2);  // key within the step (0..15)
+        const int chunk = (4 * dt + 2 * (G & 1) + ((s16 & 3) >> 1)) ^ kl;
+        voff[dt][rr] = (uint32_t)(kl * HD * 2 + chunk * 16 + (s16 & 1) * 8);
+      }
+  }
 
   float m_run = -INFINITY, l_run = 0.f;
   f32x16 o[HD / 32];
@@ -678,8 +680,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
       for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int dt = 0; dt < HD / 32; ++dt) {
-          const int d = 32 * dt + r32, c = 4 * st + 2 * s2 + hh;
-          const uint4 vv = lv[buf][d][c ^ ((d >> 1) & 7)];
+          const char *step = (const char *)&lv[buf][32 * st + 16 * s2][0];
+          const uint4 vv = lds_read_tr16x2(step + voff[dt][0], step + voff[dt][1]);
           o[dt] = mma32(vv, pb[st][s2], o[dt]);
           o[dt] = mma32(vv, pl[st][s2], o[dt]);
         }
