@@ -712,20 +712,83 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnArgs a) {
   }
 }
 
+// Merge the key-range partials of the prefill attention: few ranges (at most
+// kPrefillMaxSplits) and many (row, head) pairs, so a half-wave takes one
+// pair. Lane c holds dimensions 4c .. 4c + 3; every lane reads the ranges'
+// (max, sum) itself (the same addresses across the half-wave) and adds the
+// weighted outputs in range order, so the result does not depend on timing.
+constexpr int kPrefillMaxSplits = 8;
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_combine_rows(AttnArgs a) {
+  constexpr int LPP = HD / 4;     // lanes per (row, head) pair
+  constexpr int PPB = 256 / LPP;  // pairs per block
+  const int nh = a.n_kv * a.group;
+  const int pair = blockIdx.x * PPB + (int)threadIdx.x / LPP, c4 = threadIdx.x % LPP;
+  if (pair >= a.M * nh) return;
+  const int j = pair / nh, h = pair % nh;
+  const int ns = a.n_splits;
+  const int P = *a.kv_len;
+  // ranges past the used ones hold stale data: skipped
+  const int used = min(ns, (P + a.M + a.chunk_keys - 1) / a.chunk_keys);
+  const float *pml = a.part_ml + ((int64_t)h * ns * a.rowpad + j) * 2;
+  const float *po = a.part_o + ((int64_t)h * ns * a.rowpad + j) * HD + 4 * c4;
+  float4 v[kPrefillMaxSplits];
+  float m[kPrefillMaxSplits], l[kPrefillMaxSplits];
+#pragma unroll
+  for (int sp = 0; sp < kPrefillMaxSplits; ++sp) {
+    if (sp < used) {
+      v[sp] = *(const float4 *)(po + (int64_t)sp * a.rowpad * HD);
+      m[sp] = pml[(int64_t)sp * a.rowpad * 2];
+      l[sp] = pml[(int64_t)sp * a.rowpad * 2 + 1];
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int sp = 0; sp < kPrefillMaxSplits; ++sp)
+    if (sp < used) mx = fmaxf(mx, m[sp]);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float den = 0.f;
+#pragma unroll
+  for (int sp = 0; sp < kPrefillMaxSplits; ++sp) {
+    if (sp < used) {
+      const float w = m[sp] == -INFINITY ? 0.f : exp2f(m[sp] - mx);
+      den += w * l[sp];
+      acc.x += w * v[sp].x;
+      acc.y += w * v[sp].y;
+      acc.z += w * v[sp].z;
+      acc.w += w * v[sp].w;
+    }
+  }
+  const float r[4] = {acc.x / den, acc.y / den, acc.z / den, acc.w / den};
+  bf16_t *out = (bf16_t *)a.out;
+  const int64_t k = (int64_t)h * HD + 4 * c4;
+  if (a.out_packed) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) Elem<bf16_t>::store(out, act_off<bf16_t>(j, k + i, a.ldout), r[i]);
+  } else {
+    uint2 pk;
+    pk.x = (uint32_t)f32_to_bf16(r[0]) | ((uint32_t)f32_to_bf16(r[1]) << 16);
+    pk.y = (uint32_t)f32_to_bf16(r[2]) | ((uint32_t)f32_to_bf16(r[3]) << 16);
+    *(uint2 *)(out + (int64_t)j * a.ldout + k) = pk;
+  }
+}
+
 bool attn_prefill_supported(bool bf16, int head_dim, int group) {
   return bf16 && head_dim == 128 && group >= 4 && group <= 8;
 }
 
 hipError_t launch_attn_prefill(const AttnArgs &a, hipStream_t s) {
   if (!attn_prefill_supported(true, a.head_dim, a.group) || a.chunk_keys % kPreKeys != 0 ||
-      a.M < 1 || a.plane * 2 >= (int64_t)1 << 31)
+      a.M < 1 || a.plane * 2 >= (int64_t)1 << 31 || a.n_splits < 1 ||
+      a.n_splits > kPrefillMaxSplits || (!a.out_packed && a.ldout % 4 != 0))
     return hipErrorInvalidValue;
   const int rtiles = (a.M + 31) / 32;
   const int npairs = a.n_kv * a.n_splits;
   const int nsub = (a.group + 3) / 4;
   dim3 grid(8 * ((npairs + 7) / 8) * rtiles * nsub);
   PF_TRY(launch_k(k_attn_prefill, grid, dim3(256), s, a));
-  PF_TRY(launch_k(k_attn_combine<bf16_t, 128>, dim3(a.M, a.n_kv * a.group), 256, s, a));
+  const int pairs = a.M * a.n_kv * a.group;
+  PF_TRY(launch_k(k_attn_combine_rows<128>, dim3((pairs + 7) / 8), 256, s, a));
   return hipGetLastError();
 }
 
