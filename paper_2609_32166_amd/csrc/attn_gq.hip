@@ -4,9 +4,10 @@
 // group's query heads share one copy of each K/V chunk. A chunk (32 keys:
 // 8 KiB of keys, 8 KiB of values, both [slot][head_dim] rows in the cache) is
 // loaded once per block by all 256 threads into registers a phase ahead,
-// stored into LDS (values transposed on the way, so the value product reads
-// eight consecutive keys of one dimension per lane), and read from there by
-// the four waves, each of which holds one 16-row tile of virtual rows. Per
+// stored into LDS row-major as in the cache, and read from there by the four
+// waves, each of which holds one 16-row tile of virtual rows (the value
+// product's operand, eight keys of one dimension per lane, through
+// transposing LDS reads). Per
 // wave and chunk: S^T = K Q^T with the permuted key rows, the log2-domain
 // online softmax with the deferred rescale, then O^T += V^T P^T, two chunks
 // per phase. The probabilities enter the value product as two bf16 terms
@@ -28,17 +29,13 @@ constexpr int GQ_HD = 128;
 constexpr int GQ_KC = 32;                          // keys per chunk
 // Staged keys: [key] rows of 256 bytes padded to 272, so the 16 consecutive
 // keys one operand read touches start on 16 distinct 16-byte bank groups.
-// Staged values: [dim] rows of the chunk's 32 keys (80 bytes with padding, so
-// the 16 dimensions of a read fall on distinct bank groups), keys permuted
-// within the row to match the score layout: key k = 16a + 4c + b sits at
-// position 8c + 4a + b, so lane quarter c finds the eight keys its
-// probabilities belong to (4c..4c+3 and 16+4c..16+4c+3) in one 16-byte read.
+// Staged values: [key] rows padded to 288 bytes, so the four keys x 32 bytes
+// one 16-lane group of a transposing read touches fall on distinct banks.
 constexpr int GQ_KROW = GQ_HD * 2 + 16;            // 272
-constexpr int GQ_VROW = GQ_KC * 2 + 16;            // 80
+constexpr int GQ_VROW = GQ_HD * 2 + 32;            // 288: value rows [key][dim], padded
 constexpr int GQ_KBYTES = GQ_KC * GQ_KROW;         // 8704
-constexpr int GQ_STAGE = GQ_KBYTES + GQ_HD * GQ_VROW;  // 18944
+constexpr int GQ_STAGE = GQ_KBYTES + GQ_KC * GQ_VROW;  // 17920
 constexpr int GQ_CHUNK_BYTES = GQ_KC * GQ_HD * 2;  // 8192 bytes of one plane per chunk
-__device__ constexpr int gq_vpos(int k) { return ((k >> 2) & 3) * 8 + (k >> 4) * 4 + (k & 3); }
 
 __device__ inline uint4 pack8_bf16(const float *p) {
   typedef float f2 __attribute__((ext_vector_type(2)));
@@ -50,6 +47,19 @@ __device__ inline uint4 pack8_bf16(const float *p) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// Value operand from two transposing 64-bit LDS reads (gfx950
+// ds_read_b64_tr_b16: within a group of 16 lanes the lanes' four 16-bit
+// elements are concatenated, A[4 s + e], and lane i receives A[i + 16 j]),
+// elements 0-3 from the first address, 4-7 from the second.
+typedef short gq_v4s __attribute__((ext_vector_type(4)));
+__device__ inline uint4 gq_read_tr(const unsigned char *p0, const unsigned char *p1) {
+  const gq_v4s a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) gq_v4s *)(const_cast<unsigned char *>(p0)));
+  const gq_v4s b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) gq_v4s *)(const_cast<unsigned char *>(p1)));
+  const uint2 x = __builtin_bit_cast(uint2, a), y = __builtin_bit_cast(uint2, b);
+  return make_uint4(x.x, x.y, y.x, y.y);
+}
 __device__ __forceinline__ float gq_row_max4(float x) {
   auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
@@ -105,7 +115,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
   uint4 pr[2][4];  // the next phase's two chunks in flight
   const int kp = tid & 15, dg = tid >> 4;
   const uint32_t koff = (uint32_t)tid * 16u;
-  const uint32_t voff = (uint32_t)(2 * kp * GQ_HD + dg * E) * 2u;
+  const uint32_t voff = koff;
   auto issue_k = [&](uint4 *r4, int c) {
     const uint32_t so = (uint32_t)c * GQ_CHUNK_BYTES;
     r4[0] = gq_load(kr_, koff + so);
@@ -114,7 +124,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
   auto issue_v = [&](rsrc_t vr, uint4 *r4, int c) {
     const uint32_t so = (uint32_t)c * GQ_CHUNK_BYTES;
     r4[2] = gq_load(vr, voff + so);
-    r4[3] = gq_load(vr, voff + so + GQ_HD * 2u);
+    r4[3] = gq_load(vr, voff + so + 4096u);
   };
   {
     const rsrc_t vr0 = make_rsrc(vplane, (uint32_t)max(kb - k0, 0) * (GQ_HD * 2));
@@ -128,25 +138,22 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
   const rsrc_t vr_ = make_rsrc(vplane, (uint32_t)max(min(kb, kend) - k0, 0) * (GQ_HD * 2));
 
   const int kst = (tid >> 4) * GQ_KROW + (tid & 15) * 16;
-  const int vst = GQ_KBYTES + 8 * dg * GQ_VROW + gq_vpos(2 * kp) * 2;
+  const int vst = GQ_KBYTES + (tid >> 4) * GQ_VROW + (tid & 15) * 16;
   const int r = lane & 15;
   const int kld = r * GQ_KROW + q * 16;
-  const int vld = GQ_KBYTES + r * GQ_VROW + q * 16;
+  // value operand of lane quarter q: the probabilities' keys 4q..4q+3 and
+  // 16+4q..16+4q+3 of the chunk (the score layout). Transposing reads: source
+  // lane s of quarter q points at key 4q + s / 4 (+16 for the second read),
+  // dims 16u + 4 (s % 4) .. + 3, so lane i receives dim 16u + i of the four
+  // keys
+  const int vld = GQ_KBYTES + (4 * q + (r >> 2)) * GQ_VROW + 8 * (r & 3);
   // chunk i (0, 1) of stage sg
   auto stash = [&](const uint4 *r4, int sg, int i, int zero_from) {
     unsigned char *st = lds + sg * PH + i * GQ_STAGE;
     *(uint4 *)(st + kst) = r4[0];
     *(uint4 *)(st + kst + 16 * GQ_KROW) = r4[1];
-    const uint4 a0 = 2 * kp < zero_from ? r4[2] : make_uint4(0, 0, 0, 0);
-    const uint4 a1 = 2 * kp + 1 < zero_from ? r4[3] : make_uint4(0, 0, 0, 0);
-    const uint32_t x0[4] = {a0.x, a0.y, a0.z, a0.w};
-    const uint32_t x1[4] = {a1.x, a1.y, a1.z, a1.w};
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const uint32_t w = (e & 1) ? __builtin_amdgcn_perm(x1[e >> 1], x0[e >> 1], 0x07060302u)
-                                 : __builtin_amdgcn_perm(x1[e >> 1], x0[e >> 1], 0x05040100u);
-      *(uint32_t *)(st + vst + e * GQ_VROW) = w;
-    }
+    *(uint4 *)(st + vst) = (tid >> 4) < zero_from ? r4[2] : make_uint4(0, 0, 0, 0);
+    *(uint4 *)(st + vst + 16 * GQ_VROW) = (tid >> 4) + 16 < zero_from ? r4[3] : make_uint4(0, 0, 0, 0);
   };
 
   // query fragments and visibility of the wave's 16 virtual rows
@@ -212,7 +219,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_gq(AttnArgs a, int row_groups) 
     const unsigned char *st = lds + sg * PH + i * GQ_STAGE + vld;
     uint4 vf[NDT];
 #pragma unroll
-    for (int u = 0; u < NDT; ++u) vf[u] = *(const uint4 *)(st + u * 16 * GQ_VROW);
+    for (int u = 0; u < NDT; ++u) vf[u] = gq_read_tr(st + 32 * u, st + 32 * u + 16 * GQ_VROW);
     const uint4 phi = pack8_bf16(p);
     uint4 plo = make_uint4(0, 0, 0, 0);
     if (HILO) {
