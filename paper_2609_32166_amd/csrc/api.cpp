@@ -144,7 +144,7 @@ void model_free(pf_model *m) {
   if (!m) return;
   prefill_free(m);
   void *ptrs[] = {m->wqkv, m->wo, m->wgu, m->wd, m->lm, m->embed, m->attn_norm, m->ffn_norm,
-                  m->final_norm, m->inv_freq, m->x, m->xn, m->qb, m->attn, m->act, m->part,
+                  m->final_norm, m->inv_freq, m->x, m->xn, m->ssq, m->qb, m->attn, m->act, m->part,
                   m->apart_o, m->apart_ml, m->amax, m->rope, m->rowinfo, m->pred, m->flags};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
@@ -805,6 +805,7 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
   m->amax_elems = ((m->plm.NT + 3) / 4) * kRowPad;
   ALLOC(m->x, kRowPad * H * 4);
   ALLOC(m->xn, kRowPad * Hp * m->esz);
+  ALLOC(m->ssq, (int64_t)kRowPad * kMaxNormSlices * 4);
   ALLOC(m->qb, kRowPad * q * m->esz);
   ALLOC(m->attn, kRowPad * qp * m->esz);
   ALLOC(m->act, kRowPad * Fp * m->esz);
@@ -821,10 +822,10 @@ pf_status pf_model_create(const pf_model_config *cfg, const pf_model_weights *w,
 
   hipStream_t hs = st(s);
   hipError_t e = hipSuccess;
-  void *zero[] = {m->x, m->xn, m->qb, m->attn, m->act};
+  void *zero[] = {m->x, m->xn, m->qb, m->attn, m->act, m->ssq};
   int64_t zb[] = {kRowPad * H * 4, kRowPad * Hp * m->esz, kRowPad * q * m->esz,
-                  kRowPad * qp * m->esz, kRowPad * Fp * m->esz};
-  for (int i = 0; i < 5 && e == hipSuccess; ++i) e = hipMemsetAsync(zero[i], 0, zb[i], hs);
+                  kRowPad * qp * m->esz, kRowPad * Fp * m->esz, (int64_t)kRowPad * kMaxNormSlices * 4};
+  for (int i = 0; i < 6 && e == hipSuccess; ++i) e = hipMemsetAsync(zero[i], 0, zb[i], hs);
   if (e == hipSuccess) e = launch_pack(w->wqkv, q + 2 * kv, H, L, (q + 2 * kv) * H, bf, m->pqkv, m->wqkv, hs,
                                            c.head_dim);
   if (e == hipSuccess) e = launch_pack(w->wo, H, q, L, H * q, bf, m->po, m->wo, hs);
@@ -1026,8 +1027,13 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
   sa.rowmask = rowmask;
   sa.rope = m->rope;
   PROF(0, launch_prep(sa, hs));
+  // the norms inside the layer stack leave their scale to the next projection
+  // (x * gain in xn, sums of squares in ssq); the final norm, whose rows are
+  // also read by the retrieval keys, writes normalised rows
+  const int nss = norm_slices(H);
+  RowScale rsc{m->ssq, nss, H, eps};
   PROF(0, launch_embed_norm(bf, m->embed, m->rowinfo, M, H, m->attn_norm, eps, m->x, m->xn, Hp,
-                            true, hs));
+                            true, m->ssq, hs));
   if (resid && only_kind < 0) HIPCHK(launch_copy_rows(m->x, M, H, resid, hs));
 
   // attention geometry: key ranges over P + rows keys (P <= host bound)
@@ -1050,6 +1056,8 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     qa.KFr = m->pqkv.KFr;
     qa.X = m->xn;
     qa.ldx = Hp;
+    qa.rs = rsc;
+    if (l == 0) qa.rs.nss = 1;  // the embedding norm's one sum per row
     qa.M = M;
     qa.nq = nq;
     qa.nkv = nkv;
@@ -1102,8 +1110,8 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     go.out = m->part;
     go.ldo = H;
     PROF(4, launch_gemm(bf, EPI_PARTIAL, MT, go, m->wave_slots / 4, hs));
-    PROF(5, launch_residual_norm(bf, m->part, go.splits, kRowPad, M, H, H, m->ffn_norm + (int64_t)l * H, eps,
-                                m->x, m->xn, Hp, true, hs));
+    PROF(5, launch_residual_norm_deferred(bf, m->part, go.splits, kRowPad, M, H, H,
+                                         m->ffn_norm + (int64_t)l * H, m->x, m->xn, Hp, m->ssq, hs));
     // gate/up + SwiGLU
     GemmArgs gg{};
     gg.W = (const char *)m->wgu + (int64_t)l * m->pgu.bytes();
@@ -1117,6 +1125,7 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     gg.act = m->act;
     gg.ldact = Fp;
     gg.up_tile_off = F / 16;
+    gg.rs = rsc;
     PROF(6, launch_gemm(bf, EPI_SWIGLU, MT, gg, m->wave_slots / 4, hs));
     // down projection + residual + next norm
     GemmArgs gd{};
@@ -1131,9 +1140,13 @@ static pf_status verify_impl(pf_model *m, pf_kv_cache *kv, const pf_draft *draft
     gd.out = m->part;
     gd.ldo = H;
     PROF(7, launch_gemm(bf, EPI_PARTIAL, MT, gd, m->wave_slots / 4, hs));
-    const float *next_gain = l + 1 < L ? m->attn_norm + (int64_t)(l + 1) * H : m->final_norm;
-    PROF(5, launch_residual_norm(bf, m->part, gd.splits, kRowPad, M, H, H, next_gain, eps, m->x, m->xn, Hp,
-                                true, hs));
+    if (l + 1 < L)
+      PROF(5, launch_residual_norm_deferred(bf, m->part, gd.splits, kRowPad, M, H, H,
+                                           m->attn_norm + (int64_t)(l + 1) * H, m->x, m->xn, Hp,
+                                           m->ssq, hs));
+    else
+      PROF(5, launch_residual_norm(bf, m->part, gd.splits, kRowPad, M, H, H, m->final_norm, eps,
+                                  m->x, m->xn, Hp, true, hs));
     if (resid && only_kind < 0)
       HIPCHK(launch_copy_rows(m->x, M, H, resid + (int64_t)(l + 1) * M * H, hs));
   }
@@ -1435,7 +1448,7 @@ pf_status pf_prefill(pf_model *m, pf_kv_cache *kv, const int32_t *tokens, int32_
     HIPCHK(launch_prefill_rows(tokens + c0, rows, (int)V, kv->len, m->inv_freq, hd, m->pre_rowinfo,
                                m->pre_rope, m->pre_status, hs));
     HIPCHK(launch_embed_norm(bf, m->embed, m->pre_rowinfo, rows, H, m->attn_norm, eps, m->pre_x,
-                             m->pre_xn, Hp, false, hs));
+                             m->pre_xn, Hp, false, nullptr, hs));
     const int64_t keys_max = kv->host_bound + c0 + rows;
     // key ranges: the staged kernel takes enough of them for about two of
     // its blocks per CU; the other path a fixed 8

@@ -147,7 +147,6 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT, NP>::MinBlocks)) void k_gem
   for (int m = 0; m < MT; ++m)
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   // ring of kU fragment slots: compute slot u, then refill it with the
   // fragment kU positions ahead. Loads past the wave's range go out of the
   // buffer resource's bounds and return zeros without memory traffic, so the
@@ -162,11 +161,18 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT, NP>::MinBlocks)) void k_gem
     for (int m = 0; m < MT; ++m)
       xv[u][m] = bload16(xr, in && xbase[m] != kOOB ? xbase[m] + (uint32_t)(i * 1024) : kOOB);
   };
+  // SwiGLU: the rows' deferred RMSNorm scales (see RowInv)
+  __shared__ float invl[EPI == EPI_SWIGLU ? kRowPad : 1];
+  RowInv ri;
+  if (EPI == EPI_SWIGLU) ri.issue(a.rs, a.M);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     load(u, u);
     __builtin_amdgcn_sched_barrier(0);
   }
+  if (EPI == EPI_SWIGLU) ri.finish(a.rs, a.M, invl);
+  __builtin_amdgcn_sched_barrier(0);
   for (int64_t i = 0; i < n; i += kU) {
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
@@ -216,12 +222,13 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT, NP>::MinBlocks)) void k_gem
         const int row = m * 16 + (lane & 15);
         if (k % 4 != wid || row >= a.M || !tv[p]) continue;
         const f32x4 g = sum4(m, p), u = sum4(m, p + PR);
+        const float inv = invl[row];
         // act is the next GEMM's X: fragment-packed; the four columns stay in
         // one E-element chunk
         const int64_t col = tile[p] * 16 + 4 * q;
         T *dst = (T *)a.act + act_off<T>(row, col, a.ldact);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) Elem<T>::store(dst, i, silu(g[i]) * u[i]);
+        for (int i = 0; i < 4; ++i) Elem<T>::store(dst, i, silu(g[i] * inv) * (u[i] * inv));
       }
     }
     return;
@@ -352,6 +359,8 @@ static hipError_t launch_t(int mt, const GemmArgs &a, dim3 grid, hipStream_t s) 
 
 hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs &a, int cus, hipStream_t s) {
   if (epi == EPI_SWIGLU) {
+    if (!a.rs.ssq || a.rs.nss < 1 || a.rs.nss > kMaxNormSlices || a.M < 1 || a.M > kRowPad)
+      return hipErrorInvalidValue;
     const int np = gemm_swiglu_pairs(mt, a.up_tile_off, cus);
     const dim3 grid((unsigned)((a.up_tile_off + np - 1) / np), (unsigned)a.splits);
     if (np == 3) return bf16 ? launch_t<bf16_t, EPI_SWIGLU, 3>(mt, a, grid, s)

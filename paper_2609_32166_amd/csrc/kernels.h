@@ -65,6 +65,57 @@ __device__ inline uint4 bload16_stream(rsrc_t r, uint32_t off) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Deferred RMSNorm scale of the verify step. RMSNorm(x) W^T equals
+// inv(x) * ((x * gain) W^T) with inv(x) = 1 / sqrt(mean(x^2) + eps) one number
+// per row, so the norms inside the layer stack write x * gain (rounded to the
+// model dtype) as the next projection's operand, together with partial sums of
+// squares of x, one per slice of kNormSlice columns, at ssq[row * nss +
+// slice]; the projection adds a row's slices in slice order and multiplies
+// that row's sums by inv before its epilogue. The rounding to the model dtype
+// then comes before the per-row scale instead of after it. Spreading a row
+// over several norm blocks is what this buys: one block per row moved a whole
+// row of partials through a single compute unit.
+constexpr int kNormSlice = 512;     // columns per norm block (wider rows: more per block)
+constexpr int kMaxNormSlices = 8;
+struct RowScale {
+  const float *ssq;  // [rows][nss] partial sums of squares
+  int nss;           // slices per row (1..kMaxNormSlices)
+  int H;             // row length
+  float eps;
+};
+inline int norm_slices(int H) {
+  const int n = (H + kNormSlice - 1) / kNormSlice;
+  return n < kMaxNormSlices ? n : kMaxNormSlices;
+}
+
+// The block's rows' deferred scales into LDS (invl[row], rows < M): thread t
+// < M adds row t's slices in slice order. issue() goes before the product
+// loop's first loads and finish() right after them: these loads are then the
+// oldest in flight, so their wait costs nothing beyond the first products' own
+// wait, and the epilogue reads one LDS value per row after its barrier instead
+// of computing the scale once per output tile. Buffer loads: slices past nss
+// and rows past M read zeros, with no branch around a load.
+struct RowInv {
+  float v[kMaxNormSlices];
+  __device__ void issue(const RowScale &r, int M) {
+    const int t = (int)threadIdx.x;
+    const rsrc_t rr = make_rsrc(r.ssq, (uint32_t)(M * r.nss * 4));
+#pragma unroll
+    for (int g = 0; g < kMaxNormSlices; ++g)
+      v[g] = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(
+                     rr, t < M && g < r.nss ? (t * r.nss + g) * 4 : (int)kOOB, 0, 0));
+  }
+  __device__ void finish(const RowScale &r, int M, float *invl) const {
+    float ss = 0.f;
+#pragma unroll
+    for (int g = 0; g < kMaxNormSlices; ++g)
+      if (g < r.nss) ss += v[g];
+    const int t = (int)threadIdx.x;
+    if (t < M) invl[t] = 1.0f / sqrtf(ss / (float)r.H + r.eps);
+  }
+};
+
 enum GemmEpi { EPI_PARTIAL = 0, EPI_SWIGLU = 1, EPI_ARGMAX = 2 };
 
 struct GemmArgs {
@@ -79,10 +130,12 @@ struct GemmArgs {
   // EPI_PARTIAL: out[(split*kRowPad + m)*ldo + n]
   float *out;
   int64_t ldo;
-  // EPI_SWIGLU: act[m*ldact + n] = silu(gate)*up, gate tile t, up tile t + up_tile_off
+  // EPI_SWIGLU: act[m*ldact + n] = silu(inv*gate)*(inv*up), gate tile t, up tile
+  // t + up_tile_off, inv the row's deferred RMSNorm scale (X holds x * gain)
   void *act;
   int64_t ldact;
   int64_t up_tile_off;
+  RowScale rs;
   // EPI_ARGMAX: amax[blockIdx.x*kRowPad + m]; optional logits[m*ldlog + n]
   ArgmaxPart *amax;
   float *logits;
@@ -94,8 +147,9 @@ struct GemmArgs {
 struct QkvArgs {
   const void *W;        // packed fused QKV weights of one layer
   int64_t W_bytes, KFr;
-  const void *X;        // fragment-packed normalised rows
+  const void *X;        // fragment-packed rows x * gain (RMSNorm scale deferred)
   int64_t ldx;
+  RowScale rs;          // the rows' deferred RMSNorm scale, applied to the sums
   int M;                // valid rows
   int nq, nkv, hd;
   const float *rope;    // [kRowPad][hd/2][2] cos, sin of each row's position
@@ -172,9 +226,11 @@ struct StepArgs {
   float *rope;          // [kRowPad][hd/2][2]
 };
 hipError_t launch_prep(const StepArgs &a, hipStream_t s);
+// ssq null: xn = RMSNorm(x) * gain; otherwise xn = x * gain and ssq[row] the
+// row's sum of squares (the deferred scale, one slice per row)
 hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
                              const float *gain, float eps, float *x, void *xn, int64_t ldxn,
-                             int packed, hipStream_t s);
+                             int packed, float *ssq, hipStream_t s);
 hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int rowpad, int M, int nq,
                            int nkv, int hd, int64_t ldpart, const float *rope, const int32_t *kv_len,
                            void *qbuf, int64_t ldq, void *cache, int layer, int64_t cap,
@@ -184,6 +240,12 @@ hipError_t launch_qkv_post(bool bf16, const float *part, int splits, int rowpad,
 hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
                                 int64_t ldpart, const float *gain, float eps, float *x, void *xn,
                                 int64_t ldxn, int packed, hipStream_t s);
+// The same with the RMSNorm scale deferred (verify rows, xn fragment-packed):
+// x += partials, xn = x * gain elementwise, ssq[row * norm_slices(H) +
+// slice] = the slice's sum of squares of x; one block per (row, slice)
+hipError_t launch_residual_norm_deferred(bool bf16, const float *part, int splits, int rowpad, int M,
+                                         int H, int64_t ldpart, const float *gain, float *x,
+                                         void *xn, int64_t ldxn, float *ssq, hipStream_t s);
 // prefill rows: tokens[i] at position P + i (P = *kv_len), RoPE table, rowinfo
 hipError_t launch_prefill_rows(const int32_t *tokens, int n, int V, const int32_t *kv_len,
                                const double *inv_freq, int hd, int32_t *rowinfo, float *rope,

@@ -162,7 +162,9 @@ struct pf_model {
   double *inv_freq = nullptr;
   // step work buffers
   float *x = nullptr;        // [kRowPad][H] residual stream
-  void *xn = nullptr;        // [kRowPad][Kpad(H)] normalised activations
+  void *xn = nullptr;        // [kRowPad][Kpad(H)] normalised activations (inside the verify
+                             // layer stack: x * gain, the RMSNorm scale deferred)
+  float *ssq = nullptr;      // [kRowPad][nss] the deferred scale's partial sums of squares
   void *qb = nullptr;        // [kRowPad][q] queries after RoPE
   void *attn = nullptr;      // [kRowPad][Kpad(q)] attention output
   void *act = nullptr;       // [kRowPad][Kpad(F)] SwiGLU output

@@ -83,11 +83,18 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_qkv(QkvArgs a) {
     for (int m = 0; m < MT; ++m)
       xv[u][m] = bload16(xr, in && xbase[m] != kOOB ? xbase[m] + (uint32_t)(i * 1024) : kOOB);
   };
+  // the rows' deferred RMSNorm scales (see RowInv)
+  __shared__ float invl[kRowPad];
+  RowInv ri;
+  ri.issue(a.rs, a.M);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     load(u, u);
     __builtin_amdgcn_sched_barrier(0);
   }
+  ri.finish(a.rs, a.M, invl);
+  __builtin_amdgcn_sched_barrier(0);
   for (int64_t i = 0; i < n; i += kU) {
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
@@ -120,6 +127,9 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_qkv(QkvArgs a) {
         x += red[w][ei][xl][ec];
         y += red[w][ei][yl][ec];
       }
+      const float inv = invl[row];  // written before the loop, visible after the barrier
+      x *= inv;
+      y *= inv;
       const int64_t slot = P + row;
       if (kind == 2) {
         T *vp = (T *)a.cache + ((int64_t)(a.layer * 2 + 1) * a.nkv + (hh - a.nq - a.nkv)) * plane +
@@ -168,7 +178,9 @@ hipError_t launch_t(int mt, const QkvArgs &a, int cus, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm_qkv(bool bf16, int mt, const QkvArgs &a, int cus, hipStream_t s) {
-  if (a.hd % 32 != 0) return hipErrorInvalidValue;
+  if (a.hd % 32 != 0 || !a.rs.ssq || a.rs.nss < 1 || a.rs.nss > kMaxNormSlices || a.M < 1 ||
+      a.M > kRowPad)
+    return hipErrorInvalidValue;
   PF_TRY(bf16 ? launch_t<bf16_t>(mt, a, cus, s) : launch_t<float>(mt, a, cus, s));
   return hipGetLastError();
 }

@@ -89,28 +89,41 @@ __device__ void norm_row(const float *x, int H, const float *gain, float eps, T 
     Elem<T>::store(xn, xn_index<T>(packed, row, k, ldxn), x[k] * inv * gain[k]);
 }
 
+// ssq: the deferred form (xn = x * gain elementwise, ssq[row] = the row's sum
+// of squares); null: the normalised row
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed_norm(const T *embed, const int32_t *rowinfo, int H,
                                                     const float *gain, float eps, float *x, T *xn,
-                                                    int64_t ldxn, int packed) {
+                                                    int64_t ldxn, int packed, float *ssq) {
   const int m = blockIdx.x;
   const int tok = rowinfo[m * 4];
   float *xr = x + (int64_t)m * H;
   for (int k = threadIdx.x; k < H; k += 256) xr[k] = Elem<T>::load(embed, (int64_t)tok * H + k);
   __syncthreads();
-  norm_row<T>(xr, H, gain, eps, xn, m, ldxn, packed);
+  if (!ssq) {
+    norm_row<T>(xr, H, gain, eps, xn, m, ldxn, packed);
+    return;
+  }
+  __shared__ float sh[4];
+  float ss = 0.f;
+  for (int k = threadIdx.x; k < H; k += 256) {
+    ss += xr[k] * xr[k];
+    Elem<T>::store(xn, xn_index<T>(packed, m, k, ldxn), xr[k] * gain[k]);
+  }
+  ss = block_sum256(ss, sh);
+  if (threadIdx.x == 0) ssq[m] = ss;
 }
 
 hipError_t launch_embed_norm(bool bf16, const void *embed, const int32_t *rowinfo, int M, int H,
                              const float *gain, float eps, float *x, void *xn, int64_t ldxn,
-                             int packed, hipStream_t s) {
+                             int packed, float *ssq, hipStream_t s) {
   if (!bf16 && packed == 2) return hipErrorInvalidValue;
   if (bf16)
     PF_TRY(launch_k(k_embed_norm<bf16_t>, M, 256, s, (const bf16_t *)embed, rowinfo, H, gain, eps, x,
-                    (bf16_t *)xn, ldxn, packed));
+                    (bf16_t *)xn, ldxn, packed, ssq));
   else
     PF_TRY(launch_k(k_embed_norm<float>, M, 256, s, (const float *)embed, rowinfo, H, gain, eps, x,
-                    (float *)xn, ldxn, packed));
+                    (float *)xn, ldxn, packed, ssq));
   return hipGetLastError();
 }
 
@@ -259,6 +272,77 @@ __global__ __launch_bounds__(1024) void k_residual_norm_wide(const float *part, 
     if (c < H4) emit(c, keep[r], gk[r]);
   }
   for (int c = threadIdx.x + nt * kR; c < H4; c += nt) emit(c, xr[c], ((const float4 *)gain)[c]);
+}
+
+// x += sum of split-K partials (the same fixed order as above, so x is the
+// same), xn = x * gain elementwise in the verify GEMMs' packed layout, and
+// the slice's sum of squares of x for the next projection's deferred scale.
+// One block of 128 threads per (row, slice of norm_slices(H)), one
+// four-column chunk per thread up to kNormSlice columns a slice, with every
+// partial load in flight at once: a row's partials spread over several
+// compute units.
+template <typename T>
+__global__ __launch_bounds__(128) void k_residual_norm_deferred(const float *part, int splits, int rowpad,
+                                                                int H, int64_t ldpart,
+                                                                const float *gain, float *x, T *xn,
+                                                                int64_t ldxn, float *ssq) {
+  static_assert(kNormSlice == 4 * 128, "one four-column chunk per thread");
+  constexpr int kB = 8;
+  const int m = blockIdx.x, g = blockIdx.y, nss = gridDim.y;
+  const int H4 = H / 4, per = (H4 + nss - 1) / nss;
+  const int c1 = min(g * per + per, H4);
+  float ss = 0.f;
+  for (int c = g * per + (int)threadIdx.x; c < c1; c += 128) {
+    float4 *xr = (float4 *)(x + (int64_t)m * H);
+    const float4 gk = ((const float4 *)gain)[c];
+    float4 acc = xr[c];
+    float4 pv[kB];
+#pragma unroll
+    for (int u = 0; u < kB; ++u)
+      if (u < splits) pv[u] = ((const float4 *)(part + ((int64_t)u * rowpad + m) * ldpart))[c];
+#pragma unroll
+    for (int u = 0; u < kB; ++u) {
+      if (u < splits) {
+        acc.x += pv[u].x;
+        acc.y += pv[u].y;
+        acc.z += pv[u].z;
+        acc.w += pv[u].w;
+      }
+    }
+    for (int sp = kB; sp < splits; ++sp) {  // more splits than kB: one at a time
+      const float4 v = ((const float4 *)(part + ((int64_t)sp * rowpad + m) * ldpart))[c];
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    xr[c] = acc;
+    ss += acc.x * acc.x + acc.y * acc.y + acc.z * acc.z + acc.w * acc.w;
+    T *out = xn + xn_index<T>(1, m, 4 * c, ldxn);
+    Elem<T>::store(out, 0, acc.x * gk.x);
+    Elem<T>::store(out, 1, acc.y * gk.y);
+    Elem<T>::store(out, 2, acc.z * gk.z);
+    Elem<T>::store(out, 3, acc.w * gk.w);
+  }
+  __shared__ float sh[2];
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  if (threadIdx.x == 0) ssq[m * nss + g] = sh[0] + sh[1];
+}
+
+hipError_t launch_residual_norm_deferred(bool bf16, const float *part, int splits, int rowpad, int M,
+                                         int H, int64_t ldpart, const float *gain, float *x,
+                                         void *xn, int64_t ldxn, float *ssq, hipStream_t s) {
+  if (H % 4 != 0 || M < 1 || M > kRowPad || !ssq) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)M, (unsigned)norm_slices(H));
+  if (bf16)
+    PF_TRY(launch_k(k_residual_norm_deferred<bf16_t>, grid, 128, s, part, splits, rowpad, H, ldpart,
+                    gain, x, (bf16_t *)xn, ldxn, ssq));
+  else
+    PF_TRY(launch_k(k_residual_norm_deferred<float>, grid, 128, s, part, splits, rowpad, H, ldpart,
+                    gain, x, (float *)xn, ldxn, ssq));
+  return hipGetLastError();
 }
 
 hipError_t launch_residual_norm(bool bf16, const float *part, int splits, int rowpad, int M, int H,
