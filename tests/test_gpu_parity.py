@@ -386,6 +386,21 @@ def test_verify_bf16_ragged(pf, case):
     _compare_step(out, od, ores, wl.model, wl.prefix)
 
 
+# Rows wider than the verify norm's eight 512-column slices: 4160 columns are
+# eight slices of 520 (some threads take two four-column chunks), and the
+# final norm's wide form runs past its 1024 threads.
+WIDE = synth.ModelShape(2, 4160, 8, 2, 128, 1360, 4000, 1e6, 1e-6, "bf16")
+WIDE_WL = synth.Workload("wide", 12, WIDE, 300, 16, 4, False, 1, 16, 200, (64, 256), "zipf", 0)
+
+
+@pytest.mark.parametrize("case", range(2))
+def test_verify_bf16_wide_rows(pf, case):
+    wl = WIDE_WL
+    seed = synth.case_seed(wl, case)
+    out, od, ores, gpu, g = _verify_case(pf, wl, wl.model, seed, [None, 16][case])
+    _compare_step(out, od, ores, wl.model, wl.prefix)
+
+
 RAGGED_TREE = synth.Workload("ragged_tree", 8, RAGGED, 300, 16, 4, True, 4, 48, 200, (64, 256),
                              "zipf", 0)
 
