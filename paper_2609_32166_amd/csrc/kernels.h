@@ -66,8 +66,9 @@ __device__ inline uint4 bload16_stream(rsrc_t r, uint32_t off) {
 }
 
 // Deferred RMSNorm scale of the verify step. RMSNorm(x) W^T equals
-// inv(x) * ((x * gain) W^T) with inv(x) = 1 / sqrt(mean(x^2) + eps) one number
-// per row, so the norms inside the layer stack write x * gain (rounded to the
+// inv(x) * ((x * gain) W^T), the product with the gains elementwise and
+// inv(x) = 1 / sqrt(mean(x^2) + eps) one number per row, so the norms inside
+// the layer stack write x * gain (rounded to the
 // model dtype) as the next projection's operand, together with partial sums of
 // squares of x, one per slice of kNormSlice columns, at ssq[row * nss +
 // slice]; the projection adds a row's slices in slice order and multiplies
