@@ -164,14 +164,12 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT, NP>::MinBlocks)) void k_gem
   // SwiGLU: the rows' deferred RMSNorm scales (see RowInv)
   __shared__ float invl[EPI == EPI_SWIGLU ? kRowPad : 1];
   RowInv ri;
-  if (EPI == EPI_SWIGLU) ri.issue(a.rs, a.M);
-  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     load(u, u);
     __builtin_amdgcn_sched_barrier(0);
   }
-  if (EPI == EPI_SWIGLU) ri.finish(a.rs, a.M, invl);
+  if (EPI == EPI_SWIGLU) ri.issue(a.rs, a.M);
   __builtin_amdgcn_sched_barrier(0);
   for (int64_t i = 0; i < n; i += kU) {
 #pragma unroll
@@ -197,6 +195,7 @@ __global__ __launch_bounds__(256, (EpiTiles<EPI, MT, NP>::MinBlocks)) void k_gem
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int j = 0; j < NT; ++j) red[wid][m][j][lane] = acc[m][j];
+    if (EPI == EPI_SWIGLU) ri.finish(a.rs, a.M, invl);
     __syncthreads();
     auto sum4 = [&](int m, int j) {
       f32x4 v = red[0][m][j][lane];
